@@ -1,0 +1,180 @@
+"""Benchmark: batched paged graph beam search on one MI355X.
+
+One step = one gorio_search over the whole query batch of the workload (all
+steps of the search path).  Default workload: 1,000,000 x 128-d uint8 vectors,
+R = 64, 388-B records, 10 per 4 KB page, 10,000 queries, k = 10, L = 64, W = 4,
+every page resident in HBM.
+
+Prints one JSON line.  `value` is queries per second over the timed steps
+(inputs already resident in HBM).  `roofline` prices the search kernel's
+algorithmic bytes (expansions x (4 + 4R) + first-time evaluations x vector
+bytes) against its average duration, measured with HIP events on the launch
+stream.  `cpu_baseline` times the CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+from pathlib import Path
+
+import numpy as np
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+METRIC = "queries/sec at k=10 (oracle-exact) + achieved HBM GB/s and miss-service GB/s"
+HBM_PEAK_GBS = 8000.0
+PROFILES = ROOT / "profiles"
+KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp",
+                  "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update((ROOT / p).read_bytes())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    f = PROFILES / f"traffic_{workload}.json"
+    if not f.exists():
+        return None
+    try:
+        t = json.loads(f.read_text())
+    except ValueError:
+        return None
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(a, q, w, gpu_ids, gpu_dists, sample_nq: int, threads: int):
+    """Time the CPU oracle on the first `sample_nq` queries with `threads` threads
+    on disjoint shards; also check the GPU answers on that sample."""
+    from oracle import load
+    orc = load()
+    packed = orc.pack(a["x"], a["graph"])
+    entry = orc.medoid(a["x"])
+    qs = q[:sample_nq]
+    t0 = time.perf_counter()
+    oids, od, oc, _ = packed.search(qs, w.k, w.L, w.W, entry, threads=threads)
+    dt = time.perf_counter() - t0
+    exact = bool(np.array_equal(oids, gpu_ids[:sample_nq]) and np.array_equal(od, gpu_dists[:sample_nq]))
+    return {
+        "value": round(sample_nq / dt, 1), "unit": "queries/s", "cores": threads, "kind": "oracle",
+        "sample": f"first {sample_nq} of {len(q)} queries of the same workload, "
+                  f"{threads} threads on disjoint query shards, {dt:.2f} s wall",
+    }, exact, entry
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="u8-1m-hbm")
+    ap.add_argument("--cpu-sample", type=int, default=10000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
+              "the search shards by query across GPUs but no multi-GPU path is built.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_04415_amd as g
+    from workload import WORKLOADS, index_arrays, query_array
+
+    if not g.LIB_PATH.exists():
+        raise SystemExit("libgorio.so is not built: run python __graft_entry__.py build")
+    torch.cuda.set_device(0)
+    w = WORKLOADS[args.workload]
+    log(f"[bench] workload {w.name}: {w.description}")
+    t0 = time.perf_counter()
+    a = index_arrays(w.index)
+    q = query_array(w.index, w.queries)
+    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f} s")
+    ix = g.Index(a["x"], a["graph"])
+    info = ix.info
+    if w.cache_frac < 1.0:
+        ix.set_cache(int(w.cache_frac * info["index_bytes"]))
+        ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
+    qd = torch.from_numpy(q).cuda()
+    nq = len(q)
+    ids = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
+    dists = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    for _ in range(args.warmup):
+        ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
+    torch.cuda.synchronize()
+    kernel_ms, stats = [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st = ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
+        kernel_ms.append(st["kernel_ms"])
+        stats.append(st)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    qps = nq * args.steps / elapsed
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, {qps:,.0f} queries/s")
+
+    st = stats[-1]
+    R = info["R"]
+    vec_bytes = w.index.vec_bytes
+    first_evals = st["evaluations"] - st["reevaluations"]
+    alg_bytes = st["expansions"] * (4 + 4 * R) + first_evals * vec_bytes
+    avg_kernel_ms = float(np.mean(kernel_ms))
+    achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
+    traffic = measured_traffic(w.name)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic,
+                "kernel": "search_resident_u8", "kernel_ms_avg": round(avg_kernel_ms, 4),
+                "algorithmic_bytes_per_launch": int(alg_bytes)}
+
+    gi = ids.cpu().numpy().view(np.uint32)
+    gd = dists.cpu().numpy()
+    cpu = None
+    exact = None
+    if not args.no_cpu_baseline:
+        threads = min(os.cpu_count() or 1, 16)
+        cpu, exact, entry = cpu_baseline(a, q, w, gi, gd, min(args.cpu_sample, nq), threads)
+        assert entry == info["entry"], "entry node differs from the oracle's"
+        log(f"[bench] oracle on CPU: {cpu['value']:,.0f} queries/s with {threads} threads; "
+            f"GPU answers oracle-exact on the sample: {exact}")
+
+    out = {
+        "metric": METRIC, "value": round(qps, 1), "unit": "queries/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n": w.index.n, "D": w.index.D, "R": R, "nq": nq,
+                   "k": w.k, "L": w.L, "W": w.W, "record_bytes": info["record_bytes"],
+                   "records_per_page": info["records_per_page"], "cache_frac": w.cache_frac,
+                   "resident": bool(info["resident"])},
+        "oracle_exact": exact,
+        "achieved_hbm_gbs": roofline["achieved"],
+        "miss_service_gbs": None,
+        "counters": {k: st[k] for k in ("evaluations", "reevaluations", "expansions", "iterations")},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,179 @@
+/*
+ * gorio.h -- C ABI of the MI355X (gfx950) paged graph beam-search library.
+ *
+ * The library implements the GPU side of GORIO ("GPU-Centered Remote I/O for
+ * Graph ANNS over NVMe-oF"): batched DiskANN-style beam search whose node
+ * records live in 4 KB pages.  The GPU owns query evolution, page-miss
+ * generation, pending-query state and resume decisions (Sec. 3.1, Fig. 1); a
+ * host proxy thread only services page reads and publishes completions to
+ * GPU-visible memory (Sec. 3.3, Sec. 4 "CPU transport proxy").  On one GPU the
+ * remote NVMe-oF namespace of Sec. 4 ("Remote storage") is stood in for by a
+ * pinned host-memory backing store with an injected per-request latency.
+ *
+ * Search semantics (the loop of Sec. 1 and Sec. 2.2: expand nodes, compute
+ * distances, update the candidate frontier, discover the next pages):
+ *   key(v) = (squared L2 distance(q, v), v)       -- ties broken by node id
+ *   V = {entry};  X = {}
+ *   repeat: F = the min(L, |V|) smallest keys of V;
+ *           S = the first min(W, .) members of F not in X (in F order);
+ *           stop if S is empty;  X += S;
+ *           for u in S, for each of u's edges v: if v not in V, V += {v}
+ *   result = the first k members of F.
+ * Results do not depend on the cache size, the backing latency or the order
+ * in which page requests complete.
+ *
+ * Page layout: node v is stored at slot s = node_to_slot ? node_to_slot[v] : v,
+ * in page s / records_per_page at byte (s % records_per_page) * record_bytes.
+ * A record is [vector: D x uint8 or D x float32][uint32 degree]
+ * [R x uint32 ids, padded with UINT32_MAX]; the bytes after the last record of
+ * a page are zero.  A graph row's UINT32_MAX entries mean "no edge"; the record
+ * keeps the row's other ids in order and degree = their count.
+ *
+ * Conventions for every call:
+ *   - Status codes, never exceptions; gorio_last_error() returns a
+ *     thread-local message for the last failing call on this thread.
+ *   - The caller owns every array it passes; the library copies what it keeps.
+ *   - One search per index at a time; no call on an index may overlap a search
+ *     on it.  Different indexes may be used from different threads.
+ *   - The device is the HIP device current when gorio_build_index is called;
+ *     later calls switch to it and restore the caller's device.
+ */
+#ifndef GORIO_H
+#define GORIO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gorio_index gorio_index;
+
+typedef enum {
+    GORIO_OK = 0,
+    GORIO_EINVAL = 1,        /* an argument is out of range or inconsistent */
+    GORIO_ENOMEM = 2,        /* device or pinned host allocation failed */
+    GORIO_EDEVICE = 3,       /* a HIP runtime call or a kernel failed */
+    GORIO_ETIMEOUT = 4,      /* paged search made no progress within the watchdog limit */
+    GORIO_EUNSUPPORTED = 5   /* valid request this build does not implement */
+} gorio_status;
+
+typedef enum { GORIO_U8 = 0, GORIO_F32 = 1 } gorio_dtype;
+
+/* Node-record placement in pages.  Zero fields take the default. */
+typedef struct {
+    uint32_t page_bytes;          /* page size; default 4096; multiple of 16 */
+    uint32_t record_bytes;        /* default vec_bytes + 4 + 4R; >= that, multiple of 4 */
+    uint32_t records_per_page;    /* default page_bytes / record_bytes */
+    const uint32_t *node_to_slot; /* host array of n entries, a permutation of [0, n); NULL = identity */
+} gorio_page_layout;
+
+/* Per-search counters (filled when gorio_search gets a non-NULL stats). */
+typedef struct {
+    double kernel_ms;          /* GPU time of the search launch(es), HIP events on the search stream */
+    double wall_ms;            /* host wall time inside gorio_search */
+    uint64_t evaluations;      /* distance evaluations, including re-evaluations */
+    uint64_t reevaluations;    /* evaluations whose node could not be recorded in the visited filter
+                                  (may repeat an earlier one of the same query) */
+    uint64_t expansions;       /* nodes expanded (adjacency lists read) */
+    uint64_t iterations;       /* beams expanded, summed over queries */
+    uint64_t hits;             /* paged mode: record accesses served by a resident page */
+    uint64_t misses;           /* paged mode: record accesses that had to wait for a page */
+    uint64_t pages_served;     /* paged mode: pages moved from the backing store into the cache */
+    uint64_t bytes_served;     /* paged mode: pages_served * page_bytes */
+    uint64_t parks;            /* paged mode: times a query was set aside waiting for pages */
+    uint64_t resumes;          /* paged mode: times a parked query was picked up again */
+} gorio_stats;
+
+/* Read-only facts about a built index. */
+typedef struct {
+    gorio_dtype dtype;
+    uint64_t n;
+    uint32_t D, R;
+    uint32_t page_bytes, record_bytes, records_per_page;
+    uint64_t num_pages;
+    uint64_t index_bytes;      /* num_pages * page_bytes */
+    uint32_t entry;            /* entry node used by every search */
+    int resident;              /* 1: all pages in HBM; 0: paged through the HBM cache */
+    uint64_t cache_slots;      /* paged mode: number of page slots in the HBM cache */
+    int device;                /* HIP device ordinal */
+} gorio_index_info;
+
+/*
+ * Build an index: pack records into pages and choose the entry node.
+ *   vectors: host, n x D row-major (uint8 or float32 per dtype).
+ *   graph:   host, n x R row-major uint32; UINT32_MAX = no edge; any other id must be < n.
+ *   layout:  NULL = all defaults.
+ *   entry:   UINT32_MAX = medoid rule: the node nearest (squared L2, ties to the
+ *            smaller id) to the centroid c, where for uint8 c_d = floor((sum_i x_id
+ *            + floor(n/2)) / n) and for float32 c_d = (float)(sum_i (double)x_id / n)
+ *            summed in i order; otherwise the given node (< n).
+ * Limits: 1 <= n < 2^31; uint8: D % 4 == 0, D <= 512; float32: D <= 256; 1 <= R <= 256.
+ * The packed index is placed in HBM (resident mode).  *out is set only on GORIO_OK.
+ */
+gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors, uint64_t n, uint32_t D,
+                               const uint32_t *graph, uint32_t R,
+                               const gorio_page_layout *layout, uint32_t entry,
+                               gorio_index **out);
+
+/*
+ * Size the HBM page cache (GORIO Sec. 3.2: GPU page cache with a per-slot ready
+ * table; Sec. 4: BaM-derived page-cache path).
+ * bytes >= index_bytes: resident mode, every page in HBM, no misses.
+ * otherwise: paged mode with floor(bytes / page_bytes) slots; the pages move
+ * to a pinned host backing store and the cache starts cold.  Too few slots for
+ * the configured query slots to make progress -> GORIO_EINVAL.
+ */
+gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes);
+
+/*
+ * Configure the backing-store proxy for paged mode (Sec. 3.3 / Sec. 4: the
+ * proxy batches submissions and completions and caps outstanding remote I/O).
+ *   latency_us:      injected delay from a page request's publication to its completion (>= 0).
+ *   max_outstanding: cap on requests the proxy holds in flight (0 = default 4096).
+ *   oversub:         query slots per resident wavefront of the persistent kernel (1..16).
+ *   blocking:        0 = split-phase (park the query, run other ready queries);
+ *                    1 = wait in place for each missing page (the blocking
+ *                    demand-paging baseline the paper compares against, Sec. 5.1).
+ * Takes effect at the next search.  Ignored in resident mode.
+ */
+gorio_status gorio_set_backing(gorio_index *ix, double latency_us, uint32_t max_outstanding,
+                               uint32_t oversub, int blocking);
+
+/*
+ * Batched search (GORIO Sec. 3.3: persistent scheduler; each query is finished
+ * or parked on a missing page and later resumed).
+ *   queries: nq x D (uint8 or float32), host or device pointer.
+ *   ids:     nq x k uint32 out; dists: nq x k out, int32 (uint8 data) or float32.
+ *            Both host or device pointers (detected per pointer).
+ *   Slots past the reachable set are padded with UINT32_MAX and INT32_MAX / +inf.
+ *   stats:   NULL or a struct to fill; non-NULL makes the call wait for the search.
+ *   stream:  hipStream_t to launch on (NULL = the null stream).  With device
+ *            pointers and stats == NULL the call returns without waiting.
+ * Requires 1 <= k <= L <= 256 and 1 <= W <= L.  nq == 0 is a no-op.
+ */
+gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq,
+                          uint32_t k, uint32_t L, uint32_t W,
+                          uint32_t *ids, void *dists, gorio_stats *stats, void *stream);
+
+/* Facts about the index (entry node, page counts, mode). */
+gorio_status gorio_index_info_get(const gorio_index *ix, gorio_index_info *info);
+
+/*
+ * Copy `count` packed pages starting at page `first` to host memory `dst`
+ * (count * page_bytes bytes), from HBM or the backing store.
+ */
+gorio_status gorio_copy_pages(const gorio_index *ix, uint64_t first, uint64_t count, void *dst);
+
+/* Release everything the index owns.  NULL is a no-op. */
+void gorio_free_index(gorio_index *ix);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char *gorio_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GORIO_H */

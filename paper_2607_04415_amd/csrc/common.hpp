@@ -1,0 +1,102 @@
+// Shared device-side definitions: record addressing, fast division and the
+// per-wave visited filter.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "wave.hpp"
+
+namespace gorio {
+
+constexpr uint32_t kNoEdge = 0xFFFFFFFFu;
+constexpr uint32_t kHtEmpty = 0xFFFFFFFFu;
+constexpr int kCandCap = 256;  // candidate ids gathered per beam group
+constexpr int kMaxW = 256;
+
+// floor(x / d) for x < 2^31 with one 64-bit multiply:  m = ceil(2^(31+s) / d),
+// s = ceil(log2 d), q = (x * m) >> (31 + s)  (Granlund & Montgomery, PLDI 1994).
+struct FastDiv {
+  uint32_t d;
+  uint32_t mul;
+  uint32_t shift;  // 31 + s
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t s = 0;
+  while ((1ull << s) < d) ++s;
+  FastDiv f;
+  f.d = d;
+  f.shift = 31 + s;
+  f.mul = (uint32_t)(((1ull << (31 + s)) + d - 1) / d);
+  return f;
+}
+
+__host__ __device__ __forceinline__ uint32_t fastdiv(uint32_t x, FastDiv f) {
+  return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
+}
+
+// Where records sit inside the packed page array.
+struct PageGeom {
+  uint64_t page_bytes;
+  uint32_t record_bytes;
+  uint32_t vec_bytes;      // vector bytes at the start of a record
+  FastDiv rpp;             // records per page
+  const uint32_t *node_to_slot;  // nullptr: slot = node id
+};
+
+__device__ __forceinline__ uint32_t slot_of(const PageGeom &g, uint32_t v) {
+  return g.node_to_slot ? g.node_to_slot[v] : v;
+}
+
+// Page index and byte offset inside that page of node v's record.
+__device__ __forceinline__ void locate(const PageGeom &g, uint32_t v, uint32_t &page, uint32_t &off) {
+  uint32_t s = slot_of(g, v);
+  page = fastdiv(s, g.rpp);
+  off = (s - page * g.rpp.d) * g.record_bytes;
+}
+
+// ---------------------------------------------------------------------------
+// Visited filter: open addressing in LDS, linear probing, one table per wave.
+// It may forget (a full table stops recording) but never invents a member, so
+// a node is at worst evaluated twice; the frontier merge removes the copy.
+// ---------------------------------------------------------------------------
+template <int LOG2>
+struct VisitedLds {
+  static constexpr uint32_t kSize = 1u << LOG2;
+  static constexpr uint32_t kLimit = kSize - kSize / 4;  // stop recording at 75% load
+  static constexpr int kMaxProbe = 64;
+
+  __device__ __forceinline__ static uint32_t hash(uint32_t id) {
+    return (id * 0x9E3779B1u) >> (32 - LOG2);
+  }
+
+  __device__ __forceinline__ static void clear(uint32_t *t) {
+    uint4 *t4 = reinterpret_cast<uint4 *>(t);
+    const uint4 e = make_uint4(kHtEmpty, kHtEmpty, kHtEmpty, kHtEmpty);
+    for (uint32_t i = lane_id(); i < kSize / 4; i += kWave) t4[i] = e;
+  }
+
+  // Returns true when id was not recorded before (evaluate it).  `recorded`
+  // tells whether this call stored it; `used` is the wave's count of stored ids.
+  __device__ __forceinline__ static bool test_and_set(uint32_t *t, uint32_t id, bool may_store,
+                                                       bool &recorded) {
+    uint32_t h = hash(id);
+    recorded = false;
+    for (int p = 0; p < kMaxProbe; ++p) {
+      uint32_t old;
+      if (may_store) {
+        old = atomicCAS(&t[h], kHtEmpty, id);
+        if (old == kHtEmpty) { recorded = true; return true; }
+      } else {
+        old = t[h];
+        if (old == kHtEmpty) return true;
+      }
+      if (old == id) return false;
+      h = (h + 1) & (kSize - 1);
+    }
+    return true;
+  }
+};
+
+}  // namespace gorio

@@ -1,0 +1,387 @@
+// C ABI of the paged graph beam-search library (declared in include/gorio.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/gorio.h"
+#include "build_kernels.hpp"
+#include "index.hpp"
+#include "search_resident.hpp"
+
+using namespace gorio;
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+static thread_local std::string g_last_error;
+
+gorio_status gorio::fail(gorio_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+extern "C" const char *gorio_last_error(void) { return g_last_error.c_str(); }
+
+#define HIP_OR_FAIL(expr)                                                                  \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess)                                                                  \
+      return fail(e_ == hipErrorOutOfMemory ? GORIO_ENOMEM : GORIO_EDEVICE, "%s: %s", #expr, \
+                  hipGetErrorString(e_));                                                  \
+  } while (0)
+
+namespace {
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+// Device buffer freed on scope exit unless released.
+struct DevBuf {
+  void *p = nullptr;
+  ~DevBuf() { if (p) (void)hipFree(p); }
+  hipError_t alloc(size_t bytes) { return hipMalloc(&p, bytes ? bytes : 4); }
+  void *release() { void *r = p; p = nullptr; return r; }
+  template <class T> T *as() const { return static_cast<T *>(p); }
+};
+
+bool is_device_pointer(const void *ptr) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, ptr) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeDevice || a.isManaged;
+}
+
+uint32_t vec_bytes_of(gorio_dtype dt, uint32_t D) { return dt == GORIO_U8 ? D : 4u * D; }
+
+int grid_for(uint64_t items, int per_block, int cap = 65536) {
+  uint64_t g = (items + per_block - 1) / per_block;
+  return (int)std::max<uint64_t>(1, std::min<uint64_t>(g, cap));
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// build
+// ---------------------------------------------------------------------------
+extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors, uint64_t n, uint32_t D,
+                                          const uint32_t *graph, uint32_t R,
+                                          const gorio_page_layout *layout, uint32_t entry,
+                                          gorio_index **out) {
+  if (!out) return fail(GORIO_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (dtype != GORIO_U8 && dtype != GORIO_F32) return fail(GORIO_EINVAL, "unknown dtype %d", (int)dtype);
+  if (!vectors || !graph) return fail(GORIO_EINVAL, "vectors and graph must be non-NULL");
+  if (n == 0 || n >= (1ull << 31)) return fail(GORIO_EINVAL, "n=%llu outside [1, 2^31)", (unsigned long long)n);
+  if (R == 0 || R > 256) return fail(GORIO_EINVAL, "R=%u outside [1, 256]", R);
+  if (dtype == GORIO_U8 && (D == 0 || D % 4 != 0 || D > 512))
+    return fail(GORIO_EINVAL, "uint8 D=%u must be a multiple of 4 in [4, 512]", D);
+  if (dtype == GORIO_F32 && (D == 0 || D > 256)) return fail(GORIO_EINVAL, "float32 D=%u outside [1, 256]", D);
+  if (entry != UINT32_MAX && entry >= n) return fail(GORIO_EINVAL, "entry %u >= n", entry);
+
+  const uint32_t vb = vec_bytes_of(dtype, D);
+  const uint32_t min_rec = vb + 4 + 4 * R;
+  uint32_t page_bytes = layout && layout->page_bytes ? layout->page_bytes : 4096;
+  uint32_t rec_bytes = layout && layout->record_bytes ? layout->record_bytes : min_rec;
+  if (page_bytes % 16 != 0) return fail(GORIO_EINVAL, "page_bytes=%u is not a multiple of 16", page_bytes);
+  if (rec_bytes < min_rec || rec_bytes % 4 != 0)
+    return fail(GORIO_EINVAL, "record_bytes=%u must be a multiple of 4 and >= %u", rec_bytes, min_rec);
+  uint32_t rpp = layout && layout->records_per_page ? layout->records_per_page : page_bytes / rec_bytes;
+  if (rpp == 0 || (uint64_t)rpp * rec_bytes > page_bytes)
+    return fail(GORIO_EINVAL, "%u records of %u bytes do not fit a %u-byte page", rpp, rec_bytes, page_bytes);
+  const uint32_t *n2s_host = layout ? layout->node_to_slot : nullptr;
+
+  int dev = 0;
+  HIP_OR_FAIL(hipGetDevice(&dev));
+  auto ix = std::make_unique<gorio_index>();
+  ix->device = dev;
+  ix->dtype = dtype;
+  ix->n = n;
+  ix->D = D;
+  ix->R = R;
+  ix->vec_bytes = vb;
+  ix->page_bytes = page_bytes;
+  ix->rec_bytes = rec_bytes;
+  ix->rpp = rpp;
+  ix->num_pages = (n + rpp - 1) / rpp;
+
+  HIP_OR_FAIL(hipStreamCreateWithFlags(&ix->stream, hipStreamNonBlocking));
+  HIP_OR_FAIL(hipEventCreate(&ix->ev_start));
+  HIP_OR_FAIL(hipEventCreate(&ix->ev_stop));
+  HIP_OR_FAIL(hipMalloc(&ix->d_stats, sizeof(unsigned long long) * kStatWords));
+  hipStream_t s = ix->stream;
+
+  DevBuf d_vec, d_graph, d_flags;
+  HIP_OR_FAIL(d_vec.alloc((size_t)n * vb));
+  HIP_OR_FAIL(d_graph.alloc((size_t)n * R * 4));
+  HIP_OR_FAIL(d_flags.alloc(64));
+  HIP_OR_FAIL(hipMemcpyAsync(d_vec.p, vectors, (size_t)n * vb, hipMemcpyHostToDevice, s));
+  HIP_OR_FAIL(hipMemcpyAsync(d_graph.p, graph, (size_t)n * R * 4, hipMemcpyHostToDevice, s));
+  unsigned int *bad = d_flags.as<unsigned int>();
+  unsigned long long *best = reinterpret_cast<unsigned long long *>(d_flags.as<char>() + 8);
+  fill_u32<<<1, 64, 0, s>>>(d_flags.as<uint32_t>(), 16, 0u);
+  fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(best), 2, 0xFFFFFFFFu);
+
+  if (n2s_host) {
+    HIP_OR_FAIL(hipMalloc(&ix->d_node_to_slot, (size_t)n * 4));
+    HIP_OR_FAIL(hipMemcpyAsync(ix->d_node_to_slot, n2s_host, (size_t)n * 4, hipMemcpyHostToDevice, s));
+    DevBuf bits;
+    const uint64_t words = (n + 31) / 32;
+    HIP_OR_FAIL(bits.alloc(words * 4));
+    fill_u32<<<grid_for(words, 256), 256, 0, s>>>(bits.as<uint32_t>(), words, 0u);
+    check_permutation<<<grid_for(n, 256), 256, 0, s>>>(ix->d_node_to_slot, (uint32_t)n,
+                                                       bits.as<uint32_t>(), bad);
+    unsigned int h_bad = 0;
+    HIP_OR_FAIL(hipMemcpyAsync(&h_bad, bad, 4, hipMemcpyDeviceToHost, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    if (h_bad) return fail(GORIO_EINVAL, "node_to_slot is not a permutation of [0, n)");
+  }
+
+  // pack into HBM
+  const uint64_t index_bytes = ix->num_pages * (uint64_t)page_bytes;
+  HIP_OR_FAIL(hipMalloc(&ix->d_pages, index_bytes));
+  fill_u32<<<grid_for(index_bytes / 4, 256), 256, 0, s>>>(reinterpret_cast<uint32_t *>(ix->d_pages),
+                                                          index_bytes / 4, 0u);
+  PageGeom geom = ix->geom();
+  pack_records<<<grid_for(n, 4), 256, 0, s>>>(d_vec.as<uint8_t>(), vb, d_graph.as<uint32_t>(), R,
+                                              (uint32_t)n, geom, ix->d_pages, bad);
+  HIP_OR_FAIL(hipGetLastError());
+
+  // entry node
+  if (entry == UINT32_MAX) {
+    DevBuf sums;
+    HIP_OR_FAIL(sums.alloc(sizeof(double) * D));
+    fill_u32<<<1, 256, 0, s>>>(sums.as<uint32_t>(), 2ull * D, 0u);
+    if (dtype == GORIO_U8) {
+      const uint32_t rows = 4096;
+      column_sums_u8<<<grid_for(n, rows, 1 << 30), 256, 0, s>>>(
+          d_vec.as<uint8_t>(), (uint32_t)n, D, rows, sums.as<unsigned long long>());
+      nearest_to_centroid_u8<<<grid_for(n, 256, 2048), 256, 0, s>>>(
+          d_vec.as<uint8_t>(), (uint32_t)n, D, sums.as<unsigned long long>(), best);
+    } else {
+      column_sums_f32_ordered<<<(D + 63) / 64, 64, 0, s>>>(d_vec.as<float>(), (uint32_t)n, D,
+                                                           sums.as<double>());
+      nearest_to_centroid_f32<<<grid_for(n, 256, 2048), 256, 0, s>>>(d_vec.as<float>(), (uint32_t)n, D,
+                                                                    sums.as<double>(), best);
+    }
+    HIP_OR_FAIL(hipGetLastError());
+    unsigned long long h_best = 0;
+    HIP_OR_FAIL(hipMemcpyAsync(&h_best, best, 8, hipMemcpyDeviceToHost, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    ix->entry = (uint32_t)(h_best & 0xFFFFFFFFu);
+  } else {
+    ix->entry = entry;
+  }
+  unsigned int h_bad = 0;
+  HIP_OR_FAIL(hipMemcpyAsync(&h_bad, bad, 4, hipMemcpyDeviceToHost, s));
+  HIP_OR_FAIL(hipStreamSynchronize(s));
+  if (h_bad) return fail(GORIO_EINVAL, "graph holds %u ids >= n that are not UINT32_MAX", h_bad);
+  if (ix->entry >= n) return fail(GORIO_EDEVICE, "entry selection failed");
+
+  ix->resident = true;
+  *out = ix.release();
+  return GORIO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// cache / backing configuration
+// ---------------------------------------------------------------------------
+extern "C" gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes) {
+  if (!ix) return fail(GORIO_EINVAL, "index is NULL");
+  DeviceGuard dg(ix->device);
+  if (bytes >= ix->index_bytes()) return ix->make_resident();
+  return ix->make_paged(bytes / ix->page_bytes);
+}
+
+extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, uint32_t max_outstanding,
+                                          uint32_t oversub, int blocking) {
+  if (!ix) return fail(GORIO_EINVAL, "index is NULL");
+  if (!(latency_us >= 0.0) || latency_us > 1e7) return fail(GORIO_EINVAL, "latency_us=%g out of range", latency_us);
+  if (oversub < 1 || oversub > 16) return fail(GORIO_EINVAL, "oversub=%u outside [1, 16]", oversub);
+  if (blocking != 0 && blocking != 1) return fail(GORIO_EINVAL, "blocking must be 0 or 1");
+  ix->latency_us = latency_us;
+  ix->max_outstanding = max_outstanding ? max_outstanding : 4096;
+  ix->oversub = oversub;
+  ix->blocking = blocking;
+  return GORIO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// search
+// ---------------------------------------------------------------------------
+namespace {
+
+template <int KPL, int VDW>
+gorio_status launch_resident_ht(int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
+  switch (ht_log2) {
+    case 12: search_resident_u8<KPL, VDW, 12><<<grid, kWave, 0, s>>>(p); break;
+    case 13: search_resident_u8<KPL, VDW, 13><<<grid, kWave, 0, s>>>(p); break;
+    default: return fail(GORIO_EUNSUPPORTED, "visited table 2^%d not built", ht_log2);
+  }
+  return GORIO_OK;
+}
+
+template <int KPL>
+gorio_status launch_resident_vdw(uint32_t D, int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
+  const uint32_t vdw = (D / 4 + 7) / 8;
+  if (vdw <= 1) return launch_resident_ht<KPL, 1>(ht_log2, p, grid, s);
+  if (vdw <= 4) return launch_resident_ht<KPL, 4>(ht_log2, p, grid, s);
+  return launch_resident_ht<KPL, 16>(ht_log2, p, grid, s);
+}
+
+gorio_status launch_resident(const ResidentParams &p, int ht_log2, int grid, hipStream_t s) {
+  if (p.L <= 64) return launch_resident_vdw<1>(p.D, ht_log2, p, grid, s);
+  if (p.L <= 128) return launch_resident_vdw<2>(p.D, ht_log2, p, grid, s);
+  return launch_resident_vdw<4>(p.D, ht_log2, p, grid, s);
+}
+
+int env_int(const char *name, int dflt) {
+  const char *v = getenv(name);
+  return v && *v ? atoi(v) : dflt;
+}
+
+}  // namespace
+
+extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq, uint32_t k,
+                                     uint32_t L, uint32_t W, uint32_t *ids, void *dists,
+                                     gorio_stats *stats, void *stream) {
+  const auto t0 = std::chrono::steady_clock::now();
+  if (!ix) return fail(GORIO_EINVAL, "index is NULL");
+  if (k == 0 || L < k || L > 256) return fail(GORIO_EINVAL, "need 1 <= k <= L <= 256 (k=%u L=%u)", k, L);
+  if (W == 0 || W > L) return fail(GORIO_EINVAL, "need 1 <= W <= L (W=%u L=%u)", W, L);
+  if (nq >= (1ull << 31)) return fail(GORIO_EINVAL, "nq=%llu too large", (unsigned long long)nq);
+  if (stats) memset(stats, 0, sizeof *stats);
+  if (nq == 0) return GORIO_OK;
+  if (!queries || !ids || !dists) return fail(GORIO_EINVAL, "queries, ids and dists must be non-NULL");
+  if (ix->dtype != GORIO_U8) return fail(GORIO_EUNSUPPORTED, "float32 search is not built yet");
+  if (!ix->resident) return fail(GORIO_EUNSUPPORTED, "paged search is not built yet");
+
+  DeviceGuard dg(ix->device);
+  if (!dg.ok) return fail(GORIO_EDEVICE, "cannot select device %d", ix->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  const size_t qbytes = (size_t)nq * ix->vec_bytes;
+  const size_t obytes = (size_t)nq * k * 4;
+  const bool q_dev = is_device_pointer(queries);
+  const bool i_dev = is_device_pointer(ids);
+  const bool d_dev = is_device_pointer(dists);
+  DevBuf qbuf, ibuf, dbuf;
+  const uint8_t *d_q = static_cast<const uint8_t *>(queries);
+  uint32_t *d_ids = ids;
+  void *d_dists = dists;
+  if (!q_dev) {
+    HIP_OR_FAIL(qbuf.alloc(qbytes));
+    HIP_OR_FAIL(hipMemcpyAsync(qbuf.p, queries, qbytes, hipMemcpyHostToDevice, s));
+    d_q = qbuf.as<uint8_t>();
+  }
+  if (!i_dev) { HIP_OR_FAIL(ibuf.alloc(obytes)); d_ids = ibuf.as<uint32_t>(); }
+  if (!d_dev) { HIP_OR_FAIL(dbuf.alloc(obytes)); d_dists = dbuf.p; }
+
+  fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(ix->d_stats), 2 * kStatWords, 0u);
+
+  ResidentParams p;
+  p.pages = ix->d_pages;
+  p.geom = ix->geom();
+  p.n = (uint32_t)ix->n;
+  p.D = ix->D;
+  p.R = ix->R;
+  p.entry = ix->entry;
+  p.queries = d_q;
+  p.nq = (uint32_t)nq;
+  p.k = k;
+  p.L = L;
+  p.W = W;
+  p.out_ids = d_ids;
+  p.out_dists = static_cast<int32_t *>(d_dists);
+  p.stats = ix->d_stats;
+
+  const int ht_log2 = env_int("GORIO_HT_LOG2", 13);
+  const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
+  HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+  gorio_status st = launch_resident(p, ht_log2, grid, s);
+  if (st != GORIO_OK) return st;
+  HIP_OR_FAIL(hipGetLastError());
+  HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+
+  if (!i_dev) HIP_OR_FAIL(hipMemcpyAsync(ids, d_ids, obytes, hipMemcpyDeviceToHost, s));
+  if (!d_dev) HIP_OR_FAIL(hipMemcpyAsync(dists, d_dists, obytes, hipMemcpyDeviceToHost, s));
+  unsigned long long h_stats[kStatWords] = {};
+  if (stats) HIP_OR_FAIL(hipMemcpyAsync(h_stats, ix->d_stats, sizeof h_stats, hipMemcpyDeviceToHost, s));
+  if (stats || !i_dev || !d_dev || !q_dev) HIP_OR_FAIL(hipStreamSynchronize(s));
+  if (stats) {
+    float ms = 0.f;
+    HIP_OR_FAIL(hipEventElapsedTime(&ms, ix->ev_start, ix->ev_stop));
+    stats->kernel_ms = ms;
+    stats->evaluations = h_stats[kStatEval];
+    stats->reevaluations = h_stats[kStatReeval];
+    stats->expansions = h_stats[kStatExp];
+    stats->iterations = h_stats[kStatIter];
+    stats->wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  }
+  return GORIO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// info / pages / free
+// ---------------------------------------------------------------------------
+extern "C" gorio_status gorio_index_info_get(const gorio_index *ix, gorio_index_info *info) {
+  if (!ix || !info) return fail(GORIO_EINVAL, "NULL argument");
+  info->dtype = ix->dtype;
+  info->n = ix->n;
+  info->D = ix->D;
+  info->R = ix->R;
+  info->page_bytes = ix->page_bytes;
+  info->record_bytes = ix->rec_bytes;
+  info->records_per_page = ix->rpp;
+  info->num_pages = ix->num_pages;
+  info->index_bytes = ix->index_bytes();
+  info->entry = ix->entry;
+  info->resident = ix->resident ? 1 : 0;
+  info->cache_slots = ix->resident ? ix->num_pages : ix->cache_slots;
+  info->device = ix->device;
+  return GORIO_OK;
+}
+
+extern "C" gorio_status gorio_copy_pages(const gorio_index *ix, uint64_t first, uint64_t count, void *dst) {
+  if (!ix || (!dst && count)) return fail(GORIO_EINVAL, "NULL argument");
+  if (first > ix->num_pages || count > ix->num_pages - first) return fail(GORIO_EINVAL, "page range out of bounds");
+  if (count == 0) return GORIO_OK;
+  DeviceGuard dg(ix->device);
+  const size_t off = first * ix->page_bytes, bytes = count * ix->page_bytes;
+  if (ix->resident) {
+    HIP_OR_FAIL(hipMemcpy(dst, ix->d_pages + off, bytes, hipMemcpyDeviceToHost));
+  } else {
+    memcpy(dst, ix->h_backing + off, bytes);
+  }
+  return GORIO_OK;
+}
+
+extern "C" void gorio_free_index(gorio_index *ix) {
+  if (!ix) return;
+  {
+    DeviceGuard dg(ix->device);
+    ix->release_all();
+  }
+  delete ix;
+}

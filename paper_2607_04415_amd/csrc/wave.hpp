@@ -1,0 +1,134 @@
+// Wave64 building blocks for gfx950 (CDNA4): lane masks, prefix counts, DPP
+// reductions and 64-bit bitonic compare-exchange.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gorio {
+
+constexpr int kWave = 64;
+constexpr uint64_t kInfKey = ~0ull;
+
+__device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
+
+// Number of set bits of `mask` in lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ uint32_t readlane(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
+  uint32_t lo = readlane((uint32_t)v, lane);
+  uint32_t hi = readlane((uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t first_lane_value(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
+// Cross-lane exchange with lane ^ m (ds_bpermute through the LDS crossbar).
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
+  int src = (lane_id() ^ m) << 2;
+  uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)v);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Value of lane - 1 (lane 0 gets `fill`).
+__device__ __forceinline__ uint64_t shfl_up1_64(uint64_t v, uint64_t fill) {
+  int l = lane_id();
+  int src = ((l + 63) & 63) << 2;
+  uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)v);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)(v >> 32));
+  uint64_t r = ((uint64_t)hi << 32) | lo;
+  return l == 0 ? fill : r;
+}
+
+// Value of lane + 1 (lane 63 gets `fill`).
+__device__ __forceinline__ uint64_t shfl_down1_64(uint64_t v, uint64_t fill) {
+  int l = lane_id();
+  int src = ((l + 1) & 63) << 2;
+  uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)v);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)(v >> 32));
+  uint64_t r = ((uint64_t)hi << 32) | lo;
+  return l == kWave - 1 ? fill : r;
+}
+
+// Sum over each aligned group of 8 lanes; every lane of the group gets the total.
+// quad_perm [1,0,3,2] (0xB1), quad_perm [2,3,0,1] (0x4E), row_half_mirror (0x141).
+__device__ __forceinline__ int sum8(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+  return v;
+}
+
+// Sum over the whole wave, result in every lane (used off the hot path).
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  for (int m = 1; m < kWave; m <<= 1) v += shfl_xor64(v, m);
+  return v;
+}
+
+__device__ __forceinline__ uint64_t min64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint64_t max64(uint64_t a, uint64_t b) { return a < b ? b : a; }
+
+// ---------------------------------------------------------------------------
+// Bitonic networks over P = 64 * KPL keys held as v[r] at element r*64 + lane.
+// ---------------------------------------------------------------------------
+
+// One compare-exchange stage with partner distance j.  Element e keeps the
+// smaller key when (e is the lower of the pair) == (its block sorts upward).
+template <int KPL>
+__device__ __forceinline__ void bitonic_stage(uint64_t (&v)[KPL], int j, int k, bool descending) {
+  const int l = lane_id();
+  if (j >= kWave) {
+    const int rj = j / kWave;
+#pragma unroll
+    for (int r = 0; r < KPL; ++r) {
+      if (r & rj) continue;
+      const int e = r * kWave + l;
+      bool up = ((e & k) == 0) != descending;
+      uint64_t a = v[r], b = v[r | rj];
+      v[r] = up ? min64(a, b) : max64(a, b);
+      v[r | rj] = up ? max64(a, b) : min64(a, b);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < KPL; ++r) {
+      const int e = r * kWave + l;
+      bool up = ((e & k) == 0) != descending;
+      bool lower = (l & j) == 0;
+      uint64_t o = shfl_xor64(v[r], j);
+      v[r] = (lower == up) ? min64(v[r], o) : max64(v[r], o);
+    }
+  }
+}
+
+// Full sort of P keys (ascending unless `descending`).
+template <int KPL>
+__device__ __forceinline__ void bitonic_sort(uint64_t (&v)[KPL], bool descending) {
+  constexpr int P = KPL * kWave;
+#pragma unroll
+  for (int k = 2; k <= P; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) bitonic_stage<KPL>(v, j, k, descending);
+  }
+}
+
+// Sorts a bitonic sequence of P keys ascending.
+template <int KPL>
+__device__ __forceinline__ void bitonic_merge_up(uint64_t (&v)[KPL]) {
+  constexpr int P = KPL * kWave;
+#pragma unroll
+  for (int j = P >> 1; j > 0; j >>= 1) bitonic_stage<KPL>(v, j, 2 * P, false);
+}
+
+}  // namespace gorio

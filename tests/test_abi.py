@@ -1,0 +1,82 @@
+"""The C ABI library loads, exports every declared symbol, and rejects bad
+arguments before touching a device (runs without a GPU)."""
+import ctypes
+import re
+from pathlib import Path
+
+import numpy as np
+import pytest
+
+import paper_2607_04415_amd as g
+
+HEADER = Path(__file__).resolve().parents[1] / "include" / "gorio.h"
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not g.LIB_PATH.exists():
+        from paper_2607_04415_amd import _build
+        _build.build()
+    return g.lib()
+
+
+def declared_functions():
+    text = HEADER.read_text()
+    return sorted(set(re.findall(r"^\s*(?:gorio_status|void|const char \*)\s*(gorio_\w+)\s*\(",
+                                 text, re.M)))
+
+
+def test_header_declares_what_binding_expects():
+    assert declared_functions() == sorted(g.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_struct_sizes_match_header():
+    # gorio_stats: 2 doubles + 10 uint64; gorio_page_layout: 3 uint32 + pointer
+    assert ctypes.sizeof(g.Stats) == 2 * 8 + 10 * 8
+    assert ctypes.sizeof(g.PageLayout) == 3 * 4 + 4 + 8
+
+
+def _build(lib, dtype=0, n=10, D=8, R=4, layout=None, entry=g.NO_EDGE, vectors=True, graph=True):
+    x = np.zeros((max(n, 1), max(D, 1)), np.uint8)
+    gr = np.zeros((max(n, 1), max(R, 1)), np.uint32)
+    h = ctypes.c_void_p()
+    st = lib.gorio_build_index(dtype, x.ctypes.data if vectors else None, n, D,
+                               gr.ctypes.data if graph else None, R,
+                               ctypes.byref(layout) if layout is not None else None, entry,
+                               ctypes.byref(h))
+    return st, h
+
+
+@pytest.mark.parametrize("kw", [
+    dict(dtype=7), dict(n=0), dict(n=1 << 31), dict(R=0), dict(R=257), dict(D=0), dict(D=6),
+    dict(D=516), dict(dtype=1, D=257), dict(entry=10), dict(vectors=False), dict(graph=False),
+    dict(layout=g.PageLayout(4100, 0, 0, None)),           # page size not a multiple of 16
+    dict(layout=g.PageLayout(4096, 10, 0, None)),          # record smaller than its contents
+    dict(layout=g.PageLayout(4096, 26, 0, None)),          # record not a multiple of 4
+    dict(layout=g.PageLayout(4096, 0, 1000, None)),        # too many records per page
+])
+def test_build_rejects_bad_arguments(lib, kw):
+    st, h = _build(lib, **kw)
+    assert st == g.EINVAL
+    assert not h.value
+    assert lib.gorio_last_error().decode()
+
+
+def test_null_handles(lib):
+    assert lib.gorio_set_cache(None, 0) == g.EINVAL
+    assert lib.gorio_set_backing(None, 0.0, 0, 1, 0) == g.EINVAL
+    assert lib.gorio_search(None, None, 0, 1, 1, 1, None, None, None, None) == g.EINVAL
+    assert lib.gorio_index_info_get(None, None) == g.EINVAL
+    assert lib.gorio_copy_pages(None, 0, 0, None) == g.EINVAL
+    lib.gorio_free_index(None)
+
+
+def test_build_needs_out_pointer(lib):
+    x = np.zeros((4, 4), np.uint8)
+    gr = np.zeros((4, 2), np.uint32)
+    assert lib.gorio_build_index(0, x.ctypes.data, 4, 4, gr.ctypes.data, 2, None, g.NO_EDGE, None) == g.EINVAL

@@ -1,0 +1,218 @@
+"""GPU parity: the HIP library against the CPU oracle, element by element.
+
+uint8 data: ids and int32 distances must match bit-exact (ties broken by id),
+and the per-search counters (expansions, iterations, first-time evaluations)
+must equal the oracle's summed counts.
+"""
+import json
+import os
+from pathlib import Path
+
+import numpy as np
+import pytest
+
+import paper_2607_04415_amd as g
+from conftest import NO_EDGE, random_graph
+from workload import IndexSpec, QuerySpec, WORKLOADS, index_arrays, query_array
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = Path(__file__).parent / "golden"
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    torch.cuda.set_device(0)
+    return torch
+
+
+def run_gpu(torch, ix, q, k, L, W):
+    qd = torch.from_numpy(np.ascontiguousarray(q)).cuda()
+    ids, dists, st = ix.search(qd, k, L, W)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), st
+
+
+def check_parity(orc, torch, x, graph, q, k, L, W, layout=None, entry=None, counts=True):
+    layout = layout or {}
+    ix = g.Index(x, graph, entry=entry, **layout)
+    e = ix.info["entry"]
+    if entry is None:
+        assert e == orc.medoid(x)
+    okw = {kk: v for kk, v in layout.items() if v is not None and not (np.isscalar(v) and v == 0)}
+    oids, od, oc, _ = orc.pack(x, graph, **okw).search(q, k, L, W, e, threads=8)
+    gi, gd, st = run_gpu(torch, ix, q, k, L, W)
+    bad = np.flatnonzero((gi != oids).any(1) | (gd != od).any(1))
+    assert bad.size == 0, f"{bad.size} queries differ, first {bad[:5]}: gpu {gi[bad[0]]} {gd[bad[0]]} " \
+                          f"oracle {oids[bad[0]]} {od[bad[0]]}"
+    if counts:
+        assert st["expansions"] == int(oc["expansions"].sum())
+        assert st["iterations"] == int(oc["iterations"].sum())
+        assert st["evaluations"] - st["reevaluations"] <= int(oc["evaluations"].sum()) <= st["evaluations"]
+        if st["reevaluations"] == 0:
+            assert st["evaluations"] == int(oc["evaluations"].sum())
+    return ix, st
+
+
+# --------------------------------------------------------------------------- #
+def test_trace8_on_gpu(orc, torch_dev):
+    t = json.loads((GOLDEN / "trace8.json").read_text())
+    x = np.array(t["vectors"], np.uint8)
+    graph = np.array(t["graph"], np.uint32)
+    ix = g.Index(x, graph)
+    assert ix.info["entry"] == t["medoid"]["entry"]
+    for c in t["cases"]:
+        gi, gd, st = run_gpu(torch_dev, ix, np.array([c["query"]], np.uint8), c["k"], c["L"], c["W"])
+        assert gi[0].tolist() == c["ids"]
+        assert gd[0].tolist() == c["dists"]
+        assert st["evaluations"] == c["evaluations"]
+        assert st["expansions"] == c["expansions"]
+        assert st["iterations"] == c["iterations"]
+
+
+CASES = [
+    # n, D, R, clusters, k, L, W
+    (1000, 128, 32, 4, 10, 32, 4),
+    (777, 64, 20, 3, 5, 50, 3),
+    (5000, 128, 64, 8, 10, 64, 4),
+    (3000, 16, 100, 6, 16, 100, 7),
+    (4000, 256, 48, 5, 20, 200, 16),
+    (2000, 512, 16, 4, 1, 1, 1),
+    (1500, 32, 24, 3, 12, 256, 256),
+    (2500, 4, 8, 2, 8, 65, 2),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"n{c[0]}-D{c[1]}-R{c[2]}-k{c[4]}-L{c[5]}-W{c[6]}" for c in CASES])
+def test_parity_mixture(orc, torch_dev, case):
+    n, D, R, C, k, L, W = case
+    spec = IndexSpec(n=n, D=D, dtype="u8", clusters=C, sigma=20.0, r_near=R // 2, r_rand=R - R // 2,
+                     seed=100 + n)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(300, 7 + n))
+    check_parity(orc, torch_dev, a["x"], a["graph"], q, k, L, W)
+
+
+def test_parity_random_graph_with_missing_edges(orc, torch_dev):
+    rng = np.random.default_rng(1)
+    n, D, R = 1200, 32, 40
+    x = rng.integers(0, 256, (n, D), dtype=np.uint8)
+    graph = random_graph(rng, n, R, sentinel_frac=0.35)
+    q = rng.integers(0, 256, (200, D), dtype=np.uint8)
+    check_parity(orc, torch_dev, x, graph, q, 10, 40, 5)
+
+
+@pytest.mark.parametrize("layout", [
+    dict(node_to_slot="perm"), dict(record_bytes=400), dict(records_per_page=3),
+    dict(page_bytes=8192), dict(page_bytes=16),
+], ids=["perm", "rec400", "rpp3", "page8k", "page16-tiny"])
+def test_parity_layouts(orc, torch_dev, layout):
+    rng = np.random.default_rng(2)
+    n, D, R = 2000, 128, 64
+    if layout.get("page_bytes") == 16:
+        D, R = 4, 2
+        layout = dict(page_bytes=16)
+    spec = IndexSpec(n=n, D=D, dtype="u8", clusters=4, sigma=20.0, r_near=R // 2, r_rand=R // 2, seed=5)
+    a = index_arrays(spec, use_cache=False)
+    if layout.get("node_to_slot") == "perm":
+        layout = dict(node_to_slot=rng.permutation(n).astype(np.uint32))
+    q = query_array(spec, QuerySpec(150, 3))
+    ix, _ = check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 48, 4, layout=layout)
+    okw = {kk: v for kk, v in layout.items() if v is not None and not (np.isscalar(v) and v == 0)}
+    want = orc.pack(a["x"], a["graph"], **okw).pages
+    assert np.array_equal(ix.pages(), want), "packed pages differ from the oracle's packer"
+
+
+def test_ties_and_duplicates(orc, torch_dev):
+    rng = np.random.default_rng(3)
+    base = rng.integers(0, 256, (50, 16), dtype=np.uint8)
+    x = base[rng.integers(0, 50, 1000)]           # many identical vectors
+    graph = random_graph(rng, 1000, 24)
+    q = base[rng.integers(0, 50, 100)]            # queries equal to data points: distance 0 ties
+    check_parity(orc, torch_dev, x, graph, q, 16, 64, 4)
+
+
+def test_unreachable_and_padding(orc, torch_dev):
+    x = (np.arange(200, dtype=np.uint32) % 256).astype(np.uint8).reshape(200, 1).repeat(4, 1)
+    graph = np.full((200, 3), NO_EDGE, np.uint32)
+    for i in range(5):                       # component {0..4}; the rest is unreachable
+        graph[i] = [(i + 1) % 5, NO_EDGE, (i + 2) % 5]
+    for i in range(5, 200):
+        graph[i] = [5 + (i - 4) % 195, NO_EDGE, NO_EDGE]
+    q = np.array([[100, 100, 100, 100], [0, 0, 0, 0]], np.uint8)
+    ix, _ = check_parity(orc, torch_dev, x, graph, q, 8, 16, 2, entry=0)
+    gi, gd, _ = run_gpu(torch_dev, ix, q, 8, 16, 2)
+    assert (gi[:, 5:] == NO_EDGE).all() and (gd[:, 5:] == 2 ** 31 - 1).all()
+
+
+def test_visited_filter_overflow_still_exact(orc, torch_dev, monkeypatch):
+    """A small visited table forgets nodes: re-evaluations happen, results do not change."""
+    monkeypatch.setenv("GORIO_HT_LOG2", "12")
+    spec = IndexSpec(n=20000, D=64, dtype="u8", clusters=8, sigma=20.0, r_near=32, r_rand=32, seed=9)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(64, 10))
+    _, st = check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 256, 8)
+    assert st["reevaluations"] > 0, "the test did not exercise the overflow path"
+
+
+def test_host_pointers(orc, torch_dev):
+    spec = IndexSpec(n=1000, D=32, dtype="u8", clusters=3, sigma=20.0, r_near=8, r_rand=8, seed=11)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(40, 12))
+    ix = g.Index(a["x"], a["graph"])
+    ids, dists, st = ix.search(q, 10, 20, 2)          # numpy in -> numpy out
+    oids, od, _, _ = orc.pack(a["x"], a["graph"]).search(q, 10, 20, 2, ix.info["entry"])
+    assert np.array_equal(ids, oids) and np.array_equal(dists, od)
+
+
+def test_empty_batch_and_bad_arguments(torch_dev):
+    spec = IndexSpec(n=500, D=16, dtype="u8", clusters=2, sigma=20.0, r_near=4, r_rand=4, seed=13)
+    a = index_arrays(spec, use_cache=False)
+    ix = g.Index(a["x"], a["graph"])
+    q = np.zeros((1, 16), np.uint8)
+    assert ix.search_into(q, 0, 1, 1, 1, None, None) is not None          # nq = 0: no-op
+    for k, L, W in ((0, 4, 1), (5, 4, 1), (1, 257, 1), (1, 4, 0), (1, 4, 5)):
+        with pytest.raises(g.GorioError) as e:
+            ix.search(q, k, L, W)
+        assert e.value.status == g.EINVAL
+
+
+def test_entry_rule_matches_oracle_f32(orc, torch_dev):
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((3000, 96)).astype(np.float32)
+    graph = random_graph(rng, 3000, 8)
+    ix = g.Index(x, graph)
+    assert ix.info["entry"] == orc.medoid(x)
+    assert np.array_equal(ix.pages(), orc.pack(x, graph).pages)
+
+
+# --------------------------------------------------------------------------- #
+# benchmark workloads at full size
+# --------------------------------------------------------------------------- #
+def _workload_parity(orc, torch, name, threads=16):
+    w = WORKLOADS[name]
+    a = index_arrays(w.index)
+    q = query_array(w.index, w.queries)
+    print(f"[{name}] n={w.index.n} nq={len(q)} k={w.k} L={w.L} W={w.W}", flush=True)
+    ix = g.Index(a["x"], a["graph"])
+    e = ix.info["entry"]
+    assert e == orc.medoid(a["x"])
+    packed = orc.pack(a["x"], a["graph"])
+    assert np.array_equal(ix.pages(), packed.pages)
+    oids, od, oc, _ = packed.search(q, w.k, w.L, w.W, e, threads=threads)
+    gi, gd, st = run_gpu(torch, ix, q, w.k, w.L, w.W)
+    assert np.array_equal(gi, oids) and np.array_equal(gd, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+    assert st["evaluations"] - st["reevaluations"] <= int(oc["evaluations"].sum())
+    print(f"[{name}] bit-exact; kernel {st['kernel_ms']:.3f} ms; evals {st['evaluations']} "
+          f"(re {st['reevaluations']}) oracle {int(oc['evaluations'].sum())}", flush=True)
+
+
+def test_workload_u8_10k(orc, torch_dev):
+    _workload_parity(orc, torch_dev, "u8-10k-hbm")
+
+
+def test_workload_u8_1m(orc, torch_dev):
+    _workload_parity(orc, torch_dev, "u8-1m-hbm")
