@@ -79,20 +79,32 @@ __device__ __forceinline__ uint64_t frontier_at(const uint64_t (&F)[KPL], uint32
   return v;
 }
 
-// F is sorted; copies of one node are adjacent and the copy with the expanded
-// bit sorts last.  Keep the last copy of each node, then restore order.
+// Slow path after the visited filter forgot a node: a candidate may repeat a
+// frontier node or another candidate.  Merge without truncating (2P slots:
+// F ascending then C descending is bitonic), drop all but the last copy of
+// each node (the copy carrying the expanded bit sorts last), re-sort, keep P.
 template <int KPL>
-__device__ __forceinline__ void dedupe_sorted(uint64_t (&F)[KPL]) {
-  uint64_t next[KPL];
+__device__ __forceinline__ void merge_dedupe(uint64_t (&F)[KPL], uint64_t c_desc) {
+  uint64_t big[2 * KPL];
 #pragma unroll
   for (int r = 0; r < KPL; ++r) {
-    uint64_t fill = r + 1 < KPL ? readlane64(F[r + 1 < KPL ? r + 1 : r], 0) : kInfKey;
-    next[r] = shfl_down1_64(F[r], fill);
+    big[r] = F[r];
+    big[KPL + r] = kInfKey;
+  }
+  big[2 * KPL - 1] = c_desc;
+  bitonic_merge_up<2 * KPL>(big);
+  uint64_t next[2 * KPL];
+#pragma unroll
+  for (int r = 0; r < 2 * KPL; ++r) {
+    uint64_t fill = r + 1 < 2 * KPL ? readlane64(big[r + 1 < 2 * KPL ? r + 1 : r], 0) : kInfKey;
+    next[r] = shfl_down1_64(big[r], fill);
   }
 #pragma unroll
-  for (int r = 0; r < KPL; ++r)
-    if (F[r] != kInfKey && next[r] != kInfKey && (next[r] >> 1) == (F[r] >> 1)) F[r] = kInfKey;
-  bitonic_sort<KPL>(F, false);
+  for (int r = 0; r < 2 * KPL; ++r)
+    if (big[r] != kInfKey && next[r] != kInfKey && (next[r] >> 1) == (big[r] >> 1)) big[r] = kInfKey;
+  bitonic_sort<2 * KPL>(big, false);
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) F[r] = big[r];
 }
 
 template <int KPL, int VDW, int HT_LOG2>
@@ -224,9 +236,13 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
           if (ballot(pass) == 0) continue;
           uint64_t c[1] = {pass ? key : kInfKey};
           bitonic_sort<1>(c, true);
-          F[KPL - 1] = min64(F[KPL - 1], c[0]);
-          bitonic_merge_up<KPL>(F);
-          if (forgot) dedupe_sorted<KPL>(F);
+          if (!forgot) {
+            // no node can repeat: the P smallest of F and C are min(F, C reversed)
+            F[KPL - 1] = min64(F[KPL - 1], c[0]);
+            bitonic_merge_up<KPL>(F);
+          } else {
+            merge_dedupe<KPL>(F, c[0]);
+          }
 #pragma unroll
           for (int r = 0; r < KPL; ++r)
             if ((uint32_t)(r * kWave + l) >= p.L) F[r] = kInfKey;
