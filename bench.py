@@ -86,6 +86,8 @@ def main():
     ap.add_argument("--workload", default="u8-1m-hbm")
     ap.add_argument("--cpu-sample", type=int, default=10000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
@@ -100,6 +102,15 @@ def main():
     if not g.LIB_PATH.exists():
         raise SystemExit("libgorio.so is not built: run python __graft_entry__.py build")
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        # A plain copy kernel of known size: 1 GiB read + 1 GiB written per launch.
+        src = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "launches": 5}), flush=True)
+        return
     w = WORKLOADS[args.workload]
     log(f"[bench] workload {w.name}: {w.description}")
     t0 = time.perf_counter()

@@ -56,6 +56,21 @@ __device__ __forceinline__ void locate(const PageGeom &g, uint32_t v, uint32_t &
   off = (s - page * g.rpp.d) * g.record_bytes;
 }
 
+// Slot of node v when the caller knows at compile time whether a placement
+// permutation exists (keeps the permutation load out of paths without one,
+// so dependent record loads need not wait on it).
+template <bool N2S>
+__device__ __forceinline__ uint32_t slot_ct(const PageGeom &g, uint32_t v) {
+  if constexpr (N2S) return g.node_to_slot[v];
+  else return v;
+}
+
+// Byte offset of slot s's record in the packed page array.
+__device__ __forceinline__ uint64_t record_offset(const PageGeom &g, uint32_t s) {
+  const uint32_t page = fastdiv(s, g.rpp);
+  return (uint64_t)page * g.page_bytes + (uint64_t)((s - page * g.rpp.d) * g.record_bytes);
+}
+
 // ---------------------------------------------------------------------------
 // Visited filter: open addressing in LDS, linear probing, one table per wave.
 // It may forget (a full table stops recording) but never invents a member, so
@@ -78,7 +93,7 @@ struct VisitedLds {
   }
 
   // Returns true when id was not recorded before (evaluate it).  `recorded`
-  // tells whether this call stored it; `used` is the wave's count of stored ids.
+  // tells whether this call stored it.
   __device__ __forceinline__ static bool test_and_set(uint32_t *t, uint32_t id, bool may_store,
                                                        bool &recorded) {
     uint32_t h = hash(id);
@@ -96,6 +111,50 @@ struct VisitedLds {
       h = (h + 1) & (kSize - 1);
     }
     return true;
+  }
+
+  // N ids per lane at once (the LDS atomics of one probe round issue back to
+  // back).  isnew[i]: evaluate ids[i]; recorded[i]: this call stored it.
+  template <int N>
+  __device__ __forceinline__ static void test_and_set_n(uint32_t *t, const uint32_t (&ids)[N],
+                                                        const bool (&valid)[N], bool may_store,
+                                                        bool (&isnew)[N], bool (&recorded)[N]) {
+    uint32_t h[N];
+    bool pend[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      h[i] = hash(ids[i]);
+      pend[i] = valid[i];
+      isnew[i] = false;
+      recorded[i] = false;
+    }
+    for (int p = 0; p < kMaxProbe; ++p) {
+      bool any = false;
+#pragma unroll
+      for (int i = 0; i < N; ++i) any |= pend[i];
+      if (ballot(any) == 0) break;
+      uint32_t old[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        if (pend[i]) old[i] = may_store ? atomicCAS(&t[h[i]], kHtEmpty, ids[i]) : t[h[i]];
+      }
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        if (!pend[i]) continue;
+        if (old[i] == kHtEmpty) {
+          isnew[i] = true;
+          recorded[i] = may_store;
+          pend[i] = false;
+        } else if (old[i] == ids[i]) {
+          pend[i] = false;
+        } else {
+          h[i] = (h[i] + 1) & (kSize - 1);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (pend[i]) isnew[i] = true;  // probe limit: evaluate, unrecorded
   }
 };
 

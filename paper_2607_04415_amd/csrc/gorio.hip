@@ -232,22 +232,30 @@ extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, ui
 // ---------------------------------------------------------------------------
 namespace {
 
-template <int KPL, int VDW>
+template <int KPL, int VDW, bool EXACT, bool N2S>
 gorio_status launch_resident_ht(int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
   switch (ht_log2) {
-    case 12: search_resident_u8<KPL, VDW, 12><<<grid, kWave, 0, s>>>(p); break;
-    case 13: search_resident_u8<KPL, VDW, 13><<<grid, kWave, 0, s>>>(p); break;
+    case 13: search_resident_u8<KPL, VDW, EXACT, 13, N2S><<<grid, kWave, 0, s>>>(p); break;
     default: return fail(GORIO_EUNSUPPORTED, "visited table 2^%d not built", ht_log2);
   }
   return GORIO_OK;
 }
 
+template <int KPL, int VDW, bool EXACT>
+gorio_status launch_resident_n2s(int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
+  if (p.geom.node_to_slot) return launch_resident_ht<KPL, VDW, EXACT, true>(ht_log2, p, grid, s);
+  return launch_resident_ht<KPL, VDW, EXACT, false>(ht_log2, p, grid, s);
+}
+
+// uint8 rows: 128-d gets the exact 16-B-per-lane kernel; others the generic one
+// with 1, 4 or 16 dwords per lane.
 template <int KPL>
 gorio_status launch_resident_vdw(uint32_t D, int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
+  if (D == 128) return launch_resident_n2s<KPL, 4, true>(ht_log2, p, grid, s);
   const uint32_t vdw = (D / 4 + 7) / 8;
-  if (vdw <= 1) return launch_resident_ht<KPL, 1>(ht_log2, p, grid, s);
-  if (vdw <= 4) return launch_resident_ht<KPL, 4>(ht_log2, p, grid, s);
-  return launch_resident_ht<KPL, 16>(ht_log2, p, grid, s);
+  if (vdw <= 1) return launch_resident_n2s<KPL, 1, false>(ht_log2, p, grid, s);
+  if (vdw <= 4) return launch_resident_n2s<KPL, 4, false>(ht_log2, p, grid, s);
+  return launch_resident_n2s<KPL, 16, false>(ht_log2, p, grid, s);
 }
 
 gorio_status launch_resident(const ResidentParams &p, int ht_log2, int grid, hipStream_t s) {
@@ -306,6 +314,7 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   p.n = (uint32_t)ix->n;
   p.D = ix->D;
   p.R = ix->R;
+  p.Rdiv = make_fastdiv(ix->R);
   p.entry = ix->entry;
   p.queries = d_q;
   p.nq = (uint32_t)nq;

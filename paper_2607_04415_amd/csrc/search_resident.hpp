@@ -7,12 +7,16 @@
 // sorting networks.  One iteration (GORIO Sec. 1 / Sec. 2.2: expand nodes,
 // compute distances, update the frontier):
 //   select  - the first W unexpanded slots of F (ballot + prefix count);
-//   expand  - read each chosen node's degree and neighbour ids;
-//   filter  - drop ids already in the visited filter (LDS atomics), compact;
-//   evaluate- 8 lanes per 128-B vector, v_dot4_u32_u8 on coalesced reads:
-//             sum (q - x)^2 = q.q + sum (x.x - 2 q.x), exact in int32;
-//   merge   - keys below F's L-th key are bitonic-sorted in a 64-lane chunk
-//             and merged into F (bitonic merge), slots >= L cleared.
+//   expand  - one round trip reads the degree and id list of every chosen
+//             node of a beam group (up to 256 ids, 4 per lane);
+//   filter  - ids already in the visited filter are dropped (LDS atomics),
+//             the rest compacted into an LDS candidate list;
+//   evaluate- one round trip gathers up to 256 vectors: 8 lanes per 128-B
+//             vector, 16 B per lane, v_dot4_u32_u8 on the coalesced reads,
+//             sum (q - x)^2 = q.q + sum (x.x - 2 q.x) exact in int32;
+//   merge   - only keys below F's L-th key can enter: a few are inserted by
+//             rank (ballot + DPP shift), many are bitonic-sorted per 64-lane
+//             chunk and bitonic-merged into F.
 #pragma once
 
 #include "common.hpp"
@@ -25,6 +29,7 @@ struct ResidentParams {
   uint32_t n;
   uint32_t D;              // uint8 dimensions (multiple of 4)
   uint32_t R;              // id slots per record
+  FastDiv Rdiv;            // division by R
   uint32_t entry;
   const uint8_t *queries;  // nq x D
   uint32_t nq;
@@ -36,16 +41,27 @@ struct ResidentParams {
 
 // Lane layout for distance evaluation: 8 groups of 8 lanes; group g handles
 // one vector per round, lane gl of the group holds dwords [gl*VDW, gl*VDW+VDW).
-template <int VDW>
+// EXACT: the vector is exactly 8 * VDW dwords (no per-dword bound checks, and
+// 16-B loads when VDW is a multiple of 4; records are 4-B aligned).
+template <int VDW, bool EXACT>
 struct U8Vec {
   uint32_t w[VDW];
 
   __device__ __forceinline__ void load(const uint8_t *rec, int gl, uint32_t dwords) {
-    const uint32_t *p = reinterpret_cast<const uint32_t *>(rec);
+    const uint32_t *p = reinterpret_cast<const uint32_t *>(rec) + gl * VDW;
+    if constexpr (EXACT && VDW % 4 == 0) {
 #pragma unroll
-    for (int t = 0; t < VDW; ++t) {
-      uint32_t di = gl * VDW + t;
-      w[t] = di < dwords ? p[di] : 0u;
+      for (int t = 0; t < VDW; t += 4) {
+        uint4 u;
+        __builtin_memcpy(&u, __builtin_assume_aligned(p + t, 4), 16);
+        w[t] = u.x; w[t + 1] = u.y; w[t + 2] = u.z; w[t + 3] = u.w;
+      }
+    } else if constexpr (EXACT) {
+#pragma unroll
+      for (int t = 0; t < VDW; ++t) w[t] = p[t];
+    } else {
+#pragma unroll
+      for (int t = 0; t < VDW; ++t) w[t] = (uint32_t)(gl * VDW + t) < dwords ? p[t] : 0u;
     }
   }
   __device__ __forceinline__ void zero() {
@@ -55,8 +71,8 @@ struct U8Vec {
 };
 
 // Partial of sum (x.x - 2 q.x) over this lane's dwords.
-template <int VDW>
-__device__ __forceinline__ int partial_u8(const U8Vec<VDW> &q, const U8Vec<VDW> &x) {
+template <int VDW, bool EXACT>
+__device__ __forceinline__ int partial_u8(const U8Vec<VDW, EXACT> &q, const U8Vec<VDW, EXACT> &x) {
   int s = 0;
 #pragma unroll
   for (int t = 0; t < VDW; ++t) {
@@ -77,6 +93,33 @@ __device__ __forceinline__ uint64_t frontier_at(const uint64_t (&F)[KPL], uint32
   for (int r = 0; r < KPL; ++r)
     if ((uint32_t)r == e / kWave) v = readlane64(F[r], e % kWave);
   return v;
+}
+
+// Insert one key c (wave-uniform) by rank: slots at or above its rank move up
+// by one, the last slot falls off.  A key whose node is already in F is
+// dropped, so repeated evaluations never duplicate a frontier entry.
+template <int KPL>
+__device__ __forceinline__ void insert_key(uint64_t (&F)[KPL], uint64_t c) {
+  uint32_t rank = 0;
+  bool dup = false;
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) {
+    rank += (uint32_t)__popcll(ballot(F[r] < c));
+    dup |= ballot(F[r] != kInfKey && (F[r] >> 1) == (c >> 1)) != 0;
+  }
+  if (dup || rank >= (uint32_t)(KPL * kWave)) return;
+  uint64_t prev[KPL];
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) {
+    uint64_t fill = r == 0 ? kInfKey : readlane64(F[r == 0 ? 0 : r - 1], kWave - 1);
+    prev[r] = wave_shr1_64(F[r], fill);
+  }
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) {
+    const uint32_t e = r * kWave + l;
+    F[r] = e < rank ? F[r] : (e == rank ? c : prev[r]);
+  }
 }
 
 // Slow path after the visited filter forgot a node: a candidate may repeat a
@@ -107,9 +150,19 @@ __device__ __forceinline__ void merge_dedupe(uint64_t (&F)[KPL], uint64_t c_desc
   for (int r = 0; r < KPL; ++r) F[r] = big[r];
 }
 
-template <int KPL, int VDW, int HT_LOG2>
+// Up to this many keys below the L-th frontier key are inserted one by one;
+// more go through the sorting network.
+constexpr uint32_t kInsertMax = 12;
+
+template <int KPL, int VDW, bool EXACT, int HT_LOG2, bool N2S>
 __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
   using HT = VisitedLds<HT_LOG2>;
+  // vectors in flight per gather batch: 256 for up to 16 B per lane, fewer for wider rows
+  constexpr int kRounds = VDW <= 4 ? 32 : 128 / VDW;
+  constexpr int kBatch = kRounds * 8;
+  constexpr int kChunks = kBatch / kWave;
+  constexpr int kIdsPerLane = kCandCap / kWave;
+
   __shared__ uint32_t ht[HT::kSize];
   __shared__ uint32_t cand[kCandCap];
   __shared__ uint32_t beam[kMaxW];
@@ -118,13 +171,13 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
   const int g = l >> 3;
   const int gl = l & 7;
   const uint32_t dwords = p.D >> 2;
-  const uint32_t beams_per_group = kCandCap / p.R;
+  const uint32_t beams_per_group = min(kCandCap / p.R, (uint32_t)kWave);
 
   unsigned long long n_eval = 0, n_reeval = 0, n_exp = 0, n_iter = 0;
 
   for (uint32_t qi = blockIdx.x; qi < p.nq; qi += gridDim.x) {
     HT::clear(ht);
-    U8Vec<VDW> q;
+    U8Vec<VDW, EXACT> q;
     q.load(p.queries + (uint64_t)qi * p.D, gl, dwords);
     int qq = 0;
 #pragma unroll
@@ -140,10 +193,8 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
 #pragma unroll
     for (int r = 0; r < KPL; ++r) F[r] = kInfKey;
     {
-      uint32_t page, off;
-      locate(p.geom, p.entry, page, off);
-      U8Vec<VDW> x;
-      x.load(p.pages + page * p.geom.page_bytes + off, gl, dwords);
+      U8Vec<VDW, EXACT> x;
+      x.load(p.pages + record_offset(p.geom, slot_ct<N2S>(p.geom, p.entry)), gl, dwords);
       int d = sum8(partial_u8(q, x)) + qq;
       if (l == 0) {
         F[0] = ((uint64_t)(uint32_t)d << 32) | ((uint64_t)p.entry << 1);
@@ -177,71 +228,119 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
       ++n_iter;
 
       for (uint32_t b0 = 0; b0 < nbeam; b0 += beams_per_group) {
-        const uint32_t b1 = min(nbeam, b0 + beams_per_group);
-        // ---- expand + filter ------------------------------------------------
+        const uint32_t nb = min(nbeam - b0, beams_per_group);
+        const uint32_t nslots = nb * p.R;
+        // ---- expand: degrees (lane b) and all id slots of the group at once ---
+        // Loads are unconditional (lanes past the group read the group's first
+        // record) so that no branch separates them: one round trip in total.
+        const uint32_t my_beam = beam[b0 + min((uint32_t)l, nb - 1)];
+        const uint64_t my_rec = record_offset(p.geom, slot_ct<N2S>(p.geom, my_beam));
+        const uint32_t my_deg = *reinterpret_cast<const uint32_t *>(p.pages + my_rec + p.geom.vec_bytes);
+        uint32_t ids[kIdsPerLane];
+        uint32_t slot_beam[kIdsPerLane], slot_j[kIdsPerLane];
+#pragma unroll
+        for (int t = 0; t < kIdsPerLane; ++t) {
+          const uint32_t pos = min(t * kWave + (uint32_t)l, nslots - 1);
+          const uint32_t b = fastdiv(pos, p.Rdiv);
+          slot_beam[t] = b;
+          slot_j[t] = pos - b * p.R;
+        }
+#pragma unroll
+        for (int t = 0; t < kIdsPerLane; ++t) {
+          const uint64_t rec = __shfl(my_rec, (int)slot_beam[t]);
+          ids[t] = reinterpret_cast<const uint32_t *>(p.pages + rec + p.geom.vec_bytes + 4)[slot_j[t]];
+        }
+        bool valid[kIdsPerLane];
+#pragma unroll
+        for (int t = 0; t < kIdsPerLane; ++t) {
+          const uint32_t deg = min((uint32_t)__shfl((int)my_deg, (int)slot_beam[t]), p.R);
+          valid[t] = (uint32_t)(t * kWave + l) < nslots && slot_j[t] < deg && ids[t] < p.n;
+        }
+        // ---- filter through the visited table, compact the new ids ------------
+        bool isnew[kIdsPerLane], recorded[kIdsPerLane];
+        HT::template test_and_set_n<kIdsPerLane>(ht, ids, valid, ht_used < HT::kLimit, isnew, recorded);
         uint32_t cnt = 0;
-        for (uint32_t b = b0; b < b1; ++b) {
-          const uint32_t u = first_lane_value(beam[b]);
-          uint32_t page, off;
-          locate(p.geom, u, page, off);
-          const uint8_t *adj = p.pages + page * p.geom.page_bytes + off + p.geom.vec_bytes;
-          const uint32_t deg = min(*reinterpret_cast<const uint32_t *>(adj), p.R);
-          const uint32_t *ids = reinterpret_cast<const uint32_t *>(adj + 4);
-          for (uint32_t j0 = 0; j0 < p.R; j0 += kWave) {
-            const uint32_t j = j0 + l;
-            uint32_t v = j < deg ? ids[j] : kNoEdge;
-            bool valid = v < p.n;
-            bool recorded = false;
-            bool isnew = valid && HT::test_and_set(ht, v, ht_used < HT::kLimit, recorded);
-            uint64_t mnew = ballot(isnew);
-            uint64_t mrec = ballot(recorded);
-            if (isnew) cand[cnt + lanes_below(mnew)] = v;
-            cnt += (uint32_t)__popcll(mnew);
-            ht_used += (uint32_t)__popcll(mrec);
-            uint32_t lost = (uint32_t)__popcll(mnew & ~mrec);
-            n_reeval += lost;
-            forgot |= lost != 0;
-          }
+#pragma unroll
+        for (int t = 0; t < kIdsPerLane; ++t) {
+          const uint64_t mnew = ballot(isnew[t]);
+          const uint64_t mrec = ballot(recorded[t]);
+          if (isnew[t]) cand[cnt + lanes_below(mnew)] = ids[t];
+          cnt += (uint32_t)__popcll(mnew);
+          ht_used += (uint32_t)__popcll(mrec);
+          const uint32_t lost = (uint32_t)__popcll(mnew & ~mrec);
+          n_reeval += lost;
+          forgot |= lost != 0;
         }
         __syncthreads();
         n_eval += cnt;
 
-        // ---- evaluate + merge, 64 candidates at a time -----------------------
-        for (uint32_t c0 = 0; c0 < cnt; c0 += kWave) {
-          U8Vec<VDW> x[8];
+        // ---- evaluate: gather a batch of vectors in one round trip -------------
+        for (uint32_t c0 = 0; c0 < cnt; c0 += kBatch) {
+          // candidate node -> record; lanes past the count read the entry record
+          uint64_t rec[kRounds];
 #pragma unroll
-          for (int rr = 0; rr < 8; ++rr) {
+          for (int rr = 0; rr < kRounds; ++rr) {
+            if (c0 + rr * 8 >= cnt) break;
             const uint32_t idx = c0 + rr * 8 + g;
-            if (idx < cnt) {
-              uint32_t page, off;
-              locate(p.geom, cand[idx], page, off);
-              x[rr].load(p.pages + page * p.geom.page_bytes + off, gl, dwords);
-            } else {
-              x[rr].zero();
-            }
+            const uint32_t node = idx < cnt ? cand[idx] : p.entry;
+            rec[rr] = record_offset(p.geom, slot_ct<N2S>(p.geom, node));
           }
-          int mine = 0;
+          U8Vec<VDW, EXACT> x[kRounds];
 #pragma unroll
-          for (int rr = 0; rr < 8; ++rr) {
-            int d = sum8(partial_u8(q, x[rr])) + qq;
-            if (gl == rr) mine = d;
+          for (int rr = 0; rr < kRounds; ++rr) {
+            if (c0 + rr * 8 >= cnt) break;
+            x[rr].load(p.pages + rec[rr], gl, dwords);
           }
-          const uint32_t my_idx = c0 + gl * 8 + g;
-          uint64_t key = kInfKey;
-          if (my_idx < cnt) key = ((uint64_t)(uint32_t)mine << 32) | ((uint64_t)cand[my_idx] << 1);
-
-          // only keys below the current L-th frontier key can enter F
+          int dist[kChunks];
+#pragma unroll
+          for (int c = 0; c < kChunks; ++c) dist[c] = 0;
+#pragma unroll
+          for (int rr = 0; rr < kRounds; ++rr) {
+            if (c0 + rr * 8 >= cnt) break;
+            const int d = sum8(partial_u8(q, x[rr])) + qq;
+            if (gl == (rr & 7)) dist[rr / 8] = d;
+          }
+          // lane l of chunk c holds candidate c0 + 64c + 8*(l%8) + l/8
           const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
-          const bool pass = key < thr;
-          if (ballot(pass) == 0) continue;
-          uint64_t c[1] = {pass ? key : kInfKey};
-          bitonic_sort<1>(c, true);
-          if (!forgot) {
-            // no node can repeat: the P smallest of F and C are min(F, C reversed)
-            F[KPL - 1] = min64(F[KPL - 1], c[0]);
-            bitonic_merge_up<KPL>(F);
+          uint64_t key[kChunks];
+          uint64_t pass_mask[kChunks];
+          uint32_t survivors = 0;
+#pragma unroll
+          for (int c = 0; c < kChunks; ++c) {
+            const uint32_t my_idx = c0 + c * kWave + gl * 8 + g;
+            key[c] = my_idx < cnt ? (((uint64_t)(uint32_t)dist[c] << 32) | ((uint64_t)cand[my_idx] << 1))
+                                  : kInfKey;
+            const bool pass = key[c] < thr;
+            pass_mask[c] = ballot(pass);
+            if (!pass) key[c] = kInfKey;
+            survivors += (uint32_t)__popcll(pass_mask[c]);
+          }
+          if (survivors == 0) continue;
+          // ---- merge into the frontier ----------------------------------------
+          if (survivors <= kInsertMax) {
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+              uint64_t m = pass_mask[c];
+              while (m) {
+                const int lane = __builtin_ctzll(m);
+                m &= m - 1;
+                insert_key<KPL>(F, readlane64(key[c], lane));
+              }
+            }
           } else {
-            merge_dedupe<KPL>(F, c[0]);
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+              if (pass_mask[c] == 0) continue;
+              uint64_t cc[1] = {key[c]};
+              bitonic_sort<1>(cc, true);
+              if (!forgot) {
+                // no node can repeat: the P smallest of F and C are min(F, C reversed)
+                F[KPL - 1] = min64(F[KPL - 1], cc[0]);
+                bitonic_merge_up<KPL>(F);
+              } else {
+                merge_dedupe<KPL>(F, cc[0]);
+              }
+            }
           }
 #pragma unroll
           for (int r = 0; r < KPL; ++r)

@@ -84,8 +84,60 @@ __device__ __forceinline__ uint64_t max64(uint64_t a, uint64_t b) { return a < b
 // Bitonic networks over P = 64 * KPL keys held as v[r] at element r*64 + lane.
 // ---------------------------------------------------------------------------
 
+// Value of lane ^ M, M a power of two below 64, without the LDS crossbar:
+// DPP for M <= 8 (quad_perm, half-row mirror, row rotate), the gfx950
+// v_permlane16/32_swap for 16 and 32.
+template <int M>
+__device__ __forceinline__ uint32_t xor_lanes(uint32_t v) {
+  const int iv = (int)v;
+  if constexpr (M == 1) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, iv, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+  } else if constexpr (M == 2) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, iv, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  } else if constexpr (M == 4) {
+    int t = __builtin_amdgcn_update_dpp(0, iv, 0x141, 0xF, 0xF, false);          // i -> 7 - i in 8
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, t, 0x1B, 0xF, 0xF, false);   // reverse each quad
+  } else if constexpr (M == 8) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, iv, 0x128, 0xF, 0xF, false); // row_ror:8
+  } else if constexpr (M == 16) {
+    auto r = __builtin_amdgcn_permlane16_swap(iv, iv, false, false);
+    return (uint32_t)(((lane_id() >> 4) & 1) ? r[0] : r[1]);
+  } else {
+    static_assert(M == 32, "lane distance");
+    auto r = __builtin_amdgcn_permlane32_swap(iv, iv, false, false);
+    return (uint32_t)(lane_id() >= 32 ? r[0] : r[1]);
+  }
+}
+
+template <int M>
+__device__ __forceinline__ uint64_t xor_lanes64(uint64_t v) {
+  uint32_t lo = xor_lanes<M>((uint32_t)v);
+  uint32_t hi = xor_lanes<M>((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t xor_lanes64_rt(uint64_t v, int m) {
+  switch (m) {
+    case 1: return xor_lanes64<1>(v);
+    case 2: return xor_lanes64<2>(v);
+    case 4: return xor_lanes64<4>(v);
+    case 8: return xor_lanes64<8>(v);
+    case 16: return xor_lanes64<16>(v);
+    default: return xor_lanes64<32>(v);
+  }
+}
+
+// Value of lane - 1 for a whole wave (DPP wave_shr:1); lane 0 gets `fill`.
+__device__ __forceinline__ uint64_t wave_shr1_64(uint64_t v, uint64_t fill) {
+  uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)fill, (int)(uint32_t)v, 0x138, 0xF, 0xF, false);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(fill >> 32), (int)(uint32_t)(v >> 32), 0x138,
+                                                      0xF, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // One compare-exchange stage with partner distance j.  Element e keeps the
 // smaller key when (e is the lower of the pair) == (its block sorts upward).
+// j and k are compile-time constants after unrolling.
 template <int KPL>
 __device__ __forceinline__ void bitonic_stage(uint64_t (&v)[KPL], int j, int k, bool descending) {
   const int l = lane_id();
@@ -106,7 +158,7 @@ __device__ __forceinline__ void bitonic_stage(uint64_t (&v)[KPL], int j, int k, 
       const int e = r * kWave + l;
       bool up = ((e & k) == 0) != descending;
       bool lower = (l & j) == 0;
-      uint64_t o = shfl_xor64(v[r], j);
+      uint64_t o = xor_lanes64_rt(v[r], j);
       v[r] = (lower == up) ? min64(v[r], o) : max64(v[r], o);
     }
   }

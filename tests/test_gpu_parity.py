@@ -147,10 +147,10 @@ def test_unreachable_and_padding(orc, torch_dev):
     assert (gi[:, 5:] == NO_EDGE).all() and (gd[:, 5:] == 2 ** 31 - 1).all()
 
 
-def test_visited_filter_overflow_still_exact(orc, torch_dev, monkeypatch):
-    """A small visited table forgets nodes: re-evaluations happen, results do not change."""
-    monkeypatch.setenv("GORIO_HT_LOG2", "12")
-    spec = IndexSpec(n=20000, D=64, dtype="u8", clusters=8, sigma=20.0, r_near=32, r_rand=32, seed=9)
+def test_visited_filter_overflow_still_exact(orc, torch_dev):
+    """A search that outgrows the visited table forgets nodes: re-evaluations
+    happen, results and expansion counts do not change."""
+    spec = IndexSpec(n=60000, D=64, dtype="u8", clusters=8, sigma=20.0, r_near=32, r_rand=32, seed=9)
     a = index_arrays(spec, use_cache=False)
     q = query_array(spec, QuerySpec(64, 10))
     _, st = check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 256, 8)
