@@ -158,4 +158,70 @@ struct VisitedLds {
   }
 };
 
+// Visited filter of a parked-capable query: the same open addressing in
+// HBM.  Only its owning wave touches it; lookups use agent-scope atomic loads
+// so that a line cached in the CU's L1 before an atomic update is never read.
+template <int LOG2>
+struct VisitedHbm {
+  static constexpr uint32_t kSize = 1u << LOG2;
+  static constexpr uint32_t kLimit = kSize - kSize / 4;
+  static constexpr int kMaxProbe = 64;
+
+  __device__ __forceinline__ static uint32_t hash(uint32_t id) {
+    return (id * 0x9E3779B1u) >> (32 - LOG2);
+  }
+
+  // Plain stores, then an agent-scope fence so later atomics see them.
+  __device__ __forceinline__ static void clear(uint32_t *t) {
+    uint4 *t4 = reinterpret_cast<uint4 *>(t);
+    const uint4 e = make_uint4(kHtEmpty, kHtEmpty, kHtEmpty, kHtEmpty);
+    for (uint32_t i = lane_id(); i < kSize / 4; i += kWave) t4[i] = e;
+    __threadfence();
+  }
+
+  template <int N>
+  __device__ __forceinline__ static void test_and_set_n(uint32_t *t, const uint32_t (&ids)[N],
+                                                        const bool (&valid)[N], bool may_store,
+                                                        bool (&isnew)[N], bool (&recorded)[N]) {
+    uint32_t h[N];
+    bool pend[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      h[i] = hash(ids[i]);
+      pend[i] = valid[i];
+      isnew[i] = false;
+      recorded[i] = false;
+    }
+    for (int p = 0; p < kMaxProbe; ++p) {
+      bool any = false;
+#pragma unroll
+      for (int i = 0; i < N; ++i) any |= pend[i];
+      if (ballot(any) == 0) break;
+      uint32_t old[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        if (pend[i])
+          old[i] = may_store ? atomicCAS(&t[h[i]], kHtEmpty, ids[i])
+                             : __hip_atomic_load(&t[h[i]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        if (!pend[i]) continue;
+        if (old[i] == kHtEmpty) {
+          isnew[i] = true;
+          recorded[i] = may_store;
+          pend[i] = false;
+        } else if (old[i] == ids[i]) {
+          pend[i] = false;
+        } else {
+          h[i] = (h[i] + 1) & (kSize - 1);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (pend[i]) isnew[i] = true;
+  }
+};
+
 }  // namespace gorio

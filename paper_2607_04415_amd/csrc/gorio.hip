@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <chrono>
 #include <cstdio>
+#include <thread>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -11,6 +12,7 @@
 #include "../../include/gorio.h"
 #include "build_kernels.hpp"
 #include "index.hpp"
+#include "search_paged.hpp"
 #include "search_resident.hpp"
 
 using namespace gorio;
@@ -205,6 +207,77 @@ extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors
 }
 
 // ---------------------------------------------------------------------------
+// paged mode: memory
+// ---------------------------------------------------------------------------
+namespace {
+constexpr uint32_t kMaxPendingPerQuery = 32;  // page requests one query keeps outstanding
+
+uint32_t next_pow2(uint64_t v) {
+  uint32_t p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+template <class T>
+hipError_t host_ring(T **h, T **d, size_t count) {
+  hipError_t e = hipHostMalloc(reinterpret_cast<void **>(h), count * sizeof(T),
+                               hipHostMallocCoherent | hipHostMallocMapped);
+  if (e != hipSuccess) return e;
+  memset(*h, 0, count * sizeof(T));
+  return hipHostGetDevicePointer(reinterpret_cast<void **>(d), *h, 0);
+}
+}  // namespace
+
+gorio_status gorio_index::make_paged(uint64_t slots) {
+  using namespace gorio;
+  if (slots < 2ull * kMaxPendingPerQuery)
+    return fail(GORIO_EINVAL, "a paged cache needs at least %u slots (asked for %llu)",
+                2 * kMaxPendingPerQuery, (unsigned long long)slots);
+  if (slots >= (1ull << 30)) return fail(GORIO_EINVAL, "too many cache slots");
+  if (resident) {
+    hipError_t e = hipHostMalloc(reinterpret_cast<void **>(&h_backing), index_bytes(), hipHostMallocDefault);
+    if (e != hipSuccess)
+      return fail(GORIO_ENOMEM, "pinned backing store of %llu bytes failed", (unsigned long long)index_bytes());
+    e = hipMemcpy(h_backing, d_pages, index_bytes(), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(GORIO_EDEVICE, "page download failed: %s", hipGetErrorString(e));
+    (void)hipFree(d_pages);
+    d_pages = nullptr;
+    resident = false;
+  }
+  if (paged) paged->release();
+  paged = std::make_unique<PagedState>();
+  PagedState &P = *paged;
+  P.slots = slots;
+  HIP_OR_FAIL(hipMalloc(&P.d_cache, slots * (uint64_t)page_bytes));
+  HIP_OR_FAIL(hipMalloc(&P.d_slot_word, slots * sizeof(unsigned long long)));
+  HIP_OR_FAIL(hipMalloc(&P.d_page_slot, num_pages * sizeof(uint32_t)));
+  HIP_OR_FAIL(hipMalloc(&P.d_ctrl, PagedState::kCtrlWords * sizeof(unsigned long long)));
+  P.ring_cap = next_pow2(2 * slots + 1024);
+  HIP_OR_FAIL(host_ring(&P.h_mq, &P.d_mq, P.ring_cap));
+  HIP_OR_FAIL(host_ring(&P.h_cq, &P.d_cq, P.ring_cap));
+  HIP_OR_FAIL(host_ring(&P.h_cq_tail, &P.d_cq_tail, 8));
+  HIP_OR_FAIL(host_ring(&P.h_abort, &P.d_abort, 16));
+  cache_slots = slots;
+  gorio_status st = reset_cache();
+  if (st != GORIO_OK) return st;
+  P.proxy.start(P.h_mq, P.ring_cap - 1, P.h_cq, P.ring_cap - 1, P.h_cq_tail);
+  return GORIO_OK;
+}
+
+// Empty the cache (every slot EMPTY, no page mapped).
+gorio_status gorio_index::reset_cache() {
+  using namespace gorio;
+  PagedState &P = *paged;
+  fill_u32<<<grid_for(P.slots * 2, 256), 256, 0, stream>>>(reinterpret_cast<uint32_t *>(P.d_slot_word),
+                                                           P.slots * 2, 0u);
+  fill_u32<<<grid_for(num_pages, 256), 256, 0, stream>>>(P.d_page_slot, num_pages, 0xFFFFFFFFu);
+  fill_u32<<<1, 64, 0, stream>>>(reinterpret_cast<uint32_t *>(P.d_ctrl), 2 * PagedState::kCtrlWords, 0u);
+  HIP_OR_FAIL(hipGetLastError());
+  HIP_OR_FAIL(hipStreamSynchronize(stream));
+  return GORIO_OK;
+}
+
+// ---------------------------------------------------------------------------
 // cache / backing configuration
 // ---------------------------------------------------------------------------
 extern "C" gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes) {
@@ -271,6 +344,148 @@ int env_int(const char *name, int dflt) {
 
 }  // namespace
 
+namespace {
+
+template <int KPL, int VDW, bool EXACT, bool N2S>
+hipError_t launch_paged_t(const PagedParams &pp, int grid, size_t lds, hipStream_t s) {
+  auto k = search_paged_u8<KPL, VDW, EXACT, N2S>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  k<<<grid, kWave, lds, s>>>(pp);
+  return hipGetLastError();
+}
+
+template <int KPL>
+size_t qslot_bytes() { return sizeof(QSlot<KPL>); }
+
+template <int KPL, int VDW, bool EXACT>
+hipError_t launch_paged_n2s(const PagedParams &pp, int grid, size_t lds, hipStream_t s) {
+  if (pp.geom.node_to_slot) return launch_paged_t<KPL, VDW, EXACT, true>(pp, grid, lds, s);
+  return launch_paged_t<KPL, VDW, EXACT, false>(pp, grid, lds, s);
+}
+
+template <int KPL>
+hipError_t launch_paged_kpl(const PagedParams &pp, int grid, hipStream_t s) {
+  const size_t lds = pp.oversub * qslot_bytes<KPL>();
+  if (pp.D == 128) return launch_paged_n2s<KPL, 4, true>(pp, grid, lds, s);
+  const uint32_t vdw = (pp.D / 4 + 7) / 8;
+  if (vdw <= 1) return launch_paged_n2s<KPL, 1, false>(pp, grid, lds, s);
+  if (vdw <= 4) return launch_paged_n2s<KPL, 4, false>(pp, grid, lds, s);
+  return launch_paged_n2s<KPL, 16, false>(pp, grid, lds, s);
+}
+
+// Paged search: reset the per-search rings and counters, arm the proxy,
+// launch the persistent kernel and wait for it under a watchdog.
+gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s, bool &timed_out) {
+  PagedState &P = *ix->paged;
+  const uint32_t oversub = ix->blocking ? 1u : ix->oversub;
+  int dev = 0, cus = 0;
+  HIP_OR_FAIL(hipGetDevice(&dev));
+  HIP_OR_FAIL(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  // concurrent queries: each may hold kMaxPendingPerQuery pins, kept within
+  // half the cache so the clock always finds victims for the rest
+  const uint64_t q_cache = std::max<uint64_t>(1, P.slots / (2ull * kMaxPendingPerQuery));
+  const uint64_t q_live = std::min<uint64_t>({(uint64_t)cus * 8 * oversub, q_cache, rp.nq});
+  const int grid = (int)std::max<uint64_t>(1, (q_live + oversub - 1) / oversub);
+  const uint64_t ht_entries = (uint64_t)grid * oversub << kPagedHtLog2;
+  if (ht_entries > P.ht_pool_entries) {
+    if (P.d_ht_pool) (void)hipFree(P.d_ht_pool);
+    P.d_ht_pool = nullptr;
+    P.ht_pool_entries = 0;
+    HIP_OR_FAIL(hipMalloc(&P.d_ht_pool, ht_entries * sizeof(uint32_t)));
+    P.ht_pool_entries = ht_entries;
+  }
+  // per-search reset: rings empty, indices zero (the clock hand and the cached
+  // pages stay: a warm cache carries over to the next search)
+  memset(P.h_mq, 0, P.ring_cap * sizeof(unsigned long long));
+  __atomic_store_n(P.h_cq_tail, 0ull, __ATOMIC_RELEASE);
+  __atomic_store_n(P.h_abort, 0u, __ATOMIC_RELEASE);
+  fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(P.d_ctrl + PagedState::kMqTail),
+                            2 * (PagedState::kCtrlWords - PagedState::kMqTail), 0u);
+
+  PagedParams pp;
+  pp.cache.data = P.d_cache;
+  pp.cache.slot_word = P.d_slot_word;
+  pp.cache.page_slot = P.d_page_slot;
+  pp.cache.clock_hand = P.d_ctrl + PagedState::kClock;
+  pp.cache.slots = (uint32_t)P.slots;
+  pp.cache.page_bytes = ix->page_bytes;
+  pp.cache.mq = P.d_mq;
+  pp.cache.mq_mask = P.ring_cap - 1;
+  pp.cache.mq_tail = P.d_ctrl + PagedState::kMqTail;
+  pp.geom = rp.geom;
+  pp.n = rp.n;
+  pp.D = rp.D;
+  pp.R = rp.R;
+  pp.Rdiv = rp.Rdiv;
+  pp.entry = rp.entry;
+  pp.num_pages = (uint32_t)ix->num_pages;
+  uint8_t *d_backing = nullptr;
+  HIP_OR_FAIL(hipHostGetDevicePointer(reinterpret_cast<void **>(&d_backing), ix->h_backing, 0));
+  pp.backing = d_backing;
+  pp.cq = P.d_cq;
+  pp.cq_mask = P.ring_cap - 1;
+  pp.cq_tail = P.d_cq_tail;
+  pp.cq_head = P.d_ctrl + PagedState::kCqHead;
+  pp.tail_seen = P.d_ctrl + PagedState::kTailSeen;
+  pp.poll_lock = reinterpret_cast<unsigned int *>(P.d_ctrl + PagedState::kPollLock);
+  pp.abort_flag = P.d_abort;
+  pp.abort_seen = reinterpret_cast<unsigned int *>(P.d_ctrl + PagedState::kAbortSeen);
+  pp.queries = rp.queries;
+  pp.nq = rp.nq;
+  pp.k = rp.k;
+  pp.L = rp.L;
+  pp.W = rp.W;
+  pp.next_query = reinterpret_cast<unsigned int *>(P.d_ctrl + PagedState::kNextQuery);
+  pp.out_ids = rp.out_ids;
+  pp.out_dists = rp.out_dists;
+  pp.ht_pool = P.d_ht_pool;
+  pp.oversub = oversub;
+  pp.max_pending = kMaxPendingPerQuery;
+  pp.blocking = ix->blocking;
+  pp.stats = rp.stats;
+
+  P.proxy.begin(ix->latency_us, ix->max_outstanding);
+  HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+  hipError_t le;
+  if (rp.L <= 64) le = launch_paged_kpl<1>(pp, grid, s);
+  else if (rp.L <= 128) le = launch_paged_kpl<2>(pp, grid, s);
+  else le = launch_paged_kpl<4>(pp, grid, s);
+  if (le != hipSuccess) {
+    P.proxy.end();
+    return fail(GORIO_EDEVICE, "paged search launch failed: %s", hipGetErrorString(le));
+  }
+  HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+  // watchdog: the kernel polls the abort flag (through its device mirror)
+  const double limit_s = env_int("GORIO_WATCHDOG_S", 120);
+  const auto t0 = std::chrono::steady_clock::now();
+  for (;;) {
+    hipError_t q = hipEventQuery(ix->ev_stop);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) {
+      P.proxy.end();
+      return fail(GORIO_EDEVICE, "paged search failed: %s", hipGetErrorString(q));
+    }
+    const double el = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    if (!timed_out && el > limit_s) {
+      timed_out = true;
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+    }
+    std::this_thread::sleep_for(std::chrono::microseconds(200));
+  }
+  P.proxy.end();
+  if (timed_out) {
+    gorio_status rs = ix->reset_cache();  // pins and LOADING slots of aborted queries
+    if (rs != GORIO_OK) return rs;
+  }
+  return GORIO_OK;
+}
+
+}  // namespace
+
 extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq, uint32_t k,
                                      uint32_t L, uint32_t W, uint32_t *ids, void *dists,
                                      gorio_stats *stats, void *stream) {
@@ -283,7 +498,8 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   if (nq == 0) return GORIO_OK;
   if (!queries || !ids || !dists) return fail(GORIO_EINVAL, "queries, ids and dists must be non-NULL");
   if (ix->dtype != GORIO_U8) return fail(GORIO_EUNSUPPORTED, "float32 search is not built yet");
-  if (!ix->resident) return fail(GORIO_EUNSUPPORTED, "paged search is not built yet");
+  if (!ix->resident && W > (uint32_t)kPagedMaxW)
+    return fail(GORIO_EUNSUPPORTED, "paged search supports W <= %d (W=%u)", kPagedMaxW, W);
 
   DeviceGuard dg(ix->device);
   if (!dg.ok) return fail(GORIO_EDEVICE, "cannot select device %d", ix->device);
@@ -325,13 +541,20 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   p.out_dists = static_cast<int32_t *>(d_dists);
   p.stats = ix->d_stats;
 
-  const int ht_log2 = env_int("GORIO_HT_LOG2", 13);
-  const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
-  HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
-  gorio_status st = launch_resident(p, ht_log2, grid, s);
-  if (st != GORIO_OK) return st;
-  HIP_OR_FAIL(hipGetLastError());
-  HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+  gorio_status st;
+  bool timed_out = false;
+  if (ix->resident) {
+    const int ht_log2 = env_int("GORIO_HT_LOG2", 13);
+    const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
+    HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+    st = launch_resident(p, ht_log2, grid, s);
+    if (st != GORIO_OK) return st;
+    HIP_OR_FAIL(hipGetLastError());
+    HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+  } else {
+    st = run_paged(ix, p, s, timed_out);
+    if (st != GORIO_OK) return st;
+  }
 
   if (!i_dev) HIP_OR_FAIL(hipMemcpyAsync(ids, d_ids, obytes, hipMemcpyDeviceToHost, s));
   if (!d_dev) HIP_OR_FAIL(hipMemcpyAsync(dists, d_dists, obytes, hipMemcpyDeviceToHost, s));
@@ -346,8 +569,15 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
     stats->reevaluations = h_stats[kStatReeval];
     stats->expansions = h_stats[kStatExp];
     stats->iterations = h_stats[kStatIter];
+    stats->hits = h_stats[kStatHit];
+    stats->misses = h_stats[kStatMiss];
+    stats->pages_served = h_stats[kStatServed];
+    stats->bytes_served = h_stats[kStatServed] * ix->page_bytes;
+    stats->parks = h_stats[kStatPark];
+    stats->resumes = h_stats[kStatResume];
     stats->wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
   }
+  if (timed_out) return fail(GORIO_ETIMEOUT, "paged search made no progress within the watchdog limit");
   return GORIO_OK;
 }
 

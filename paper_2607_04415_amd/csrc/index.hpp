@@ -9,6 +9,7 @@
 
 #include "../../include/gorio.h"
 #include "common.hpp"
+#include "proxy.hpp"
 
 namespace gorio {
 
@@ -27,6 +28,52 @@ enum StatWord : int {
   kStatWords = 16
 };
 
+// Device and host memory of the paged mode (one per index, sized by set_cache).
+struct PagedState {
+  uint64_t slots = 0;
+  uint8_t *d_cache = nullptr;                 // slots * page_bytes
+  unsigned long long *d_slot_word = nullptr;  // slots
+  uint32_t *d_page_slot = nullptr;            // num_pages
+  // device control words (one allocation): clock hand, mq tail, cq head,
+  // tail mirror, poll lock, abort mirror, next query
+  unsigned long long *d_ctrl = nullptr;
+  // host rings (coherent pinned memory) and their device-visible addresses
+  unsigned long long *h_mq = nullptr, *d_mq = nullptr;
+  unsigned long long *h_cq = nullptr, *d_cq = nullptr;
+  unsigned long long *h_cq_tail = nullptr, *d_cq_tail = nullptr;
+  unsigned int *h_abort = nullptr, *d_abort = nullptr;
+  uint32_t ring_cap = 0;
+  uint32_t *d_ht_pool = nullptr;
+  uint64_t ht_pool_entries = 0;
+  Proxy proxy;
+
+  enum Ctrl { kClock = 0, kMqTail, kCqHead, kTailSeen, kPollLock, kAbortSeen, kNextQuery, kCtrlWords = 8 };
+
+  void release() {
+    proxy.stop();
+    if (d_cache) (void)hipFree(d_cache);
+    if (d_slot_word) (void)hipFree(d_slot_word);
+    if (d_page_slot) (void)hipFree(d_page_slot);
+    if (d_ctrl) (void)hipFree(d_ctrl);
+    if (d_ht_pool) (void)hipFree(d_ht_pool);
+    if (h_mq) (void)hipHostFree(h_mq);
+    if (h_cq) (void)hipHostFree(h_cq);
+    if (h_cq_tail) (void)hipHostFree(h_cq_tail);
+    if (h_abort) (void)hipHostFree(h_abort);
+    d_cache = nullptr;
+    d_slot_word = nullptr;
+    d_page_slot = nullptr;
+    d_ctrl = nullptr;
+    d_ht_pool = nullptr;
+    h_mq = d_mq = h_cq = d_cq = h_cq_tail = d_cq_tail = nullptr;
+    h_abort = d_abort = nullptr;
+    slots = 0;
+    ring_cap = 0;
+    ht_pool_entries = 0;
+  }
+  ~PagedState() { release(); }
+};
+
 }  // namespace gorio
 
 struct gorio_index {
@@ -43,6 +90,8 @@ struct gorio_index {
   uint8_t *d_pages = nullptr;    // resident mode: packed pages in HBM
   uint8_t *h_backing = nullptr;  // paged mode: packed pages in pinned host memory
   uint64_t cache_slots = 0;
+
+  std::unique_ptr<gorio::PagedState> paged;
 
   double latency_us = 0.0;
   uint32_t max_outstanding = 4096;
@@ -75,29 +124,21 @@ struct gorio_index {
     if (e != hipSuccess) return gorio::fail(GORIO_EDEVICE, "page upload failed: %s", hipGetErrorString(e));
     (void)hipHostFree(h_backing);
     h_backing = nullptr;
+    if (paged) paged->release();
+    paged.reset();
     cache_slots = 0;
     resident = true;
     return GORIO_OK;
   }
 
-  // Pages to the pinned host backing store; the HBM copy is released.
-  gorio_status make_paged(uint64_t slots) {
-    if (slots == 0) return gorio::fail(GORIO_EINVAL, "a paged cache needs at least one slot");
-    if (resident) {
-      hipError_t e = hipHostMalloc(reinterpret_cast<void **>(&h_backing), index_bytes(), hipHostMallocDefault);
-      if (e != hipSuccess) return gorio::fail(GORIO_ENOMEM, "pinned backing store of %llu bytes failed",
-                                              (unsigned long long)index_bytes());
-      e = hipMemcpy(h_backing, d_pages, index_bytes(), hipMemcpyDeviceToHost);
-      if (e != hipSuccess) return gorio::fail(GORIO_EDEVICE, "page download failed: %s", hipGetErrorString(e));
-      (void)hipFree(d_pages);
-      d_pages = nullptr;
-      resident = false;
-    }
-    cache_slots = slots;
-    return GORIO_OK;
-  }
+  // Pages to the pinned host backing store (the HBM copy is released) and an
+  // empty HBM cache of `slots` pages.  Defined in gorio.hip.
+  gorio_status make_paged(uint64_t slots);
+  gorio_status reset_cache();
 
   void release_all() {
+    if (paged) paged->release();
+    paged.reset();
     if (d_pages) (void)hipFree(d_pages);
     if (h_backing) (void)hipHostFree(h_backing);
     if (d_node_to_slot) (void)hipFree(d_node_to_slot);

@@ -1,0 +1,113 @@
+// Host transport proxy: descriptor intake, deadline queue, completion publish.
+#include "proxy.hpp"
+
+#include <chrono>
+#include <deque>
+#include <utility>
+
+#if defined(__x86_64__)
+#include <immintrin.h>
+#define GORIO_PAUSE() _mm_pause()
+#else
+#define GORIO_PAUSE() std::this_thread::yield()
+#endif
+
+namespace gorio {
+
+namespace {
+uint64_t now_ns() {
+  return (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+             std::chrono::steady_clock::now().time_since_epoch())
+      .count();
+}
+}  // namespace
+
+void Proxy::start(unsigned long long *mq, uint32_t mq_mask, unsigned long long *cq, uint32_t cq_mask,
+                  unsigned long long *cq_tail) {
+  stop();
+  mq_ = mq;
+  mq_mask_ = mq_mask;
+  cq_ = cq;
+  cq_mask_ = cq_mask;
+  cq_tail_ = cq_tail;
+  quit_.store(false);
+  active_.store(false);
+  th_ = std::thread([this] { loop(); });
+}
+
+void Proxy::begin(double latency_us, uint32_t max_outstanding) {
+  latency_ns_.store((uint64_t)(latency_us * 1000.0));
+  max_outstanding_.store(max_outstanding ? max_outstanding : 4096);
+  requests_.store(0);
+  completed_.store(0);
+  max_in_flight_.store(0);
+  epoch_.fetch_add(1);
+  active_.store(true, std::memory_order_release);
+}
+
+void Proxy::end() {
+  active_.store(false, std::memory_order_release);
+  // wait until the thread has left its serving iteration: nothing it does can
+  // land in the rings after this returns
+  while (th_.joinable() && !idle_.load(std::memory_order_acquire)) std::this_thread::yield();
+}
+
+void Proxy::stop() {
+  if (th_.joinable()) {
+    quit_.store(true);
+    th_.join();
+  }
+}
+
+void Proxy::loop() {
+  // (descriptor, due time); latency is the same for every request, so FIFO
+  // order is deadline order
+  std::deque<std::pair<unsigned long long, uint64_t>> fifo;
+  uint64_t head = 0, tail = 0, epoch = ~0ull;
+  while (!quit_.load(std::memory_order_relaxed)) {
+    if (!active_.load(std::memory_order_acquire)) {
+      idle_.store(true, std::memory_order_release);
+      std::this_thread::sleep_for(std::chrono::microseconds(50));
+      continue;
+    }
+    idle_.store(false, std::memory_order_release);
+    if (!active_.load(std::memory_order_acquire)) continue;  // end() raced with the flag above
+    if (epoch != epoch_.load()) {  // a new search: rings were reset by the host
+      epoch = epoch_.load();
+      fifo.clear();
+      head = tail = 0;
+    }
+    const uint64_t lat = latency_ns_.load(std::memory_order_relaxed);
+    const uint32_t cap = max_outstanding_.load(std::memory_order_relaxed);
+    const uint64_t now = now_ns();
+    uint32_t intake = 0;
+    while (fifo.size() < cap) {
+      unsigned long long *slot = &mq_[head & mq_mask_];
+      const unsigned long long e = __atomic_load_n(slot, __ATOMIC_ACQUIRE);
+      if (e == 0) break;
+      __atomic_store_n(slot, 0ull, __ATOMIC_RELAXED);
+      ++head;
+      fifo.emplace_back(e, now + lat);
+      ++intake;
+    }
+    if (intake) {
+      requests_.fetch_add(intake, std::memory_order_relaxed);
+      if (fifo.size() > max_in_flight_.load(std::memory_order_relaxed))
+        max_in_flight_.store(fifo.size(), std::memory_order_relaxed);
+    }
+    uint32_t done = 0;
+    while (!fifo.empty() && fifo.front().second <= now) {
+      cq_[(tail + done) & cq_mask_] = fifo.front().first;
+      fifo.pop_front();
+      ++done;
+    }
+    if (done) {
+      tail += done;
+      __atomic_store_n(cq_tail_, (unsigned long long)tail, __ATOMIC_RELEASE);
+      completed_.fetch_add(done, std::memory_order_relaxed);
+    }
+    if (!intake && !done) GORIO_PAUSE();
+  }
+}
+
+}  // namespace gorio

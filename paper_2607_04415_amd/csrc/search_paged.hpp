@@ -1,0 +1,591 @@
+// Paged beam search: a persistent kernel whose waves own query slots and
+// overlap traversal with page service (GORIO Sec. 3.2 and Sec. 3.3).
+//
+// Each wave owns `oversub` query slots kept in its LDS (frontier, beam,
+// candidate list, per-item wait state) plus a visited table in HBM.  The
+// wave's scheduler loop
+//   - admits a new query into a free slot (global atomic counter),
+//   - resumes a parked query when a page it waits on is READY in the cache
+//     (the per-slot ready test of Sec. 3.2) or when it can issue more requests,
+//   - otherwise claims completions from the proxy's ring and fills the pages
+//     (copies 4 KB from the pinned backing store into the HBM slot), then
+//     marks them READY.
+// A query runs its iteration (select -> expand -> evaluate -> merge) until a
+// record it needs is not resident: the miss is published as a descriptor
+// {page, slot}, the slot stays pinned, and the query is parked.  An
+// iteration's next beam is selected only after every candidate of the
+// current one is evaluated, so results equal the resident search's.
+//
+// blocking = 1 replaces split-phase service with wait-in-place: one query per
+// wave and one outstanding page per lane (the blocking demand-paging path the
+// paper compares against).
+#pragma once
+
+#include "frontier.hpp"
+#include "page_cache.hpp"
+
+namespace gorio {
+
+constexpr int kPagedMaxW = 64;
+constexpr uint32_t kTodo = 0xFFFFFFFFu;  // item not requested yet
+constexpr uint32_t kDone = 0xFFFFFFFEu;  // item handled; other values: waiting on that cache slot
+constexpr int kPagedHtLog2 = 13;
+constexpr uint32_t kFillBatch = 8;
+
+enum : uint32_t { kPhSelect = 0, kPhExpand = 1, kPhEval = 2 };
+
+struct PagedParams {
+  CacheView cache;
+  PageGeom geom;  // record geometry inside a page (page_bytes, record_bytes, rpp, node_to_slot)
+  uint32_t n, D, R;
+  FastDiv Rdiv;
+  uint32_t entry;
+  uint32_t num_pages;
+  const uint8_t *backing;                 // pinned host copy of every page
+  const unsigned long long *cq;           // completions from the proxy (host memory)
+  uint32_t cq_mask;
+  const unsigned long long *cq_tail;      // proxy's publish index (host memory)
+  unsigned long long *cq_head;            // next completion to claim (device)
+  unsigned long long *tail_seen;          // device mirror of cq_tail
+  unsigned int *poll_lock;                // device: one wave at a time reads host memory
+  const unsigned int *abort_flag;         // host memory; nonzero ends the search
+  unsigned int *abort_seen;               // device mirror of abort_flag
+  const uint8_t *queries;
+  uint32_t nq, k, L, W;
+  unsigned int *next_query;
+  uint32_t *out_ids;
+  int32_t *out_dists;
+  uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
+  uint32_t oversub, max_pending;
+  int blocking;
+  unsigned long long *stats;              // [eval, reeval, exp, iter, hit, miss, served, park, resume, bad]
+};
+
+template <int KPL>
+struct QSlot {
+  uint64_t F[KPL * kWave];
+  uint32_t beam[kPagedMaxW];
+  uint32_t bstate[kPagedMaxW];
+  uint32_t cand[kCandCap];
+  uint32_t cstate[kCandCap];
+  uint32_t qi, active, phase, nbeam, b0, ncand, ht_used, forgot, parked;
+};
+
+struct PagedCounters {
+  unsigned long long eval = 0, reeval = 0, exp = 0, iter = 0, hit = 0, miss = 0, served = 0,
+                     park = 0, resume = 0;
+};
+
+__device__ __forceinline__ bool aborted(const PagedParams &p) {
+  return __hip_atomic_load(p.abort_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+}
+
+// Record of node v inside cache slot s.
+template <bool N2S>
+__device__ __forceinline__ const uint8_t *cached_record(const PagedParams &p, uint32_t s, uint32_t v) {
+  const uint32_t sl = slot_ct<N2S>(p.geom, v);
+  const uint32_t within = sl - fastdiv(sl, p.geom.rpp) * p.geom.rpp.d;
+  return p.cache.data + (uint64_t)s * p.cache.page_bytes + within * p.geom.record_bytes;
+}
+
+template <bool N2S>
+__device__ __forceinline__ uint32_t page_of(const PagedParams &p, uint32_t v) {
+  return fastdiv(slot_ct<N2S>(p.geom, v), p.geom.rpp);
+}
+
+// Copy the 4 KB pages of completions i0 .. i0+3 (those below n; entry i in
+// lane i of e) from the backing store into their cache slots: 16 loads in
+// flight per lane, then the stores.  Kept out of line so the copy gets its
+// own registers.
+__device__ __attribute__((noinline)) void copy_pages4(const uint8_t *backing, uint8_t *cache,
+                                                      unsigned long long e, uint32_t i0, uint32_t n) {
+  const int l = lane_id();
+  const uint32_t i1 = min(i0 + 1, n - 1), i2 = min(i0 + 2, n - 1), i3 = min(i0 + 3, n - 1);
+  const uint64_t e0 = readlane64(e, i0), e1 = readlane64(e, i1), e2 = readlane64(e, i2), e3 = readlane64(e, i3);
+  const uint4 *s0 = reinterpret_cast<const uint4 *>(backing + (uint64_t)((uint32_t)(e0 >> 32) - 1u) * 4096u);
+  const uint4 *s1 = reinterpret_cast<const uint4 *>(backing + (uint64_t)((uint32_t)(e1 >> 32) - 1u) * 4096u);
+  const uint4 *s2 = reinterpret_cast<const uint4 *>(backing + (uint64_t)((uint32_t)(e2 >> 32) - 1u) * 4096u);
+  const uint4 *s3 = reinterpret_cast<const uint4 *>(backing + (uint64_t)((uint32_t)(e3 >> 32) - 1u) * 4096u);
+  const uint4 a0 = s0[l], a1 = s0[l + 64], a2 = s0[l + 128], a3 = s0[l + 192];
+  const uint4 b0 = s1[l], b1 = s1[l + 64], b2 = s1[l + 128], b3 = s1[l + 192];
+  const uint4 c0 = s2[l], c1 = s2[l + 64], c2 = s2[l + 128], c3 = s2[l + 192];
+  const uint4 d0 = s3[l], d1 = s3[l + 64], d2 = s3[l + 128], d3 = s3[l + 192];
+  uint4 *t0 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e0 * 4096u);
+  t0[l] = a0; t0[l + 64] = a1; t0[l + 128] = a2; t0[l + 192] = a3;
+  if (i0 + 1 < n) {
+    uint4 *t1 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e1 * 4096u);
+    t1[l] = b0; t1[l + 64] = b1; t1[l + 128] = b2; t1[l + 192] = b3;
+  }
+  if (i0 + 2 < n) {
+    uint4 *t2 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e2 * 4096u);
+    t2[l] = c0; t2[l + 64] = c1; t2[l + 128] = c2; t2[l + 192] = c3;
+  }
+  if (i0 + 3 < n) {
+    uint4 *t3 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e3 * 4096u);
+    t3[l] = d0; t3[l + 64] = d1; t3[l + 128] = d2; t3[l + 192] = d3;
+  }
+}
+
+// Claim up to kFillBatch completions and copy their pages into the cache.
+// Host memory is read by one wave at a time (the poll lock): it refreshes the
+// device mirrors of the proxy's tail and of the abort flag; every other wave
+// only reads the mirrors.
+__device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
+  const int l = lane_id();
+  uint32_t n = 0;
+  unsigned long long h = 0;
+  if (l == 0) {
+    h = __hip_atomic_load(p.cq_head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned long long t = __hip_atomic_load(p.tail_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (h >= t && atomicCAS(p.poll_lock, 0u, 1u) == 0u) {
+      t = __hip_atomic_load(p.cq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      atomicMax(p.tail_seen, t);
+      if (__hip_atomic_load(p.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0)
+        atomicExch(p.abort_seen, 1u);
+      atomicExch(p.poll_lock, 0u);
+    }
+    if (h < t) {
+      const unsigned long long want = min((unsigned long long)kFillBatch, t - h);
+      if (atomicCAS(p.cq_head, h, h + want) == h) n = (uint32_t)want;
+    }
+  }
+  n = first_lane_value(n);
+  if (n == 0) return 0;
+  h = ((unsigned long long)first_lane_value((uint32_t)(h >> 32)) << 32) | first_lane_value((uint32_t)h);
+  // completion i in lane i (completions are published before the tail)
+  unsigned long long e = 0;
+  if ((uint32_t)l < n)
+    e = __hip_atomic_load(&p.cq[(h + l) & p.cq_mask], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  // a malformed completion is never copied: its waiter times out instead of
+  // the copy leaving the backing store or the cache
+  {
+    const uint32_t pg = (uint32_t)(e >> 32) - 1u, sl = (uint32_t)e;
+    const bool bad = (uint32_t)l < n && (pg >= p.num_pages || sl >= p.cache.slots);
+    const uint64_t mbad = ballot(bad);
+    if (mbad) {
+      if (l == 0) atomicAdd(&p.stats[9], (unsigned long long)__popcll(mbad));
+      n = min(n, (uint32_t)__builtin_ctzll(mbad));  // the well-formed prefix only
+      if (n == 0) return 0;
+    }
+  }
+  if (p.cache.page_bytes == 4096) {
+    for (uint32_t i0 = 0; i0 < n; i0 += 4) copy_pages4(p.backing, p.cache.data, e, i0, n);
+  } else {
+    const uint32_t chunks = (uint32_t)(p.cache.page_bytes / 16);
+    for (uint32_t i = 0; i < n; ++i) {
+      const uint64_t ei = readlane64(e, i);
+      const uint4 *src = reinterpret_cast<const uint4 *>(p.backing + (uint64_t)((uint32_t)(ei >> 32) - 1u) *
+                                                                         p.cache.page_bytes);
+      uint4 *dst = reinterpret_cast<uint4 *>(p.cache.data + (uint64_t)(uint32_t)ei * p.cache.page_bytes);
+      for (uint32_t c = l; c < chunks; c += kWave) dst[c] = src[c];
+    }
+  }
+  // page bytes visible device-wide before any READY state
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  if ((uint32_t)l < n) atomicAdd(&p.cache.slot_word[(uint32_t)e], (1ull << kStateShift) | kRefBit);
+  return n;
+}
+
+// Frontier-to-LDS and back.
+template <int KPL>
+__device__ __forceinline__ void load_frontier(const QSlot<KPL> &S, uint64_t (&F)[KPL]) {
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) F[r] = S.F[r * kWave + lane_id()];
+}
+template <int KPL>
+__device__ __forceinline__ void store_frontier(QSlot<KPL> &S, const uint64_t (&F)[KPL]) {
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) S.F[r * kWave + lane_id()] = F[r];
+}
+
+// Whether a parked query can make progress: a page it waits on is READY, or
+// it has requests it may still issue.
+template <int KPL>
+__device__ __forceinline__ bool query_runnable(const PagedParams &p, const QSlot<KPL> &S) {
+  const int l = lane_id();
+  bool ready = false;
+  uint32_t waiting = 0, todo = 0;
+  if (S.phase == kPhExpand) {
+    const uint32_t nb = min(S.nbeam - S.b0, min(kCandCap / p.R, (uint32_t)kPagedMaxW));
+    if ((uint32_t)l < nb) {
+      const uint32_t st = S.bstate[S.b0 + l];
+      if (st < kDone) { ++waiting; ready = slot_ready(p.cache, st); }
+      else if (st == kTodo) ++todo;
+    }
+  } else if (S.phase == kPhEval) {
+    for (uint32_t c = l; c < S.ncand; c += kWave) {
+      const uint32_t st = S.cstate[c];
+      if (st < kDone) { ++waiting; ready |= slot_ready(p.cache, st); }
+      else if (st == kTodo) ++todo;
+    }
+  } else {
+    return true;
+  }
+  if (ballot(ready) != 0) return true;
+  uint32_t nwait = 0, ntodo = 0;
+  for (int m = 1; m < kWave; m <<= 1) {
+    waiting += __shfl_xor(waiting, m);
+    todo += __shfl_xor(todo, m);
+  }
+  nwait = waiting;
+  ntodo = todo;
+  if (p.blocking) return nwait == 0;
+  return ntodo > 0 && nwait < p.max_pending;
+}
+
+// Runs one query until it finishes (returns true) or parks (false).
+template <int KPL, int VDW, bool EXACT, bool N2S>
+__device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, PagedCounters &ctr) {
+  using HT = VisitedHbm<kPagedHtLog2>;
+  const int l = lane_id();
+  const int g = l >> 3;
+  const int gl = l & 7;
+  const uint32_t dwords = p.D >> 2;
+  const uint32_t GB = min(kCandCap / p.R, (uint32_t)kPagedMaxW);
+  constexpr int kIdsPerLane = kCandCap / kWave;
+
+  U8Vec<VDW, EXACT> q;
+  q.load(p.queries + (uint64_t)S.qi * p.D, gl, dwords);
+  int qq = 0;
+#pragma unroll
+  for (int t = 0; t < VDW; ++t) qq += (int)__builtin_amdgcn_udot4(q.w[t], q.w[t], 0u, false);
+  qq = sum8(qq);
+  uint64_t F[KPL];
+  load_frontier(S, F);
+
+  for (uint32_t guard = 0; guard < 4u * p.n + 16u; ++guard) {
+    if (S.phase == kPhSelect) {
+      uint32_t nbeam = 0;
+#pragma unroll
+      for (int r = 0; r < KPL; ++r) {
+        const uint32_t e = r * kWave + l;
+        bool unexp = e < p.L && F[r] != kInfKey && !(F[r] & 1ull);
+        uint64_t m = ballot(unexp);
+        uint32_t rank = nbeam + lanes_below(m);
+        if (unexp && rank < p.W) {
+          S.beam[rank] = key_id(F[r]);
+          S.bstate[rank] = kTodo;
+          F[r] |= 1ull;
+        }
+        nbeam += (uint32_t)__popcll(m);
+      }
+      nbeam = min(nbeam, p.W);
+      if (nbeam == 0) {
+#pragma unroll
+        for (int r = 0; r < KPL; ++r) {
+          const uint32_t e = r * kWave + l;
+          if (e < p.k) {
+            const bool ok = F[r] != kInfKey;
+            p.out_ids[(uint64_t)S.qi * p.k + e] = ok ? key_id(F[r]) : kNoEdge;
+            p.out_dists[(uint64_t)S.qi * p.k + e] = ok ? (int32_t)(F[r] >> 32) : INT32_MAX;
+          }
+        }
+        return true;
+      }
+      S.nbeam = nbeam;
+      S.b0 = 0;
+      S.ncand = 0;
+      S.phase = kPhExpand;
+      ctr.exp += nbeam;
+      ++ctr.iter;
+      __syncthreads();
+    }
+
+    if (S.phase == kPhExpand) {
+      const uint32_t nb = min(S.nbeam - S.b0, GB);
+      const bool mine = (uint32_t)l < nb;
+      const uint32_t bi = S.b0 + min((uint32_t)l, nb - 1);
+      uint32_t st = mine ? S.bstate[bi] : kDone;
+      uint32_t slot = 0;
+      bool ready = false;
+      bool hit = false, miss = false;
+      if (mine && st == kTodo) {
+        bool issued;
+        const uint32_t r = acquire_page(p.cache, page_of<N2S>(p, S.beam[bi]), true, slot, issued);
+        if (r == kAcqReady) { ready = true; hit = true; }
+        else if (r == kAcqWait) { st = slot; miss = true; }
+      } else if (mine && st < kDone) {
+        if (slot_ready(p.cache, st)) { ready = true; slot = st; }
+      }
+      ctr.hit += (uint32_t)__popcll(ballot(hit));
+      ctr.miss += (uint32_t)__popcll(ballot(miss));
+      if (mine && !ready) S.bstate[bi] = st;
+      uint64_t rmask = ballot(ready);
+      if (rmask) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        while (rmask) {
+          const int b = __builtin_ctzll(rmask);
+          rmask &= rmask - 1;
+          const uint32_t s_b = readlane(slot, b);
+          const uint32_t u = S.beam[S.b0 + b];
+          const uint8_t *adj = cached_record<N2S>(p, s_b, u) + p.geom.vec_bytes;
+          const uint32_t deg = min(*reinterpret_cast<const uint32_t *>(adj), p.R);
+          const uint32_t *idp = reinterpret_cast<const uint32_t *>(adj + 4);
+          for (uint32_t j0 = 0; j0 < p.R; j0 += kCandCap) {
+            uint32_t ids[kIdsPerLane];
+            bool valid[kIdsPerLane], isnew[kIdsPerLane], rec[kIdsPerLane];
+#pragma unroll
+            for (int t = 0; t < kIdsPerLane; ++t) {
+              const uint32_t j = j0 + t * kWave + l;
+              ids[t] = j < deg ? idp[j] : kNoEdge;
+              valid[t] = ids[t] < p.n;
+            }
+            HT::template test_and_set_n<kIdsPerLane>(ht, ids, valid, S.ht_used < HT::kLimit, isnew, rec);
+#pragma unroll
+            for (int t = 0; t < kIdsPerLane; ++t) {
+              const uint64_t mnew = ballot(isnew[t]);
+              const uint64_t mrec = ballot(rec[t]);
+              const uint32_t base = S.ncand;
+              if (isnew[t]) {
+                const uint32_t pos = base + lanes_below(mnew);
+                S.cand[pos] = ids[t];
+                S.cstate[pos] = kTodo;
+              }
+              S.ncand = base + (uint32_t)__popcll(mnew);
+              S.ht_used += (uint32_t)__popcll(mrec);
+              const uint32_t lost = (uint32_t)__popcll(mnew & ~mrec);
+              ctr.reeval += lost;
+              if (lost) S.forgot = 1;
+            }
+          }
+          if (l == 0) {
+            unpin(p.cache, s_b);
+            S.bstate[S.b0 + b] = kDone;
+          }
+          __syncthreads();
+        }
+      }
+      __syncthreads();
+      const bool pending = mine && S.bstate[bi] != kDone;
+      if (ballot(pending) != 0) break;  // park
+      S.phase = kPhEval;
+      __syncthreads();
+    }
+
+    if (S.phase == kPhEval) {
+      // request or re-test every candidate; evaluate the resident ones
+      uint32_t npend = 0;
+      bool lane_waiting = false;
+      for (uint32_t c = l; c < S.ncand; c += kWave) {
+        const bool w = S.cstate[c] < kDone;
+        npend += w ? 1u : 0u;
+        lane_waiting |= w;
+      }
+      for (int m = 1; m < kWave; m <<= 1) npend += __shfl_xor(npend, m);
+      uint32_t rslot[kIdsPerLane];
+      bool rdy[kIdsPerLane];
+#pragma unroll
+      for (int t = 0; t < kIdsPerLane; ++t) {
+        const uint32_t c = t * kWave + l;
+        const bool mine = c < S.ncand;
+        uint32_t st = mine ? S.cstate[c] : kDone;
+        rdy[t] = false;
+        rslot[t] = 0;
+        // blocking: a lane keeps at most one page request outstanding
+        const bool want = mine && st == kTodo && !(p.blocking && lane_waiting);
+        const uint64_t mwant = ballot(want);
+        const bool allowed = want && npend + lanes_below(mwant) < p.max_pending;
+        bool waited = false, hit = false;
+        if (allowed) {
+          bool issued;
+          uint32_t s;
+          const uint32_t r = acquire_page(p.cache, page_of<N2S>(p, S.cand[c]), true, s, issued);
+          if (r == kAcqReady) { rdy[t] = true; rslot[t] = s; hit = true; }
+          else if (r == kAcqWait) { st = s; waited = true; }
+        } else if (mine && st < kDone) {
+          if (slot_ready(p.cache, st)) { rdy[t] = true; rslot[t] = st; }
+        }
+        if (mine && !rdy[t]) S.cstate[c] = st;
+        lane_waiting |= waited;
+        const uint32_t nw = (uint32_t)__popcll(ballot(waited));
+        npend += nw;
+        ctr.miss += nw;
+        ctr.hit += (uint32_t)__popcll(ballot(hit));
+      }
+      // gather the ready candidates, 64 at a time
+      bool any_ready = false;
+#pragma unroll
+      for (int t = 0; t < kIdsPerLane; ++t) any_ready |= ballot(rdy[t]) != 0;
+      if (any_ready) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+#pragma unroll
+        for (int t = 0; t < kIdsPerLane; ++t) {
+          const uint64_t mr = ballot(rdy[t]);
+          if (mr == 0) continue;
+          // candidate of lane src: t*64 + src; evaluate in 8 rounds of 8 vectors
+          const uint32_t cnt = (uint32_t)__popcll(mr);
+          // compact ready lanes: the i-th ready lane's candidate index and slot
+          const uint32_t my_rank = lanes_below(mr);
+          __shared__ uint32_t rc[kWave], rs[kWave];
+          if (rdy[t]) {
+            rc[my_rank] = t * kWave + l;
+            rs[my_rank] = rslot[t];
+          }
+          __syncthreads();
+          U8Vec<VDW, EXACT> x[8];
+#pragma unroll
+          for (int rr = 0; rr < 8; ++rr) {
+            const uint32_t idx = rr * 8 + g;
+            const uint32_t ci = idx < cnt ? rc[idx] : rc[0];
+            const uint32_t si = idx < cnt ? rs[idx] : rs[0];
+            x[rr].load(cached_record<N2S>(p, si, S.cand[ci]), gl, dwords);
+          }
+          int mine_d = 0;
+#pragma unroll
+          for (int rr = 0; rr < 8; ++rr) {
+            const int d = sum8(partial_u8(q, x[rr])) + qq;
+            if (gl == rr) mine_d = d;
+          }
+          const uint32_t my_idx = gl * 8 + g;
+          uint64_t key = kInfKey;
+          if (my_idx < cnt) key = ((uint64_t)(uint32_t)mine_d << 32) | ((uint64_t)S.cand[rc[my_idx]] << 1);
+          ctr.eval += cnt;
+          const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
+          const bool pass = key < thr;
+          uint64_t pm = ballot(pass);
+          if (!pass) key = kInfKey;
+          if (pm != 0) {
+            if ((uint32_t)__popcll(pm) <= kInsertMax) {
+              while (pm) {
+                const int lane = __builtin_ctzll(pm);
+                pm &= pm - 1;
+                insert_key<KPL>(F, readlane64(key, lane));
+              }
+            } else {
+              uint64_t cc[1] = {key};
+              bitonic_sort<1>(cc, true);
+              if (!S.forgot) {
+                F[KPL - 1] = min64(F[KPL - 1], cc[0]);
+                bitonic_merge_up<KPL>(F);
+              } else {
+                merge_dedupe<KPL>(F, cc[0]);
+              }
+            }
+#pragma unroll
+            for (int r = 0; r < KPL; ++r)
+              if ((uint32_t)(r * kWave + l) >= p.L) F[r] = kInfKey;
+          }
+          if (rdy[t]) {
+            unpin(p.cache, rslot[t]);
+            S.cstate[t * kWave + l] = kDone;
+          }
+          __syncthreads();
+        }
+      }
+      __syncthreads();
+      bool left = false;
+      for (uint32_t c = l; c < S.ncand; c += kWave) left |= S.cstate[c] != kDone;
+      if (ballot(left) != 0) {
+        if (any_ready) continue;  // progress: pins were released, more requests may go out
+        break;                    // park until a page arrives
+      }
+      // iteration group done
+      S.b0 += min(S.nbeam - S.b0, GB);
+      S.ncand = 0;
+      S.phase = S.b0 < S.nbeam ? kPhExpand : kPhSelect;
+      __syncthreads();
+    }
+  }
+  store_frontier(S, F);
+  __syncthreads();
+  return false;
+}
+
+template <int KPL, int VDW, bool EXACT, bool N2S>
+__global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  QSlot<KPL> *slots = reinterpret_cast<QSlot<KPL> *>(lds);
+  const int l = lane_id();
+  for (uint32_t j = 0; j < p.oversub; ++j) {
+    if (l == 0) {
+      slots[j].active = 0;
+      slots[j].parked = 0;
+    }
+  }
+  __syncthreads();
+  PagedCounters ctr;
+  bool admitting = true;
+  uint32_t idle = 0;
+  for (;;) {
+    if (aborted(p)) break;
+    bool any_active = false, progressed = false;
+    for (uint32_t j = 0; j < p.oversub; ++j) {
+      QSlot<KPL> &S = slots[j];
+      uint32_t *ht = p.ht_pool + ((uint64_t)(blockIdx.x * p.oversub + j) << kPagedHtLog2);
+      if (!S.active) {
+        if (!admitting) continue;
+        uint32_t qi = 0;
+        if (l == 0) qi = atomicAdd(p.next_query, 1u);
+        qi = first_lane_value(qi);
+        if (qi >= p.nq) {
+          admitting = false;
+          continue;
+        }
+        VisitedHbm<kPagedHtLog2>::clear(ht);
+        // V = {entry}: the entry is the first candidate to evaluate
+        if (l == 0) {
+          S.qi = qi;
+          S.active = 1;
+          S.parked = 0;
+          S.phase = kPhEval;
+          S.nbeam = 0;
+          S.b0 = 0;
+          S.ncand = 1;
+          S.cand[0] = p.entry;
+          S.cstate[0] = kTodo;
+          S.ht_used = 1;
+          S.forgot = 0;
+        }
+#pragma unroll
+        for (int r = 0; r < KPL; ++r) S.F[r * kWave + l] = kInfKey;
+        __syncthreads();
+        {
+          uint32_t e1[1] = {p.entry};
+          bool v1[1] = {l == 0}, n1[1], r1[1];
+          VisitedHbm<kPagedHtLog2>::test_and_set_n<1>(ht, e1, v1, true, n1, r1);
+        }
+        __syncthreads();
+      } else if (S.parked) {
+        any_active = true;
+        if (!query_runnable(p, S)) continue;
+        ++ctr.resume;
+      }
+      any_active = true;
+      const bool done = run_query<KPL, VDW, EXACT, N2S>(p, S, ht, ctr);
+      progressed = true;
+      if (l == 0) {
+        if (done) {
+          S.active = 0;
+          S.parked = 0;
+        } else {
+          S.parked = 1;
+        }
+      }
+      if (!done) ++ctr.park;
+      __syncthreads();
+    }
+    if (!any_active && !admitting) break;
+    const uint32_t served = service_completions(p);
+    ctr.served += served;
+    if (!progressed && served == 0) {
+      if (++idle > 4) __builtin_amdgcn_s_sleep(2);
+    } else {
+      idle = 0;
+    }
+  }
+  // A wave leaves only when none of its queries is active: every page any
+  // query waits on has a waiting wave that keeps serving completions.
+  if (l == 0) {
+    atomicAdd(&p.stats[0], ctr.eval);
+    atomicAdd(&p.stats[1], ctr.reeval);
+    atomicAdd(&p.stats[2], ctr.exp);
+    atomicAdd(&p.stats[3], ctr.iter);
+    atomicAdd(&p.stats[4], ctr.hit);
+    atomicAdd(&p.stats[5], ctr.miss);
+    atomicAdd(&p.stats[6], ctr.served);
+    atomicAdd(&p.stats[7], ctr.park);
+    atomicAdd(&p.stats[8], ctr.resume);
+  }
+}
+
+}  // namespace gorio

@@ -11,6 +11,10 @@ if str(ROOT) not in sys.path:
 
 NO_EDGE = 0xFFFFFFFF
 
+# a paged search that stops making progress is aborted by the library's
+# watchdog well before the per-test time limit
+os.environ.setdefault("GORIO_WATCHDOG_S", "90")
+
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")

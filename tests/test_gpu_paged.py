@@ -1,0 +1,151 @@
+"""GPU parity of the paged search (HBM page cache + host backing store + proxy).
+
+Results must equal the CPU oracle bit-exact whatever the cache size, the
+injected latency, the query-slot oversubscription or the blocking mode.
+"""
+import numpy as np
+import pytest
+
+import paper_2607_04415_amd as g
+from workload import IndexSpec, QuerySpec, WORKLOADS, index_arrays, query_array
+
+pytestmark = pytest.mark.gpu
+
+SPEC = IndexSpec(n=20000, D=128, dtype="u8", clusters=8, sigma=20.0, r_near=16, r_rand=16, seed=41)
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    torch.cuda.set_device(0)
+    return torch
+
+
+@pytest.fixture(scope="module")
+def small(orc):
+    a = index_arrays(SPEC, use_cache=False)
+    q = query_array(SPEC, QuerySpec(400, 42))
+    e = orc.medoid(a["x"])
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"]).search(q, 10, 32, 4, e, threads=8)
+    return a, q, oids, od, oc
+
+
+def search(torch, ix, q, k, L, W):
+    qd = torch.from_numpy(np.ascontiguousarray(q)).cuda()
+    ids, dists, st = ix.search(qd, k, L, W)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), st
+
+
+def assert_same(gi, gd, oids, od):
+    bad = np.flatnonzero((gi != oids).any(1) | (gd != od).any(1))
+    assert bad.size == 0, f"{bad.size} queries differ, first {bad[:5]}"
+
+
+@pytest.mark.parametrize("frac,latency,oversub,blocking", [
+    (0.10, 0.0, 1, 0), (0.10, 20.0, 4, 0), (0.30, 0.0, 2, 0), (0.10, 0.0, 1, 1), (0.50, 5.0, 8, 0),
+], ids=["c10-l0-o1", "c10-l20-o4", "c30-l0-o2", "c10-l0-blocking", "c50-l5-o8"])
+def test_paged_matches_oracle(torch_dev, small, frac, latency, oversub, blocking):
+    a, q, oids, od, oc = small
+    ix = g.Index(a["x"], a["graph"])
+    info = ix.info
+    ix.set_cache(max(int(frac * info["index_bytes"]), 128 * 4096))
+    ix.set_backing(latency_us=latency, oversub=oversub, blocking=bool(blocking))
+    assert not ix.info["resident"]
+    gi, gd, st = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+    assert st["iterations"] == int(oc["iterations"].sum())
+    assert st["misses"] > 0 and st["pages_served"] > 0
+    # every record access was either a hit or a miss
+    assert st["hits"] + st["misses"] == st["expansions"] + st["evaluations"]
+    assert st["bytes_served"] == st["pages_served"] * 4096
+    assert st["parks"] > 0
+
+
+def test_paged_tiny_cache_slot_reuse(torch_dev, small):
+    """The smallest cache (128 slots): every slot is reused many times."""
+    a, q, oids, od, _ = small
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(128 * 4096)
+    ix.set_backing(latency_us=0.0, oversub=1)
+    assert ix.info["cache_slots"] == 128
+    gi, gd, st = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    assert st["pages_served"] > 10 * 128
+
+
+def test_warm_cache_second_search(torch_dev, small):
+    a, q, oids, od, _ = small
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(ix.info["index_bytes"] // 2)
+    s1 = search(torch_dev, ix, q, 10, 32, 4)
+    s2 = search(torch_dev, ix, q, 10, 32, 4)           # cache carries over
+    for gi, gd, _ in (s1, s2):
+        assert_same(gi, gd, oids, od)
+    assert s2[2]["misses"] < s1[2]["misses"]
+    ix.set_cache(ix.info["index_bytes"] // 2)           # empties it again
+    s3 = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(s3[0], s3[1], oids, od)
+
+
+def test_paged_to_resident_and_back(torch_dev, small):
+    a, q, oids, od, _ = small
+    ix = g.Index(a["x"], a["graph"])
+    pages = ix.pages()
+    ix.set_cache(200 * 4096)
+    assert np.array_equal(ix.pages(), pages)            # backing store holds the same bytes
+    ix.set_cache(ix.info["index_bytes"])
+    assert ix.info["resident"]
+    gi, gd, _ = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+
+
+def test_paged_rejects(torch_dev, small):
+    a, q, _, _, _ = small
+    ix = g.Index(a["x"], a["graph"])
+    with pytest.raises(g.GorioError) as e:
+        ix.set_cache(10 * 4096)                          # fewer than two queries' worth of pins
+    assert e.value.status == g.EINVAL
+    ix.set_cache(300 * 4096)
+    with pytest.raises(g.GorioError) as e:
+        ix.search(q[:4], 10, 128, 65)                    # paged search takes W <= 64
+    assert e.value.status == g.EUNSUPPORTED
+    with pytest.raises(g.GorioError):
+        ix.set_backing(oversub=0)
+
+
+def test_watchdog_abort_then_recover(torch_dev, small, monkeypatch):
+    """The host trips the watchdog at once: the kernel exits, the call reports
+    a time-out, and the next search runs normally."""
+    a, q, oids, od, _ = small
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(300 * 4096)
+    ix.set_backing(latency_us=50.0)
+    monkeypatch.setenv("GORIO_WATCHDOG_S", "0")
+    with pytest.raises(g.GorioError) as e:
+        search(torch_dev, ix, q, 10, 32, 4)
+    assert e.value.status == g.ETIMEOUT
+    monkeypatch.delenv("GORIO_WATCHDOG_S")
+    ix.set_backing(latency_us=0.0)
+    gi, gd, _ = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+
+
+def test_paged_1m_index_slice(orc, torch_dev):
+    """The 1M-vector index with a 10% cache, on the first 2,000 queries."""
+    w = WORKLOADS["u8-1m-cache10-lat0"]
+    a = index_arrays(w.index)
+    q = query_array(w.index, w.queries)[:2000]
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(int(0.10 * ix.info["index_bytes"]))
+    ix.set_backing(latency_us=0.0, oversub=1)
+    gi, gd, st = search(torch_dev, ix, q, w.k, w.L, w.W)
+    e = ix.info["entry"]
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"]).search(q, w.k, w.L, w.W, e, threads=16)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+    hr = st["hits"] / max(1, st["hits"] + st["misses"])
+    print(f"[1m paged] {st['kernel_ms']:.1f} ms, hit rate {hr:.3f}, served {st['pages_served']}, "
+          f"{st['bytes_served'] / st['kernel_ms'] / 1e6:.2f} GB/s", flush=True)
