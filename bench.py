@@ -78,6 +78,52 @@ def cpu_baseline(a, q, w, gpu_ids, gpu_dists, sample_nq: int, threads: int):
     }, exact, entry
 
 
+def host_link_peak_gbs(torch) -> float:
+    """Pinned host -> HBM copy bandwidth (256 MiB, best of 5), the host-link ceiling."""
+    src = torch.empty(1 << 28, dtype=torch.uint8).pin_memory()
+    dst = torch.empty(1 << 28, dtype=torch.uint8, device="cuda")
+    best = 0.0
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src, non_blocking=True)
+        b.record()
+        torch.cuda.synchronize()
+        best = max(best, src.numel() / (a.elapsed_time(b) * 1e-3) / 1e9)
+    return best
+
+
+def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: bool = False):
+    """One cold-cache paged search over the first nq_sample queries of workload w."""
+    from workload import query_array
+    q = query_array(w.index, w.queries)[:nq_sample]
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))      # empty cache
+    ix.set_backing(latency_us=w.latency_us, oversub=1 if blocking else w.oversub, blocking=blocking)
+    qd = torch.from_numpy(q).cuda()
+    ids = torch.empty((len(q), w.k), dtype=torch.int32, device="cuda")
+    dists = torch.empty((len(q), w.k), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    st = ix.search_into(qd, len(q), w.k, w.L, w.W, ids, dists,
+                        stream=torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = st["kernel_ms"]
+    acc = st["hits"] + st["misses"]
+    out = {"workload": w.name, "queries": len(q), "blocking": blocking,
+           "cache_slots": ix.info["cache_slots"], "latency_us": w.latency_us,
+           "oversub": 1 if blocking else w.oversub,
+           "qps": round(len(q) / wall, 1), "kernel_ms": round(ms, 2),
+           "hit_rate": round(st["hits"] / max(1, acc), 4),
+           "pages_served": st["pages_served"],
+           "miss_service_gbs": round(st["bytes_served"] / (ms * 1e-3) / 1e9, 2),
+           "parks": st["parks"], "resumes": st["resumes"],
+           "vs_resident_qps": round(len(q) / wall / resident_qps, 5)}
+    ix.close()
+    return out, ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), q
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -88,6 +134,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
+    ap.add_argument("--paged-sample", type=int, default=2000,
+                    help="queries of each paged configuration to run (0 = skip the paged legs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
@@ -168,6 +216,24 @@ def main():
         log(f"[bench] oracle on CPU: {cpu['value']:,.0f} queries/s with {threads} threads; "
             f"GPU answers oracle-exact on the sample: {exact}")
 
+    paged = None
+    miss_gbs = None
+    if args.paged_sample > 0 and w.name == "u8-1m-hbm":
+        link = host_link_peak_gbs(torch)
+        legs = []
+        for name, blocking in (("u8-1m-cache10-lat0", False), ("u8-1m-cache10-lat0", True),
+                               ("u8-1m-cache10-lat20", False)):
+            leg, pi, pd, pq = paged_leg(torch, g, a, WORKLOADS[name], args.paged_sample, qps, blocking)
+            # the paged results must equal the resident results on the same queries
+            if WORKLOADS[name].queries == w.queries:
+                leg["equals_resident"] = bool(np.array_equal(pi, gi[:len(pq)]) and np.array_equal(pd, gd[:len(pq)]))
+            log(f"[bench] paged {name} blocking={blocking}: {leg['qps']:,.0f} q/s, hit rate "
+                f"{leg['hit_rate']:.3f}, miss service {leg['miss_service_gbs']} GB/s")
+            legs.append(leg)
+        miss_gbs = legs[0]["miss_service_gbs"]
+        paged = {"host_link_peak_gbs": round(link, 1), "legs": legs,
+                 "split_phase_vs_blocking": round(legs[0]["qps"] / max(1e-9, legs[1]["qps"]), 3)}
+
     out = {
         "metric": METRIC, "value": round(qps, 1), "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
@@ -179,10 +245,11 @@ def main():
                    "resident": bool(info["resident"])},
         "oracle_exact": exact,
         "achieved_hbm_gbs": roofline["achieved"],
-        "miss_service_gbs": None,
+        "miss_service_gbs": miss_gbs,
         "counters": {k: st[k] for k in ("evaluations", "reevaluations", "expansions", "iterations")},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "paged": paged,
     }
     print(json.dumps(out), flush=True)
 
