@@ -84,6 +84,7 @@ typedef struct {
     uint64_t bytes_served;     /* paged mode: pages_served * page_bytes */
     uint64_t parks;            /* paged mode: times a query was set aside waiting for pages */
     uint64_t resumes;          /* paged mode: times a parked query was picked up again */
+    uint64_t proxy_peak;       /* paged mode: most page requests the proxy held at once */
 } gorio_stats;
 
 /* Read-only facts about a built index. */

@@ -35,7 +35,7 @@ class Stats(ctypes.Structure):
     _fields_ = [("kernel_ms", ctypes.c_double), ("wall_ms", ctypes.c_double)] + [
         (f, ctypes.c_uint64) for f in ("evaluations", "reevaluations", "expansions", "iterations",
                                        "hits", "misses", "pages_served", "bytes_served",
-                                       "parks", "resumes")]
+                                       "parks", "resumes", "proxy_peak")]
 
     def as_dict(self) -> dict:
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -167,8 +167,12 @@ class Index:
         """Raw call: queries/ids/dists are numpy arrays or device tensors."""
         st = Stats()
         sp = None if stream is None else ctypes.c_void_p(stream)
-        _check(lib().gorio_search(self._h, _ptr(queries), nq, k, L, W, _ptr(ids), _ptr(dists),
-                                  ctypes.byref(st) if stats else None, sp))
+        status = lib().gorio_search(self._h, _ptr(queries), nq, k, L, W, _ptr(ids), _ptr(dists),
+                                    ctypes.byref(st) if stats else None, sp)
+        if status != OK:
+            err = GorioError(status, lib().gorio_last_error().decode())
+            err.stats = st.as_dict() if stats else None   # counters up to the failure
+            raise err
         return st.as_dict() if stats else None
 
     def search(self, queries, k: int, L: int, W: int, stream=None, stats: bool = True):

@@ -75,6 +75,11 @@ bool is_device_pointer(const void *ptr) {
   return a.type == hipMemoryTypeDevice || a.isManaged;
 }
 
+int env_int(const char *name, int dflt) {
+  const char *v = getenv(name);
+  return v && *v ? atoi(v) : dflt;
+}
+
 uint32_t vec_bytes_of(gorio_dtype dt, uint32_t D) { return dt == GORIO_U8 ? D : 4u * D; }
 
 int grid_for(uint64_t items, int per_block, int cap = 65536) {
@@ -233,7 +238,9 @@ gorio_status gorio_index::make_paged(uint64_t slots) {
   if (slots < 2ull * kMaxPendingPerQuery)
     return fail(GORIO_EINVAL, "a paged cache needs at least %u slots (asked for %llu)",
                 2 * kMaxPendingPerQuery, (unsigned long long)slots);
-  if (slots >= (1ull << 30)) return fail(GORIO_EINVAL, "too many cache slots");
+  if (slots * (uint64_t)page_bytes > 0x7FFFF000ull)
+    return fail(GORIO_EUNSUPPORTED, "a paged cache is limited to 2 GiB (asked for %llu slots)",
+                (unsigned long long)slots);
   if (resident) {
     hipError_t e = hipHostMalloc(reinterpret_cast<void **>(&h_backing), index_bytes(), hipHostMallocDefault);
     if (e != hipSuccess)
@@ -248,10 +255,11 @@ gorio_status gorio_index::make_paged(uint64_t slots) {
   paged = std::make_unique<PagedState>();
   PagedState &P = *paged;
   P.slots = slots;
+  P.ctrl_stride = (uint32_t)std::max(1, std::min(32, env_int("GORIO_CTRL_STRIDE", (int)PagedState::kCtrlStride)));
   HIP_OR_FAIL(hipMalloc(&P.d_cache, slots * (uint64_t)page_bytes));
   HIP_OR_FAIL(hipMalloc(&P.d_slot_word, slots * sizeof(unsigned long long)));
   HIP_OR_FAIL(hipMalloc(&P.d_page_slot, num_pages * sizeof(uint32_t)));
-  HIP_OR_FAIL(hipMalloc(&P.d_ctrl, PagedState::kCtrlWords * sizeof(unsigned long long)));
+  HIP_OR_FAIL(hipMalloc(&P.d_ctrl, PagedState::kCtrlWords * PagedState::kCtrlStride * sizeof(unsigned long long)));
   P.ring_cap = next_pow2(2 * slots + 1024);
   HIP_OR_FAIL(host_ring(&P.h_mq, &P.d_mq, P.ring_cap));
   HIP_OR_FAIL(host_ring(&P.h_cq, &P.d_cq, P.ring_cap));
@@ -260,7 +268,7 @@ gorio_status gorio_index::make_paged(uint64_t slots) {
   cache_slots = slots;
   gorio_status st = reset_cache();
   if (st != GORIO_OK) return st;
-  P.proxy.start(P.h_mq, P.ring_cap - 1, P.h_cq, P.ring_cap - 1, P.h_cq_tail);
+  P.proxy.start(P.h_mq, P.ring_cap - 1, P.h_cq, P.ring_cap - 1, P.h_cq_tail, 1, 1);
   return GORIO_OK;
 }
 
@@ -271,7 +279,7 @@ gorio_status gorio_index::reset_cache() {
   fill_u32<<<grid_for(P.slots * 2, 256), 256, 0, stream>>>(reinterpret_cast<uint32_t *>(P.d_slot_word),
                                                            P.slots * 2, 0u);
   fill_u32<<<grid_for(num_pages, 256), 256, 0, stream>>>(P.d_page_slot, num_pages, 0xFFFFFFFFu);
-  fill_u32<<<1, 64, 0, stream>>>(reinterpret_cast<uint32_t *>(P.d_ctrl), 2 * PagedState::kCtrlWords, 0u);
+  fill_u32<<<1, 256, 0, stream>>>(reinterpret_cast<uint32_t *>(P.d_ctrl), 2 * PagedState::kCtrlWords * PagedState::kCtrlStride, 0u);
   HIP_OR_FAIL(hipGetLastError());
   HIP_OR_FAIL(hipStreamSynchronize(stream));
   return GORIO_OK;
@@ -337,10 +345,6 @@ gorio_status launch_resident(const ResidentParams &p, int ht_log2, int grid, hip
   return launch_resident_vdw<4>(p.D, ht_log2, p, grid, s);
 }
 
-int env_int(const char *name, int dflt) {
-  const char *v = getenv(name);
-  return v && *v ? atoi(v) : dflt;
-}
 
 }  // namespace
 
@@ -387,10 +391,15 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   HIP_OR_FAIL(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
   // concurrent queries: each may hold kMaxPendingPerQuery pins, kept within
   // half the cache so the clock always finds victims for the rest
-  const uint64_t q_cache = std::max<uint64_t>(1, P.slots / (2ull * kMaxPendingPerQuery));
+  const uint32_t max_pending = (uint32_t)std::max(1, std::min(256, env_int("GORIO_MAX_PENDING", (int)kMaxPendingPerQuery)));
+  const uint64_t q_cache = std::max<uint64_t>(1, P.slots / (2ull * max_pending));
   const uint64_t q_live = std::min<uint64_t>({(uint64_t)cus * 8 * oversub, q_cache, rp.nq});
-  const int grid = (int)std::max<uint64_t>(1, (q_live + oversub - 1) / oversub);
-  const uint64_t ht_entries = (uint64_t)grid * oversub << kPagedHtLog2;
+  const int qwaves = (int)std::max<uint64_t>(1, (q_live + oversub - 1) / oversub);
+  // extra waves that only copy arriving pages, so the fill rate does not
+  // depend on how many queries run at once
+  const int fwaves = std::max(0, env_int("GORIO_FILL_WAVES", 16));
+  const int grid = qwaves + fwaves;
+  const uint64_t ht_entries = (uint64_t)qwaves * oversub << kPagedHtLog2;
   if (ht_entries > P.ht_pool_entries) {
     if (P.d_ht_pool) (void)hipFree(P.d_ht_pool);
     P.d_ht_pool = nullptr;
@@ -403,19 +412,19 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   memset(P.h_mq, 0, P.ring_cap * sizeof(unsigned long long));
   __atomic_store_n(P.h_cq_tail, 0ull, __ATOMIC_RELEASE);
   __atomic_store_n(P.h_abort, 0u, __ATOMIC_RELEASE);
-  fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(P.d_ctrl + PagedState::kMqTail),
-                            2 * (PagedState::kCtrlWords - PagedState::kMqTail), 0u);
+  fill_u32<<<1, 256, 0, s>>>(reinterpret_cast<uint32_t *>(P.ctrl(PagedState::kMqTail)),
+                             2 * (PagedState::kCtrlWords - PagedState::kMqTail) * PagedState::kCtrlStride, 0u);
 
   PagedParams pp;
   pp.cache.data = P.d_cache;
   pp.cache.slot_word = P.d_slot_word;
   pp.cache.page_slot = P.d_page_slot;
-  pp.cache.clock_hand = P.d_ctrl + PagedState::kClock;
+  pp.cache.clock_hand = P.ctrl(PagedState::kClock);
   pp.cache.slots = (uint32_t)P.slots;
   pp.cache.page_bytes = ix->page_bytes;
   pp.cache.mq = P.d_mq;
   pp.cache.mq_mask = P.ring_cap - 1;
-  pp.cache.mq_tail = P.d_ctrl + PagedState::kMqTail;
+  pp.cache.mq_tail = P.ctrl(PagedState::kMqTail);
   pp.geom = rp.geom;
   pp.n = rp.n;
   pp.D = rp.D;
@@ -429,22 +438,25 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.cq = P.d_cq;
   pp.cq_mask = P.ring_cap - 1;
   pp.cq_tail = P.d_cq_tail;
-  pp.cq_head = P.d_ctrl + PagedState::kCqHead;
-  pp.tail_seen = P.d_ctrl + PagedState::kTailSeen;
-  pp.poll_lock = reinterpret_cast<unsigned int *>(P.d_ctrl + PagedState::kPollLock);
+  pp.cq_head = P.ctrl(PagedState::kCqHead);
+  pp.tail_seen = P.ctrl(PagedState::kTailSeen);
+  pp.poll_lock = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kPollLock));
   pp.abort_flag = P.d_abort;
-  pp.abort_seen = reinterpret_cast<unsigned int *>(P.d_ctrl + PagedState::kAbortSeen);
+  pp.abort_seen = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kAbortSeen));
   pp.queries = rp.queries;
   pp.nq = rp.nq;
   pp.k = rp.k;
   pp.L = rp.L;
   pp.W = rp.W;
-  pp.next_query = reinterpret_cast<unsigned int *>(P.d_ctrl + PagedState::kNextQuery);
+  pp.next_query = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kNextQuery));
+  pp.done_queries = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kDoneQueries));
+  pp.query_waves = (uint32_t)qwaves;
+  pp.dedicated_poller = fwaves > 0 ? 1 : 0;
   pp.out_ids = rp.out_ids;
   pp.out_dists = rp.out_dists;
   pp.ht_pool = P.d_ht_pool;
   pp.oversub = oversub;
-  pp.max_pending = kMaxPendingPerQuery;
+  pp.max_pending = max_pending;
   pp.blocking = ix->blocking;
   pp.stats = rp.stats;
 
@@ -575,6 +587,7 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
     stats->bytes_served = h_stats[kStatServed] * ix->page_bytes;
     stats->parks = h_stats[kStatPark];
     stats->resumes = h_stats[kStatResume];
+    stats->proxy_peak = ix->paged ? ix->paged->proxy.max_in_flight() : 0;
     stats->wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
   }
   if (timed_out) return fail(GORIO_ETIMEOUT, "paged search made no progress within the watchdog limit");

@@ -47,7 +47,12 @@ struct PagedState {
   uint64_t ht_pool_entries = 0;
   Proxy proxy;
 
-  enum Ctrl { kClock = 0, kMqTail, kCqHead, kTailSeen, kPollLock, kAbortSeen, kNextQuery, kCtrlWords = 8 };
+  enum Ctrl { kClock = 0, kMqTail, kCqHead, kTailSeen, kPollLock, kAbortSeen, kNextQuery, kDoneQueries, kCtrlWords = 8 };
+  // each control word on its own 256-byte line: they are hot atomics of
+  // different waves and must not serialize on one L2 channel
+  static constexpr uint32_t kCtrlStride = 32;  // u64 words
+  uint32_t ctrl_stride = kCtrlStride;
+  unsigned long long *ctrl(int w) const { return d_ctrl + (size_t)w * ctrl_stride; }
 
   void release() {
     proxy.stop();

@@ -4,6 +4,7 @@
 #include <chrono>
 #include <deque>
 #include <utility>
+#include <vector>
 
 #if defined(__x86_64__)
 #include <immintrin.h>
@@ -23,13 +24,15 @@ uint64_t now_ns() {
 }  // namespace
 
 void Proxy::start(unsigned long long *mq, uint32_t mq_mask, unsigned long long *cq, uint32_t cq_mask,
-                  unsigned long long *cq_tail) {
+                  unsigned long long *cq_tail, uint32_t rings, uint32_t tail_stride) {
   stop();
   mq_ = mq;
   mq_mask_ = mq_mask;
   cq_ = cq;
   cq_mask_ = cq_mask;
   cq_tail_ = cq_tail;
+  rings_ = rings ? rings : 1;
+  tail_stride_ = tail_stride ? tail_stride : 1;
   quit_.store(false);
   active_.store(false);
   th_ = std::thread([this] { loop(); });
@@ -63,7 +66,8 @@ void Proxy::loop() {
   // (descriptor, due time); latency is the same for every request, so FIFO
   // order is deadline order
   std::deque<std::pair<unsigned long long, uint64_t>> fifo;
-  uint64_t head = 0, tail = 0, epoch = ~0ull;
+  std::vector<uint64_t> tails;  // completions published per ring
+  uint64_t head = 0, dealt = 0, epoch = ~0ull;
   while (!quit_.load(std::memory_order_relaxed)) {
     if (!active_.load(std::memory_order_acquire)) {
       idle_.store(true, std::memory_order_release);
@@ -75,11 +79,11 @@ void Proxy::loop() {
     if (epoch != epoch_.load()) {  // a new search: rings were reset by the host
       epoch = epoch_.load();
       fifo.clear();
-      head = tail = 0;
+      tails.assign(rings_, 0);
+      head = dealt = 0;
     }
     const uint64_t lat = latency_ns_.load(std::memory_order_relaxed);
     const uint32_t cap = max_outstanding_.load(std::memory_order_relaxed);
-    const uint64_t now = now_ns();
     uint32_t intake = 0;
     while (fifo.size() < cap) {
       unsigned long long *slot = &mq_[head & mq_mask_];
@@ -87,9 +91,13 @@ void Proxy::loop() {
       if (e == 0) break;
       __atomic_store_n(slot, 0ull, __ATOMIC_RELAXED);
       ++head;
-      fifo.emplace_back(e, now + lat);
+      fifo.emplace_back(e, 0);
       ++intake;
     }
+    // the clock is read after the intake, so no request is due before it was
+    // published plus the latency
+    const uint64_t now = now_ns();
+    for (size_t i = fifo.size() - intake; i < fifo.size(); ++i) fifo[i].second = now + lat;
     if (intake) {
       requests_.fetch_add(intake, std::memory_order_relaxed);
       if (fifo.size() > max_in_flight_.load(std::memory_order_relaxed))
@@ -97,13 +105,18 @@ void Proxy::loop() {
     }
     uint32_t done = 0;
     while (!fifo.empty() && fifo.front().second <= now) {
-      cq_[(tail + done) & cq_mask_] = fifo.front().first;
+      const uint32_t r = (uint32_t)(dealt++ % rings_);
+      cq_[(uint64_t)r * (cq_mask_ + 1) + (tails[r]++ & cq_mask_)] = fifo.front().first;
       fifo.pop_front();
       ++done;
     }
     if (done) {
-      tail += done;
-      __atomic_store_n(cq_tail_, (unsigned long long)tail, __ATOMIC_RELEASE);
+      // publish every ring that received completions (entries before tails)
+      const uint32_t touched = done < rings_ ? done : rings_;
+      for (uint32_t i = 0; i < touched; ++i) {
+        const uint32_t r = (uint32_t)((dealt - 1 - i) % rings_);
+        __atomic_store_n(&cq_tail_[(uint64_t)r * tail_stride_], (unsigned long long)tails[r], __ATOMIC_RELEASE);
+      }
       completed_.fetch_add(done, std::memory_order_relaxed);
     }
     if (!intake && !done) GORIO_PAUSE();

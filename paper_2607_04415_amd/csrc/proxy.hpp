@@ -4,7 +4,7 @@
 // page-level descriptors: it takes {page, slot} descriptors that GPU waves
 // publish into a ring in coherent pinned memory, holds each one until its
 // injected service latency has elapsed (the stand-in for a remote read), and
-// publishes it to the completion ring the GPU polls.  It never looks at query
+// publishes it to a completion ring the GPU polls (one ring per GPU fill wave).  It never looks at query
 // state.  It batches both directions and caps the requests it holds in flight.
 // The page bytes themselves are copied by GPU waves from the pinned backing
 // store into the HBM slot, standing in for the RNIC's direct placement.
@@ -24,8 +24,10 @@ class Proxy {
   Proxy &operator=(const Proxy &) = delete;
 
   // Rings live in host memory that both sides can access; capacities are powers of two.
+  // Completions are dealt round-robin over `rings` completion rings: ring r is
+  // cq + r * (cq_mask + 1), its publish index cq_tail[r * tail_stride].
   void start(unsigned long long *mq, uint32_t mq_mask, unsigned long long *cq, uint32_t cq_mask,
-             unsigned long long *cq_tail);
+             unsigned long long *cq_tail, uint32_t rings, uint32_t tail_stride);
   // Reset ring indices and counters for a new search and begin serving.
   void begin(double latency_us, uint32_t max_outstanding);
   // Stop serving (the search ended); descriptors in flight are dropped.
@@ -40,7 +42,7 @@ class Proxy {
   void loop();
 
   unsigned long long *mq_ = nullptr, *cq_ = nullptr, *cq_tail_ = nullptr;
-  uint32_t mq_mask_ = 0, cq_mask_ = 0;
+  uint32_t mq_mask_ = 0, cq_mask_ = 0, rings_ = 1, tail_stride_ = 1;
   std::atomic<bool> quit_{false}, active_{false}, idle_{true};
   std::atomic<uint64_t> epoch_{0};
   std::atomic<uint64_t> latency_ns_{0};

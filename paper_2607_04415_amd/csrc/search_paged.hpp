@@ -30,7 +30,7 @@ constexpr int kPagedMaxW = 64;
 constexpr uint32_t kTodo = 0xFFFFFFFFu;  // item not requested yet
 constexpr uint32_t kDone = 0xFFFFFFFEu;  // item handled; other values: waiting on that cache slot
 constexpr int kPagedHtLog2 = 13;
-constexpr uint32_t kFillBatch = 8;
+constexpr uint32_t kFillBatch = 4;   // completions one wave claims and copies at a time
 
 enum : uint32_t { kPhSelect = 0, kPhExpand = 1, kPhEval = 2 };
 
@@ -47,12 +47,15 @@ struct PagedParams {
   const unsigned long long *cq_tail;      // proxy's publish index (host memory)
   unsigned long long *cq_head;            // next completion to claim (device)
   unsigned long long *tail_seen;          // device mirror of cq_tail
-  unsigned int *poll_lock;                // device: one wave at a time reads host memory
+  unsigned int *poll_lock;                // device try-lock for host reads when no poller wave runs
+  int dedicated_poller;                   // the first fill wave keeps the mirrors fresh
   const unsigned int *abort_flag;         // host memory; nonzero ends the search
   unsigned int *abort_seen;               // device mirror of abort_flag
   const uint8_t *queries;
   uint32_t nq, k, L, W;
   unsigned int *next_query;
+  unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
+  uint32_t query_waves;                   // blocks [0, query_waves) run queries; the rest only fill
   uint32_t *out_ids;
   int32_t *out_dists;
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
@@ -80,12 +83,30 @@ __device__ __forceinline__ bool aborted(const PagedParams &p) {
   return __hip_atomic_load(p.abort_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
 }
 
-// Record of node v inside cache slot s.
+// Byte offset of node v's record inside cache slot s.
 template <bool N2S>
-__device__ __forceinline__ const uint8_t *cached_record(const PagedParams &p, uint32_t s, uint32_t v) {
+__device__ __forceinline__ uint32_t cached_record(const PagedParams &p, uint32_t s, uint32_t v) {
   const uint32_t sl = slot_ct<N2S>(p.geom, v);
   const uint32_t within = sl - fastdiv(sl, p.geom.rpp) * p.geom.rpp.d;
-  return p.cache.data + (uint64_t)s * p.cache.page_bytes + within * p.geom.record_bytes;
+  return s * (uint32_t)p.cache.page_bytes + within * p.geom.record_bytes;
+}
+
+// The query-side vector read of a cached record (coherent, see page_cache.hpp).
+template <int VDW, bool EXACT>
+__device__ __forceinline__ void load_cached_vec(U8Vec<VDW, EXACT> &x, __amdgpu_buffer_rsrc_t r, uint32_t rec,
+                                                int gl, uint32_t dwords) {
+  const uint32_t base = rec + (uint32_t)gl * VDW * 4u;
+  if constexpr (EXACT && VDW % 4 == 0) {
+#pragma unroll
+    for (int t = 0; t < VDW; t += 4) {
+      const uint4 u = coherent_load_u128(r, base + t * 4u);
+      x.w[t] = u.x; x.w[t + 1] = u.y; x.w[t + 2] = u.z; x.w[t + 3] = u.w;
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < VDW; ++t)
+      x.w[t] = (EXACT || (uint32_t)(gl * VDW + t) < dwords) ? coherent_load_u32(r, base + t * 4u) : 0u;
+  }
 }
 
 template <bool N2S>
@@ -97,7 +118,7 @@ __device__ __forceinline__ uint32_t page_of(const PagedParams &p, uint32_t v) {
 // lane i of e) from the backing store into their cache slots: 16 loads in
 // flight per lane, then the stores.  Kept out of line so the copy gets its
 // own registers.
-__device__ __attribute__((noinline)) void copy_pages4(const uint8_t *backing, uint8_t *cache,
+__device__ __attribute__((noinline)) void copy_pages4(const uint8_t *backing, __amdgpu_buffer_rsrc_t cache,
                                                       unsigned long long e, uint32_t i0, uint32_t n) {
   const int l = lane_id();
   const uint32_t i1 = min(i0 + 1, n - 1), i2 = min(i0 + 2, n - 1), i3 = min(i0 + 3, n - 1);
@@ -110,26 +131,41 @@ __device__ __attribute__((noinline)) void copy_pages4(const uint8_t *backing, ui
   const uint4 b0 = s1[l], b1 = s1[l + 64], b2 = s1[l + 128], b3 = s1[l + 192];
   const uint4 c0 = s2[l], c1 = s2[l + 64], c2 = s2[l + 128], c3 = s2[l + 192];
   const uint4 d0 = s3[l], d1 = s3[l + 64], d2 = s3[l + 128], d3 = s3[l + 192];
-  uint4 *t0 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e0 * 4096u);
-  t0[l] = a0; t0[l + 64] = a1; t0[l + 128] = a2; t0[l + 192] = a3;
+  const uint32_t lo = (uint32_t)l * 16u;
+  uint32_t t = (uint32_t)e0 * 4096u + lo;
+  coherent_store_u128(cache, t, a0); coherent_store_u128(cache, t + 1024, a1);
+  coherent_store_u128(cache, t + 2048, a2); coherent_store_u128(cache, t + 3072, a3);
   if (i0 + 1 < n) {
-    uint4 *t1 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e1 * 4096u);
-    t1[l] = b0; t1[l + 64] = b1; t1[l + 128] = b2; t1[l + 192] = b3;
+    t = (uint32_t)e1 * 4096u + lo;
+    coherent_store_u128(cache, t, b0); coherent_store_u128(cache, t + 1024, b1);
+    coherent_store_u128(cache, t + 2048, b2); coherent_store_u128(cache, t + 3072, b3);
   }
   if (i0 + 2 < n) {
-    uint4 *t2 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e2 * 4096u);
-    t2[l] = c0; t2[l + 64] = c1; t2[l + 128] = c2; t2[l + 192] = c3;
+    t = (uint32_t)e2 * 4096u + lo;
+    coherent_store_u128(cache, t, c0); coherent_store_u128(cache, t + 1024, c1);
+    coherent_store_u128(cache, t + 2048, c2); coherent_store_u128(cache, t + 3072, c3);
   }
   if (i0 + 3 < n) {
-    uint4 *t3 = reinterpret_cast<uint4 *>(cache + (uint64_t)(uint32_t)e3 * 4096u);
-    t3[l] = d0; t3[l + 64] = d1; t3[l + 128] = d2; t3[l + 192] = d3;
+    t = (uint32_t)e3 * 4096u + lo;
+    coherent_store_u128(cache, t, d0); coherent_store_u128(cache, t + 1024, d1);
+    coherent_store_u128(cache, t + 2048, d2); coherent_store_u128(cache, t + 3072, d3);
   }
 }
 
+// Read the proxy's tail and the abort flag from host memory into their HBM
+// mirrors (one PCIe round trip).
+__device__ __forceinline__ unsigned long long refresh_mirrors(const PagedParams &p) {
+  const unsigned long long t = __hip_atomic_load(p.cq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  atomicMax(p.tail_seen, t);
+  if (__hip_atomic_load(p.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0)
+    atomicExch(p.abort_seen, 1u);
+  return t;
+}
+
 // Claim up to kFillBatch completions and copy their pages into the cache.
-// Host memory is read by one wave at a time (the poll lock): it refreshes the
-// device mirrors of the proxy's tail and of the abort flag; every other wave
-// only reads the mirrors.
+// Only one wave reads host memory: the dedicated poller when fill waves run,
+// otherwise whichever query wave wins the try-lock.  All others read the
+// HBM mirrors of the proxy's tail and of the abort flag.
 __device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
   const int l = lane_id();
   uint32_t n = 0;
@@ -137,11 +173,8 @@ __device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
   if (l == 0) {
     h = __hip_atomic_load(p.cq_head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     unsigned long long t = __hip_atomic_load(p.tail_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (h >= t && atomicCAS(p.poll_lock, 0u, 1u) == 0u) {
-      t = __hip_atomic_load(p.cq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-      atomicMax(p.tail_seen, t);
-      if (__hip_atomic_load(p.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0)
-        atomicExch(p.abort_seen, 1u);
+    if (h >= t && !p.dedicated_poller && atomicCAS(p.poll_lock, 0u, 1u) == 0u) {
+      t = refresh_mirrors(p);
       atomicExch(p.poll_lock, 0u);
     }
     if (h < t) {
@@ -168,20 +201,21 @@ __device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
       if (n == 0) return 0;
     }
   }
+  const __amdgpu_buffer_rsrc_t crs = cache_rsrc(p.cache);
   if (p.cache.page_bytes == 4096) {
-    for (uint32_t i0 = 0; i0 < n; i0 += 4) copy_pages4(p.backing, p.cache.data, e, i0, n);
+    copy_pages4(p.backing, crs, e, 0, n);  // n <= kFillBatch = 4
   } else {
     const uint32_t chunks = (uint32_t)(p.cache.page_bytes / 16);
     for (uint32_t i = 0; i < n; ++i) {
       const uint64_t ei = readlane64(e, i);
       const uint4 *src = reinterpret_cast<const uint4 *>(p.backing + (uint64_t)((uint32_t)(ei >> 32) - 1u) *
                                                                          p.cache.page_bytes);
-      uint4 *dst = reinterpret_cast<uint4 *>(p.cache.data + (uint64_t)(uint32_t)ei * p.cache.page_bytes);
-      for (uint32_t c = l; c < chunks; c += kWave) dst[c] = src[c];
+      const uint32_t base = (uint32_t)ei * (uint32_t)p.cache.page_bytes;
+      for (uint32_t c = l; c < chunks; c += kWave) coherent_store_u128(crs, base + c * 16u, src[c]);
     }
   }
-  // page bytes visible device-wide before any READY state
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  // page bytes performed device-wide before any READY state
+  wait_stores_performed();
   if ((uint32_t)l < n) atomicAdd(&p.cache.slot_word[(uint32_t)e], (1ull << kStateShift) | kRefBit);
   return n;
 }
@@ -243,6 +277,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
   const uint32_t dwords = p.D >> 2;
   const uint32_t GB = min(kCandCap / p.R, (uint32_t)kPagedMaxW);
   constexpr int kIdsPerLane = kCandCap / kWave;
+  const __amdgpu_buffer_rsrc_t crs = cache_rsrc(p.cache);
 
   U8Vec<VDW, EXACT> q;
   q.load(p.queries + (uint64_t)S.qi * p.D, gl, dwords);
@@ -312,22 +347,21 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
       if (mine && !ready) S.bstate[bi] = st;
       uint64_t rmask = ballot(ready);
       if (rmask) {
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        order_after_ready();
         while (rmask) {
           const int b = __builtin_ctzll(rmask);
           rmask &= rmask - 1;
           const uint32_t s_b = readlane(slot, b);
           const uint32_t u = S.beam[S.b0 + b];
-          const uint8_t *adj = cached_record<N2S>(p, s_b, u) + p.geom.vec_bytes;
-          const uint32_t deg = min(*reinterpret_cast<const uint32_t *>(adj), p.R);
-          const uint32_t *idp = reinterpret_cast<const uint32_t *>(adj + 4);
+          const uint32_t adj = cached_record<N2S>(p, s_b, u) + p.geom.vec_bytes;
+          const uint32_t deg = min(coherent_load_u32(crs, adj), p.R);
           for (uint32_t j0 = 0; j0 < p.R; j0 += kCandCap) {
             uint32_t ids[kIdsPerLane];
             bool valid[kIdsPerLane], isnew[kIdsPerLane], rec[kIdsPerLane];
 #pragma unroll
             for (int t = 0; t < kIdsPerLane; ++t) {
               const uint32_t j = j0 + t * kWave + l;
-              ids[t] = j < deg ? idp[j] : kNoEdge;
+              ids[t] = j < deg ? coherent_load_u32(crs, adj + 4u + 4u * j) : kNoEdge;
               valid[t] = ids[t] < p.n;
             }
             HT::template test_and_set_n<kIdsPerLane>(ht, ids, valid, S.ht_used < HT::kLimit, isnew, rec);
@@ -407,7 +441,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
 #pragma unroll
       for (int t = 0; t < kIdsPerLane; ++t) any_ready |= ballot(rdy[t]) != 0;
       if (any_ready) {
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        order_after_ready();
 #pragma unroll
         for (int t = 0; t < kIdsPerLane; ++t) {
           const uint64_t mr = ballot(rdy[t]);
@@ -428,7 +462,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
             const uint32_t idx = rr * 8 + g;
             const uint32_t ci = idx < cnt ? rc[idx] : rc[0];
             const uint32_t si = idx < cnt ? rs[idx] : rs[0];
-            x[rr].load(cached_record<N2S>(p, si, S.cand[ci]), gl, dwords);
+            load_cached_vec(x[rr], crs, cached_record<N2S>(p, si, S.cand[ci]), gl, dwords);
           }
           int mine_d = 0;
 #pragma unroll
@@ -491,8 +525,32 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
   return false;
 }
 
+// A fill wave: claims completions and copies pages until every query is done.
+// The first fill wave also refreshes the host mirrors on every pass.
+__device__ void fill_loop(const PagedParams &p, bool poller) {
+  unsigned long long served = 0;
+  uint32_t idle = 0;
+  for (;;) {
+    if (poller && lane_id() == 0) refresh_mirrors(p);
+    if (aborted(p)) break;
+    if (__hip_atomic_load(p.done_queries, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.nq) break;
+    const uint32_t n = service_completions(p);
+    served += n;
+    if (n == 0) {
+      if (!poller && ++idle > 8) __builtin_amdgcn_s_sleep(8);
+    } else {
+      idle = 0;
+    }
+  }
+  if (lane_id() == 0) atomicAdd(&p.stats[6], served);
+}
+
 template <int KPL, int VDW, bool EXACT, bool N2S>
 __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
+  if (blockIdx.x >= p.query_waves) {
+    fill_loop(p, blockIdx.x == p.query_waves);
+    return;
+  }
   extern __shared__ __align__(16) unsigned char lds[];
   QSlot<KPL> *slots = reinterpret_cast<QSlot<KPL> *>(lds);
   const int l = lane_id();
@@ -511,7 +569,7 @@ __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
     bool any_active = false, progressed = false;
     for (uint32_t j = 0; j < p.oversub; ++j) {
       QSlot<KPL> &S = slots[j];
-      uint32_t *ht = p.ht_pool + ((uint64_t)(blockIdx.x * p.oversub + j) << kPagedHtLog2);
+      uint32_t *ht = p.ht_pool + ((uint64_t)(blockIdx.x * p.oversub + j) << kPagedHtLog2);  // query waves only
       if (!S.active) {
         if (!admitting) continue;
         uint32_t qi = 0;
@@ -557,6 +615,7 @@ __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
         if (done) {
           S.active = 0;
           S.parked = 0;
+          atomicAdd(p.done_queries, 1u);
         } else {
           S.parked = 1;
         }

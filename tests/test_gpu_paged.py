@@ -76,18 +76,30 @@ def test_paged_tiny_cache_slot_reuse(torch_dev, small):
     assert st["pages_served"] > 10 * 128
 
 
-def test_warm_cache_second_search(torch_dev, small):
-    a, q, oids, od, _ = small
+def test_warm_cache_second_search(orc, torch_dev):
+    """A cache that never has to evict: the second search over the same
+    queries finds every page resident (no misses) and returns the same answers."""
+    spec = IndexSpec(n=200000, D=128, dtype="u8", clusters=16, sigma=20.0, r_near=16, r_rand=16, seed=43)
+    a = index_arrays(spec)
+    q = query_array(spec, QuerySpec(4, 44))
+    e = orc.medoid(a["x"])
+    oids, od, _, _ = orc.pack(a["x"], a["graph"]).search(q, 10, 32, 4, e)
     ix = g.Index(a["x"], a["graph"])
-    ix.set_cache(ix.info["index_bytes"] // 2)
+    nearly_all = int(0.95 * ix.info["index_bytes"])    # far more slots than 4 queries touch
+    ix.set_cache(nearly_all)
     s1 = search(torch_dev, ix, q, 10, 32, 4)
     s2 = search(torch_dev, ix, q, 10, 32, 4)           # cache carries over
     for gi, gd, _ in (s1, s2):
         assert_same(gi, gd, oids, od)
-    assert s2[2]["misses"] < s1[2]["misses"]
-    ix.set_cache(ix.info["index_bytes"] // 2)           # empties it again
+    assert s1[2]["misses"] > 0
+    assert s2[2]["misses"] == 0 and s2[2]["pages_served"] == 0
+    assert s2[2]["hits"] == s1[2]["hits"] + s1[2]["misses"]
+    ix.set_cache(nearly_all)                            # empties it again
     s3 = search(torch_dev, ix, q, 10, 32, 4)
     assert_same(s3[0], s3[1], oids, od)
+    # cold again (exact counts vary: a page two queries want at once is a
+    # miss for both or a hit for the later one, depending on timing)
+    assert s3[2]["misses"] > s1[2]["misses"] // 2
 
 
 def test_paged_to_resident_and_back(torch_dev, small):

@@ -100,7 +100,7 @@ WORKLOADS = {
         Workload("u8-1m-hbm", _U8_1M, QuerySpec(10_000, 2002), k=10, L=64, W=4,
                  description="1M x 128-d uint8, R=64, 10k queries, L=64 W=4, HBM-resident"),
         Workload("u8-1m-cache10-lat0", _U8_1M, QuerySpec(10_000, 2002), k=10, L=64, W=4,
-                 cache_frac=0.10, latency_us=0.0,
+                 cache_frac=0.10, latency_us=0.0, oversub=4,
                  description="1M uint8 index, 10% HBM page cache (cold), pinned-host "
                              "backing store, 0 us injected latency"),
         Workload("u8-1m-cache10-lat20", _U8_1M, QuerySpec(100_000, 2004), k=10, L=64, W=4,
