@@ -260,15 +260,18 @@ gorio_status gorio_index::make_paged(uint64_t slots) {
   HIP_OR_FAIL(hipMalloc(&P.d_slot_word, slots * sizeof(unsigned long long)));
   HIP_OR_FAIL(hipMalloc(&P.d_page_slot, num_pages * sizeof(uint32_t)));
   HIP_OR_FAIL(hipMalloc(&P.d_ctrl, PagedState::kCtrlWords * PagedState::kCtrlStride * sizeof(unsigned long long)));
+  // Every descriptor and every unconsumed completion belongs to a LOADING
+  // slot, so no ring ever holds more than `slots` live entries.
   P.ring_cap = next_pow2(2 * slots + 1024);
+  P.cq_cap = next_pow2(slots + 1024);
   HIP_OR_FAIL(host_ring(&P.h_mq, &P.d_mq, P.ring_cap));
-  HIP_OR_FAIL(host_ring(&P.h_cq, &P.d_cq, P.ring_cap));
-  HIP_OR_FAIL(host_ring(&P.h_cq_tail, &P.d_cq_tail, 8));
+  HIP_OR_FAIL(host_ring(&P.h_cq, &P.d_cq, (size_t)P.cq_cap * PagedState::kMaxRings));
+  HIP_OR_FAIL(host_ring(&P.h_cq_tail, &P.d_cq_tail, (size_t)PagedState::kTailStride * PagedState::kMaxRings));
   HIP_OR_FAIL(host_ring(&P.h_abort, &P.d_abort, 16));
   cache_slots = slots;
   gorio_status st = reset_cache();
   if (st != GORIO_OK) return st;
-  P.proxy.start(P.h_mq, P.ring_cap - 1, P.h_cq, P.ring_cap - 1, P.h_cq_tail, 1, 1);
+  P.proxy.start(P.h_mq, P.ring_cap - 1, P.h_cq, P.cq_cap - 1, P.h_cq_tail, PagedState::kTailStride);
   return GORIO_OK;
 }
 
@@ -395,9 +398,11 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   const uint64_t q_cache = std::max<uint64_t>(1, P.slots / (2ull * max_pending));
   const uint64_t q_live = std::min<uint64_t>({(uint64_t)cus * 8 * oversub, q_cache, rp.nq});
   const int qwaves = (int)std::max<uint64_t>(1, (q_live + oversub - 1) / oversub);
-  // extra waves that only copy arriving pages, so the fill rate does not
-  // depend on how many queries run at once
-  const int fwaves = std::max(0, env_int("GORIO_FILL_WAVES", 16));
+  // waves that only copy arriving pages, each from a completion ring of its
+  // own, so the fill rate does not depend on how many queries run at once
+  // and no two waves contend for completions
+  const int fwaves = std::max(0, std::min((int)PagedState::kMaxRings, env_int("GORIO_FILL_WAVES", 16)));
+  const uint32_t rings = (uint32_t)std::max(1, fwaves);
   const int grid = qwaves + fwaves;
   const uint64_t ht_entries = (uint64_t)qwaves * oversub << kPagedHtLog2;
   if (ht_entries > P.ht_pool_entries) {
@@ -410,7 +415,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   // per-search reset: rings empty, indices zero (the clock hand and the cached
   // pages stay: a warm cache carries over to the next search)
   memset(P.h_mq, 0, P.ring_cap * sizeof(unsigned long long));
-  __atomic_store_n(P.h_cq_tail, 0ull, __ATOMIC_RELEASE);
+  for (uint32_t r = 0; r < rings; ++r) __atomic_store_n(P.h_cq_tail + (size_t)r * PagedState::kTailStride, 0ull, __ATOMIC_RELEASE);
   __atomic_store_n(P.h_abort, 0u, __ATOMIC_RELEASE);
   fill_u32<<<1, 256, 0, s>>>(reinterpret_cast<uint32_t *>(P.ctrl(PagedState::kMqTail)),
                              2 * (PagedState::kCtrlWords - PagedState::kMqTail) * PagedState::kCtrlStride, 0u);
@@ -436,8 +441,9 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   HIP_OR_FAIL(hipHostGetDevicePointer(reinterpret_cast<void **>(&d_backing), ix->h_backing, 0));
   pp.backing = d_backing;
   pp.cq = P.d_cq;
-  pp.cq_mask = P.ring_cap - 1;
+  pp.cq_mask = P.cq_cap - 1;
   pp.cq_tail = P.d_cq_tail;
+  pp.tail_stride = PagedState::kTailStride;
   pp.cq_head = P.ctrl(PagedState::kCqHead);
   pp.tail_seen = P.ctrl(PagedState::kTailSeen);
   pp.poll_lock = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kPollLock));
@@ -450,8 +456,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.W = rp.W;
   pp.next_query = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kNextQuery));
   pp.done_queries = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kDoneQueries));
-  pp.query_waves = (uint32_t)qwaves;
-  pp.dedicated_poller = fwaves > 0 ? 1 : 0;
+  pp.fill_waves = (uint32_t)fwaves;
   pp.out_ids = rp.out_ids;
   pp.out_dists = rp.out_dists;
   pp.ht_pool = P.d_ht_pool;
@@ -460,7 +465,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.blocking = ix->blocking;
   pp.stats = rp.stats;
 
-  P.proxy.begin(ix->latency_us, ix->max_outstanding);
+  P.proxy.begin(ix->latency_us, ix->max_outstanding, rings);
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
   hipError_t le;
   if (rp.L <= 64) le = launch_paged_kpl<1>(pp, grid, s);

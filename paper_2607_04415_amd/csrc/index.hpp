@@ -42,7 +42,12 @@ struct PagedState {
   unsigned long long *h_cq = nullptr, *d_cq = nullptr;
   unsigned long long *h_cq_tail = nullptr, *d_cq_tail = nullptr;
   unsigned int *h_abort = nullptr, *d_abort = nullptr;
-  uint32_t ring_cap = 0;
+  uint32_t ring_cap = 0;   // descriptor ring entries
+  uint32_t cq_cap = 0;     // entries of each completion ring
+  // completion rings: one per fill wave (or one shared ring when query waves
+  // serve completions themselves); tails 128 bytes apart
+  static constexpr uint32_t kMaxRings = 64;
+  static constexpr uint32_t kTailStride = 16;  // u64 words
   uint32_t *d_ht_pool = nullptr;
   uint64_t ht_pool_entries = 0;
   Proxy proxy;
@@ -74,6 +79,7 @@ struct PagedState {
     h_abort = d_abort = nullptr;
     slots = 0;
     ring_cap = 0;
+    cq_cap = 0;
     ht_pool_entries = 0;
   }
   ~PagedState() { release(); }

@@ -24,21 +24,21 @@ uint64_t now_ns() {
 }  // namespace
 
 void Proxy::start(unsigned long long *mq, uint32_t mq_mask, unsigned long long *cq, uint32_t cq_mask,
-                  unsigned long long *cq_tail, uint32_t rings, uint32_t tail_stride) {
+                  unsigned long long *cq_tail, uint32_t tail_stride) {
   stop();
   mq_ = mq;
   mq_mask_ = mq_mask;
   cq_ = cq;
   cq_mask_ = cq_mask;
   cq_tail_ = cq_tail;
-  rings_ = rings ? rings : 1;
   tail_stride_ = tail_stride ? tail_stride : 1;
   quit_.store(false);
   active_.store(false);
   th_ = std::thread([this] { loop(); });
 }
 
-void Proxy::begin(double latency_us, uint32_t max_outstanding) {
+void Proxy::begin(double latency_us, uint32_t max_outstanding, uint32_t rings) {
+  rings_.store(rings ? rings : 1);
   latency_ns_.store((uint64_t)(latency_us * 1000.0));
   max_outstanding_.store(max_outstanding ? max_outstanding : 4096);
   requests_.store(0);
@@ -68,6 +68,7 @@ void Proxy::loop() {
   std::deque<std::pair<unsigned long long, uint64_t>> fifo;
   std::vector<uint64_t> tails;  // completions published per ring
   uint64_t head = 0, dealt = 0, epoch = ~0ull;
+  uint32_t rings = 1;
   while (!quit_.load(std::memory_order_relaxed)) {
     if (!active_.load(std::memory_order_acquire)) {
       idle_.store(true, std::memory_order_release);
@@ -79,7 +80,8 @@ void Proxy::loop() {
     if (epoch != epoch_.load()) {  // a new search: rings were reset by the host
       epoch = epoch_.load();
       fifo.clear();
-      tails.assign(rings_, 0);
+      rings = rings_.load();
+      tails.assign(rings, 0);
       head = dealt = 0;
     }
     const uint64_t lat = latency_ns_.load(std::memory_order_relaxed);
@@ -105,16 +107,16 @@ void Proxy::loop() {
     }
     uint32_t done = 0;
     while (!fifo.empty() && fifo.front().second <= now) {
-      const uint32_t r = (uint32_t)(dealt++ % rings_);
+      const uint32_t r = (uint32_t)(dealt++ % rings);
       cq_[(uint64_t)r * (cq_mask_ + 1) + (tails[r]++ & cq_mask_)] = fifo.front().first;
       fifo.pop_front();
       ++done;
     }
     if (done) {
       // publish every ring that received completions (entries before tails)
-      const uint32_t touched = done < rings_ ? done : rings_;
+      const uint32_t touched = done < rings ? done : rings;
       for (uint32_t i = 0; i < touched; ++i) {
-        const uint32_t r = (uint32_t)((dealt - 1 - i) % rings_);
+        const uint32_t r = (uint32_t)((dealt - 1 - i) % rings);
         __atomic_store_n(&cq_tail_[(uint64_t)r * tail_stride_], (unsigned long long)tails[r], __ATOMIC_RELEASE);
       }
       completed_.fetch_add(done, std::memory_order_relaxed);

@@ -24,12 +24,13 @@ class Proxy {
   Proxy &operator=(const Proxy &) = delete;
 
   // Rings live in host memory that both sides can access; capacities are powers of two.
-  // Completions are dealt round-robin over `rings` completion rings: ring r is
-  // cq + r * (cq_mask + 1), its publish index cq_tail[r * tail_stride].
+  // Completions are dealt round-robin over the completion rings of a search:
+  // ring r is cq + r * (cq_mask + 1), its publish index cq_tail[r * tail_stride].
   void start(unsigned long long *mq, uint32_t mq_mask, unsigned long long *cq, uint32_t cq_mask,
-             unsigned long long *cq_tail, uint32_t rings, uint32_t tail_stride);
-  // Reset ring indices and counters for a new search and begin serving.
-  void begin(double latency_us, uint32_t max_outstanding);
+             unsigned long long *cq_tail, uint32_t tail_stride);
+  // Reset ring indices and counters for a new search and begin serving over
+  // `rings` completion rings (the caller has zeroed their tails).
+  void begin(double latency_us, uint32_t max_outstanding, uint32_t rings);
   // Stop serving (the search ended); descriptors in flight are dropped.
   void end();
   void stop();
@@ -42,7 +43,8 @@ class Proxy {
   void loop();
 
   unsigned long long *mq_ = nullptr, *cq_ = nullptr, *cq_tail_ = nullptr;
-  uint32_t mq_mask_ = 0, cq_mask_ = 0, rings_ = 1, tail_stride_ = 1;
+  uint32_t mq_mask_ = 0, cq_mask_ = 0, tail_stride_ = 1;
+  std::atomic<uint32_t> rings_{1};
   std::atomic<bool> quit_{false}, active_{false}, idle_{true};
   std::atomic<uint64_t> epoch_{0};
   std::atomic<uint64_t> latency_ns_{0};

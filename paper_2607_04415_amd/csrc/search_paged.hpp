@@ -7,9 +7,11 @@
 //   - admits a new query into a free slot (global atomic counter),
 //   - resumes a parked query when a page it waits on is READY in the cache
 //     (the per-slot ready test of Sec. 3.2) or when it can issue more requests,
-//   - otherwise claims completions from the proxy's ring and fills the pages
-//     (copies 4 KB from the pinned backing store into the HBM slot), then
-//     marks them READY.
+// Page service runs beside it: by default a few fill waves (the lowest block
+// indices) each consume a completion ring of their own, copy each page (4 KB
+// from the pinned backing store into its HBM slot) and mark it READY.  With
+// no fill waves, the query waves claim completions from one shared ring
+// whenever their queries cannot run.
 // A query runs its iteration (select -> expand -> evaluate -> merge) until a
 // record it needs is not resident: the miss is published as a descriptor
 // {page, slot}, the slot stays pinned, and the query is parked.  An
@@ -42,20 +44,21 @@ struct PagedParams {
   uint32_t entry;
   uint32_t num_pages;
   const uint8_t *backing;                 // pinned host copy of every page
-  const unsigned long long *cq;           // completions from the proxy (host memory)
+  const unsigned long long *cq;           // completion rings from the proxy (host memory), cq_mask + 1 entries each
   uint32_t cq_mask;
-  const unsigned long long *cq_tail;      // proxy's publish index (host memory)
-  unsigned long long *cq_head;            // next completion to claim (device)
-  unsigned long long *tail_seen;          // device mirror of cq_tail
-  unsigned int *poll_lock;                // device try-lock for host reads when no poller wave runs
-  int dedicated_poller;                   // the first fill wave keeps the mirrors fresh
+  const unsigned long long *cq_tail;      // proxy's publish index of each ring (host memory), tail_stride apart
+  uint32_t tail_stride;
+  uint32_t fill_waves;                    // blocks [0, fill_waves) only fill pages, wave k from ring k;
+                                          // 0: one shared ring served by the query waves
+  unsigned long long *cq_head;            // shared ring: next completion to claim (device)
+  unsigned long long *tail_seen;          // shared ring: device mirror of its tail
+  unsigned int *poll_lock;                // shared ring: try-lock for the one host read of the tail
   const unsigned int *abort_flag;         // host memory; nonzero ends the search
   unsigned int *abort_seen;               // device mirror of abort_flag
   const uint8_t *queries;
   uint32_t nq, k, L, W;
   unsigned int *next_query;
   unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
-  uint32_t query_waves;                   // blocks [0, query_waves) run queries; the rest only fill
   uint32_t *out_ids;
   int32_t *out_dists;
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
@@ -152,20 +155,58 @@ __device__ __attribute__((noinline)) void copy_pages4(const uint8_t *backing, __
   }
 }
 
-// Read the proxy's tail and the abort flag from host memory into their HBM
-// mirrors (one PCIe round trip).
-__device__ __forceinline__ unsigned long long refresh_mirrors(const PagedParams &p) {
-  const unsigned long long t = __hip_atomic_load(p.cq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  atomicMax(p.tail_seen, t);
+// Mirror the host abort flag into HBM, where every wave polls it.
+__device__ __forceinline__ void refresh_abort(const PagedParams &p) {
   if (__hip_atomic_load(p.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0)
     atomicExch(p.abort_seen, 1u);
-  return t;
 }
 
-// Claim up to kFillBatch completions and copy their pages into the cache.
-// Only one wave reads host memory: the dedicated poller when fill waves run,
-// otherwise whichever query wave wins the try-lock.  All others read the
-// HBM mirrors of the proxy's tail and of the abort flag.
+// Load completions [head, head + n) of a ring (entry i in lane i, n <= 64;
+// entries are published before the tail that covers them).  Returns how many
+// lead entries are well formed: a malformed one is never copied, so that the
+// copy cannot leave the backing store or the cache; its waiter times out.
+__device__ __forceinline__ uint32_t load_completions(const PagedParams &p, const unsigned long long *ring,
+                                                     unsigned long long head, uint32_t n,
+                                                     unsigned long long &e) {
+  const int l = lane_id();
+  e = 0;
+  if ((uint32_t)l < n)
+    e = __hip_atomic_load(&ring[(head + l) & p.cq_mask], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  const uint32_t pg = (uint32_t)(e >> 32) - 1u, sl = (uint32_t)e;
+  const uint64_t mbad = ballot((uint32_t)l < n && (pg >= p.num_pages || sl >= p.cache.slots));
+  if (mbad == 0) return n;
+  if (l == 0) atomicAdd(&p.stats[9], (unsigned long long)__popcll(mbad));
+  return (uint32_t)__builtin_ctzll(mbad);
+}
+
+// Copy the pages of the completions in lanes [0, n) of e into their cache
+// slots, kFillBatch at a time, and mark each batch READY once its bytes are
+// performed device-wide.
+__device__ __forceinline__ void fill_entries(const PagedParams &p, unsigned long long e, uint32_t n) {
+  const int l = lane_id();
+  const __amdgpu_buffer_rsrc_t crs = cache_rsrc(p.cache);
+  for (uint32_t i0 = 0; i0 < n; i0 += kFillBatch) {
+    if (p.cache.page_bytes == 4096) {
+      copy_pages4(p.backing, crs, e, i0, n);
+    } else {
+      const uint32_t chunks = (uint32_t)(p.cache.page_bytes / 16);
+      for (uint32_t i = i0; i < min(i0 + kFillBatch, n); ++i) {
+        const uint64_t ei = readlane64(e, i);
+        const uint4 *src = reinterpret_cast<const uint4 *>(p.backing + (uint64_t)((uint32_t)(ei >> 32) - 1u) *
+                                                                           p.cache.page_bytes);
+        const uint32_t base = (uint32_t)ei * (uint32_t)p.cache.page_bytes;
+        for (uint32_t c = l; c < chunks; c += kWave) coherent_store_u128(crs, base + c * 16u, src[c]);
+      }
+    }
+    wait_stores_performed();
+    if ((uint32_t)l >= i0 && (uint32_t)l < min(i0 + kFillBatch, n))
+      atomicAdd(&p.cache.slot_word[(uint32_t)e], (1ull << kStateShift) | kRefBit);
+  }
+}
+
+// Shared completion ring (no fill waves): claim up to kFillBatch completions
+// and fill their pages.  Only the wave that wins the try-lock reads the
+// proxy's tail from host memory; all others read its HBM mirror.
 __device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
   const int l = lane_id();
   uint32_t n = 0;
@@ -173,8 +214,10 @@ __device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
   if (l == 0) {
     h = __hip_atomic_load(p.cq_head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     unsigned long long t = __hip_atomic_load(p.tail_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (h >= t && !p.dedicated_poller && atomicCAS(p.poll_lock, 0u, 1u) == 0u) {
-      t = refresh_mirrors(p);
+    if (h >= t && atomicCAS(p.poll_lock, 0u, 1u) == 0u) {
+      t = __hip_atomic_load(p.cq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      atomicMax(p.tail_seen, t);
+      refresh_abort(p);
       atomicExch(p.poll_lock, 0u);
     }
     if (h < t) {
@@ -184,39 +227,10 @@ __device__ __forceinline__ uint32_t service_completions(const PagedParams &p) {
   }
   n = first_lane_value(n);
   if (n == 0) return 0;
-  h = ((unsigned long long)first_lane_value((uint32_t)(h >> 32)) << 32) | first_lane_value((uint32_t)h);
-  // completion i in lane i (completions are published before the tail)
-  unsigned long long e = 0;
-  if ((uint32_t)l < n)
-    e = __hip_atomic_load(&p.cq[(h + l) & p.cq_mask], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  // a malformed completion is never copied: its waiter times out instead of
-  // the copy leaving the backing store or the cache
-  {
-    const uint32_t pg = (uint32_t)(e >> 32) - 1u, sl = (uint32_t)e;
-    const bool bad = (uint32_t)l < n && (pg >= p.num_pages || sl >= p.cache.slots);
-    const uint64_t mbad = ballot(bad);
-    if (mbad) {
-      if (l == 0) atomicAdd(&p.stats[9], (unsigned long long)__popcll(mbad));
-      n = min(n, (uint32_t)__builtin_ctzll(mbad));  // the well-formed prefix only
-      if (n == 0) return 0;
-    }
-  }
-  const __amdgpu_buffer_rsrc_t crs = cache_rsrc(p.cache);
-  if (p.cache.page_bytes == 4096) {
-    copy_pages4(p.backing, crs, e, 0, n);  // n <= kFillBatch = 4
-  } else {
-    const uint32_t chunks = (uint32_t)(p.cache.page_bytes / 16);
-    for (uint32_t i = 0; i < n; ++i) {
-      const uint64_t ei = readlane64(e, i);
-      const uint4 *src = reinterpret_cast<const uint4 *>(p.backing + (uint64_t)((uint32_t)(ei >> 32) - 1u) *
-                                                                         p.cache.page_bytes);
-      const uint32_t base = (uint32_t)ei * (uint32_t)p.cache.page_bytes;
-      for (uint32_t c = l; c < chunks; c += kWave) coherent_store_u128(crs, base + c * 16u, src[c]);
-    }
-  }
-  // page bytes performed device-wide before any READY state
-  wait_stores_performed();
-  if ((uint32_t)l < n) atomicAdd(&p.cache.slot_word[(uint32_t)e], (1ull << kStateShift) | kRefBit);
+  h = readlane64(h, 0);
+  unsigned long long e;
+  n = load_completions(p, p.cq, h, n, e);  // a malformed entry stays claimed but unfilled
+  fill_entries(p, e, n);
   return n;
 }
 
@@ -525,32 +539,47 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
   return false;
 }
 
-// A fill wave: claims completions and copies pages until every query is done.
-// The first fill wave also refreshes the host mirrors on every pass.
-__device__ void fill_loop(const PagedParams &p, bool poller) {
-  unsigned long long served = 0;
+// Fill wave k: consumes completion ring k (its own: no atomics on the ring)
+// and copies the pages until every query is done.  Wave 0 also mirrors the
+// host abort flag.
+__device__ void fill_loop(const PagedParams &p, uint32_t k) {
+  const int l = lane_id();
+  const unsigned long long *ring = p.cq + (uint64_t)k * (p.cq_mask + 1);
+  const unsigned long long *tail = p.cq_tail + (uint64_t)k * p.tail_stride;
+  unsigned long long head = 0, served = 0;
   uint32_t idle = 0;
   for (;;) {
-    if (poller && lane_id() == 0) refresh_mirrors(p);
+    if (k == 0 && l == 0) refresh_abort(p);
     if (aborted(p)) break;
     if (__hip_atomic_load(p.done_queries, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.nq) break;
-    const uint32_t n = service_completions(p);
-    served += n;
-    if (n == 0) {
-      if (!poller && ++idle > 8) __builtin_amdgcn_s_sleep(8);
-    } else {
-      idle = 0;
+    unsigned long long t = 0;
+    if (l == 0) t = __hip_atomic_load(tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    t = readlane64(t, 0);
+    if (t <= head) {
+      if (++idle > 8) __builtin_amdgcn_s_sleep(2);
+      continue;
+    }
+    idle = 0;
+    while (head < t) {
+      const uint32_t n = (uint32_t)min((unsigned long long)kWave, t - head);
+      unsigned long long e;
+      const uint32_t good = load_completions(p, ring, head, n, e);
+      fill_entries(p, e, good);
+      served += good;
+      head += good < n ? good + 1 : n;  // step over a malformed entry
     }
   }
-  if (lane_id() == 0) atomicAdd(&p.stats[6], served);
+  if (l == 0) atomicAdd(&p.stats[6], served);
 }
 
 template <int KPL, int VDW, bool EXACT, bool N2S>
 __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
-  if (blockIdx.x >= p.query_waves) {
-    fill_loop(p, blockIdx.x == p.query_waves);
+  // fill waves take the lowest block indices, so they are dispatched first
+  if (blockIdx.x < p.fill_waves) {
+    fill_loop(p, blockIdx.x);
     return;
   }
+  const uint32_t qb = blockIdx.x - p.fill_waves;
   extern __shared__ __align__(16) unsigned char lds[];
   QSlot<KPL> *slots = reinterpret_cast<QSlot<KPL> *>(lds);
   const int l = lane_id();
@@ -569,7 +598,7 @@ __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
     bool any_active = false, progressed = false;
     for (uint32_t j = 0; j < p.oversub; ++j) {
       QSlot<KPL> &S = slots[j];
-      uint32_t *ht = p.ht_pool + ((uint64_t)(blockIdx.x * p.oversub + j) << kPagedHtLog2);  // query waves only
+      uint32_t *ht = p.ht_pool + ((uint64_t)(qb * p.oversub + j) << kPagedHtLog2);
       if (!S.active) {
         if (!admitting) continue;
         uint32_t qi = 0;
@@ -624,7 +653,7 @@ __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
       __syncthreads();
     }
     if (!any_active && !admitting) break;
-    const uint32_t served = service_completions(p);
+    const uint32_t served = p.fill_waves ? 0u : service_completions(p);
     ctr.served += served;
     if (!progressed && served == 0) {
       if (++idle > 4) __builtin_amdgcn_s_sleep(2);

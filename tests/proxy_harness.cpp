@@ -39,8 +39,8 @@ int main(int argc, char **argv) {
   std::vector<unsigned long long> cq_tail((size_t)rings * tail_stride, 0);
 
   gorio::Proxy proxy;
-  proxy.start(mq.data(), ring - 1, cq.data(), ring - 1, cq_tail.data(), rings, tail_stride);
-  proxy.begin(latency_us, cap);
+  proxy.start(mq.data(), ring - 1, cq.data(), ring - 1, cq_tail.data(), tail_stride);
+  proxy.begin(latency_us, cap, rings);
 
   // slot s is "LOADING" while in flight; a producer may only use a free slot,
   // as the GPU may only publish a descriptor for a slot it claimed
