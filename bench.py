@@ -29,7 +29,7 @@ sys.path.insert(0, str(ROOT))
 METRIC = "queries/sec at k=10 (oracle-exact) + achieved HBM GB/s and miss-service GB/s"
 HBM_PEAK_GBS = 8000.0
 PROFILES = ROOT / "profiles"
-KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp",
+KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp", "paper_2607_04415_amd/csrc/frontier.hpp",
                   "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
 
 
