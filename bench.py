@@ -102,7 +102,8 @@ def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: boo
     ix.set_backing(latency_us=w.latency_us, oversub=1 if blocking else w.oversub, blocking=blocking)
     qd = torch.from_numpy(q).cuda()
     ids = torch.empty((len(q), w.k), dtype=torch.int32, device="cuda")
-    dists = torch.empty((len(q), w.k), dtype=torch.int32, device="cuda")
+    dists = torch.empty((len(q), w.k), dtype=torch.int32 if q.dtype == np.uint8 else torch.float32,
+                        device="cuda")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     st = ix.search_into(qd, len(q), w.k, w.L, w.W, ids, dists,
@@ -119,7 +120,7 @@ def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: boo
            "pages_served": st["pages_served"],
            "miss_service_gbs": round(st["bytes_served"] / (ms * 1e-3) / 1e9, 2),
            "parks": st["parks"], "resumes": st["resumes"],
-           "vs_resident_qps": round(len(q) / wall / resident_qps, 5)}
+           "vs_resident_qps": round(len(q) / wall / resident_qps, 5) if resident_qps else None}
     ix.close()
     return out, ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), q
 
@@ -136,6 +137,9 @@ def main():
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
     ap.add_argument("--paged-sample", type=int, default=2000,
                     help="queries of each paged configuration to run (0 = skip the paged legs)")
+    ap.add_argument("--f32-sample", type=int, default=0,
+                    help="queries of the 10M x 96-d float32 paged configuration to run (0 = skip; "
+                         "generating that index takes minutes the first time)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
@@ -233,6 +237,28 @@ def main():
         miss_gbs = legs[0]["miss_service_gbs"]
         paged = {"host_link_peak_gbs": round(link, 1), "legs": legs,
                  "split_phase_vs_blocking": round(legs[0]["qps"] / max(1e-9, legs[1]["qps"]), 3)}
+
+    if args.f32_sample > 0:
+        wf = WORKLOADS["f32-10m-cache5-lat20"]
+        log(f"[bench] {wf.name}: loading or generating the index")
+        af = index_arrays(wf.index)
+        qf = query_array(wf.index, wf.queries)[:args.f32_sample]
+        # the same queries on the HBM-resident index: the reference answers and rate
+        ixr = g.Index(af["x"], af["graph"])
+        ri, rd, rst = ixr.search(torch.from_numpy(qf).cuda(), wf.k, wf.L, wf.W)
+        torch.cuda.synchronize()
+        ri, rd = ri.cpu().numpy().view(np.uint32), rd.cpu().numpy()
+        rqps = len(qf) / (rst["kernel_ms"] * 1e-3)
+        ixr.close()
+        leg, pi, pd, _ = paged_leg(torch, g, af, wf, args.f32_sample, rqps)
+        leg["resident_kernel_qps"] = round(rqps, 1)
+        leg["equals_resident"] = bool(np.array_equal(pi, ri) and np.array_equal(pd.view(np.uint32), rd.view(np.uint32)))
+        log(f"[bench] paged {wf.name}: {leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, "
+            f"miss service {leg['miss_service_gbs']} GB/s (resident {rqps:,.0f} q/s)")
+        if paged is None:
+            paged = {"host_link_peak_gbs": round(host_link_peak_gbs(torch), 1), "legs": []}
+        paged["legs"].append(leg)
+        del af
 
     out = {
         "metric": METRIC, "value": round(qps, 1), "unit": "queries/s", "n_gpus": 1,

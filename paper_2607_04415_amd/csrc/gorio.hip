@@ -12,8 +12,7 @@
 #include "../../include/gorio.h"
 #include "build_kernels.hpp"
 #include "index.hpp"
-#include "search_paged.hpp"
-#include "search_resident.hpp"
+#include "launch.hpp"
 
 using namespace gorio;
 
@@ -316,73 +315,12 @@ extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, ui
 // ---------------------------------------------------------------------------
 namespace {
 
-template <int KPL, int VDW, bool EXACT, bool N2S>
-gorio_status launch_resident_ht(int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
-  switch (ht_log2) {
-    case 13: search_resident_u8<KPL, VDW, EXACT, 13, N2S><<<grid, kWave, 0, s>>>(p); break;
-    default: return fail(GORIO_EUNSUPPORTED, "visited table 2^%d not built", ht_log2);
-  }
-  return GORIO_OK;
-}
 
-template <int KPL, int VDW, bool EXACT>
-gorio_status launch_resident_n2s(int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
-  if (p.geom.node_to_slot) return launch_resident_ht<KPL, VDW, EXACT, true>(ht_log2, p, grid, s);
-  return launch_resident_ht<KPL, VDW, EXACT, false>(ht_log2, p, grid, s);
-}
-
-// uint8 rows: 128-d gets the exact 16-B-per-lane kernel; others the generic one
-// with 1, 4 or 16 dwords per lane.
-template <int KPL>
-gorio_status launch_resident_vdw(uint32_t D, int ht_log2, const ResidentParams &p, int grid, hipStream_t s) {
-  if (D == 128) return launch_resident_n2s<KPL, 4, true>(ht_log2, p, grid, s);
-  const uint32_t vdw = (D / 4 + 7) / 8;
-  if (vdw <= 1) return launch_resident_n2s<KPL, 1, false>(ht_log2, p, grid, s);
-  if (vdw <= 4) return launch_resident_n2s<KPL, 4, false>(ht_log2, p, grid, s);
-  return launch_resident_n2s<KPL, 16, false>(ht_log2, p, grid, s);
-}
-
-gorio_status launch_resident(const ResidentParams &p, int ht_log2, int grid, hipStream_t s) {
-  if (p.L <= 64) return launch_resident_vdw<1>(p.D, ht_log2, p, grid, s);
-  if (p.L <= 128) return launch_resident_vdw<2>(p.D, ht_log2, p, grid, s);
-  return launch_resident_vdw<4>(p.D, ht_log2, p, grid, s);
-}
 
 
 }  // namespace
 
 namespace {
-
-template <int KPL, int VDW, bool EXACT, bool N2S>
-hipError_t launch_paged_t(const PagedParams &pp, int grid, size_t lds, hipStream_t s) {
-  auto k = search_paged_u8<KPL, VDW, EXACT, N2S>;
-  if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  k<<<grid, kWave, lds, s>>>(pp);
-  return hipGetLastError();
-}
-
-template <int KPL>
-size_t qslot_bytes() { return sizeof(QSlot<KPL>); }
-
-template <int KPL, int VDW, bool EXACT>
-hipError_t launch_paged_n2s(const PagedParams &pp, int grid, size_t lds, hipStream_t s) {
-  if (pp.geom.node_to_slot) return launch_paged_t<KPL, VDW, EXACT, true>(pp, grid, lds, s);
-  return launch_paged_t<KPL, VDW, EXACT, false>(pp, grid, lds, s);
-}
-
-template <int KPL>
-hipError_t launch_paged_kpl(const PagedParams &pp, int grid, hipStream_t s) {
-  const size_t lds = pp.oversub * qslot_bytes<KPL>();
-  if (pp.D == 128) return launch_paged_n2s<KPL, 4, true>(pp, grid, lds, s);
-  const uint32_t vdw = (pp.D / 4 + 7) / 8;
-  if (vdw <= 1) return launch_paged_n2s<KPL, 1, false>(pp, grid, lds, s);
-  if (vdw <= 4) return launch_paged_n2s<KPL, 4, false>(pp, grid, lds, s);
-  return launch_paged_n2s<KPL, 16, false>(pp, grid, lds, s);
-}
 
 // Paged search: reset the per-search rings and counters, arm the proxy,
 // launch the persistent kernel and wait for it under a watchdog.
@@ -467,10 +405,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
 
   P.proxy.begin(ix->latency_us, ix->max_outstanding, rings);
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
-  hipError_t le;
-  if (rp.L <= 64) le = launch_paged_kpl<1>(pp, grid, s);
-  else if (rp.L <= 128) le = launch_paged_kpl<2>(pp, grid, s);
-  else le = launch_paged_kpl<4>(pp, grid, s);
+  const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, grid, s) : launch_paged_u8(pp, grid, s);
   if (le != hipSuccess) {
     P.proxy.end();
     return fail(GORIO_EDEVICE, "paged search launch failed: %s", hipGetErrorString(le));
@@ -514,7 +449,6 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   if (stats) memset(stats, 0, sizeof *stats);
   if (nq == 0) return GORIO_OK;
   if (!queries || !ids || !dists) return fail(GORIO_EINVAL, "queries, ids and dists must be non-NULL");
-  if (ix->dtype != GORIO_U8) return fail(GORIO_EUNSUPPORTED, "float32 search is not built yet");
   if (!ix->resident && W > (uint32_t)kPagedMaxW)
     return fail(GORIO_EUNSUPPORTED, "paged search supports W <= %d (W=%u)", kPagedMaxW, W);
 
@@ -528,13 +462,13 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   const bool i_dev = is_device_pointer(ids);
   const bool d_dev = is_device_pointer(dists);
   DevBuf qbuf, ibuf, dbuf;
-  const uint8_t *d_q = static_cast<const uint8_t *>(queries);
+  const void *d_q = queries;
   uint32_t *d_ids = ids;
   void *d_dists = dists;
   if (!q_dev) {
     HIP_OR_FAIL(qbuf.alloc(qbytes));
     HIP_OR_FAIL(hipMemcpyAsync(qbuf.p, queries, qbytes, hipMemcpyHostToDevice, s));
-    d_q = qbuf.as<uint8_t>();
+    d_q = qbuf.p;
   }
   if (!i_dev) { HIP_OR_FAIL(ibuf.alloc(obytes)); d_ids = ibuf.as<uint32_t>(); }
   if (!d_dev) { HIP_OR_FAIL(dbuf.alloc(obytes)); d_dists = dbuf.p; }
@@ -555,18 +489,15 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   p.L = L;
   p.W = W;
   p.out_ids = d_ids;
-  p.out_dists = static_cast<int32_t *>(d_dists);
+  p.out_dists = static_cast<uint32_t *>(d_dists);
   p.stats = ix->d_stats;
 
   gorio_status st;
   bool timed_out = false;
   if (ix->resident) {
-    const int ht_log2 = env_int("GORIO_HT_LOG2", 13);
     const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
     HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
-    st = launch_resident(p, ht_log2, grid, s);
-    if (st != GORIO_OK) return st;
-    HIP_OR_FAIL(hipGetLastError());
+    HIP_OR_FAIL(ix->dtype == GORIO_F32 ? launch_resident_f32(p, grid, s) : launch_resident_u8(p, grid, s));
     HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
   } else {
     st = run_paged(ix, p, s, timed_out);

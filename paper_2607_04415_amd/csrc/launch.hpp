@@ -1,0 +1,63 @@
+// Kernel launchers.  Each dtype's kernel variants are instantiated in a
+// translation unit of their own (resident_u8.hip, resident_f32.hip,
+// paged_u8.hip, paged_f32.hip) so that they compile in parallel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "search_paged.hpp"
+#include "search_resident.hpp"
+
+namespace gorio {
+
+// Resident search, one workgroup per query (grid <= nq, queries strided).
+hipError_t launch_resident_u8(const ResidentParams &p, int grid, hipStream_t s);
+hipError_t launch_resident_f32(const ResidentParams &p, int grid, hipStream_t s);
+
+// Paged search: the persistent kernel (fill waves + query waves).
+hipError_t launch_paged_u8(const PagedParams &pp, int grid, hipStream_t s);
+hipError_t launch_paged_f32(const PagedParams &pp, int grid, hipStream_t s);
+
+// Visited-table size of the resident kernel (LDS entries = 2^kResidentHtLog2).
+constexpr int kResidentHtLog2 = 13;
+
+namespace detail {
+
+template <int KPL, class M, bool N2S>
+hipError_t resident_t(const ResidentParams &p, int grid, hipStream_t s) {
+  search_resident<KPL, M, kResidentHtLog2, N2S><<<grid, kWave, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+// frontier slots per lane (L <= 64 KPL) and node_to_slot presence
+template <class M>
+hipError_t resident(const ResidentParams &p, int grid, hipStream_t s) {
+  const bool n2s = p.geom.node_to_slot != nullptr;
+  if (p.L <= 64) return n2s ? resident_t<1, M, true>(p, grid, s) : resident_t<1, M, false>(p, grid, s);
+  if (p.L <= 128) return n2s ? resident_t<2, M, true>(p, grid, s) : resident_t<2, M, false>(p, grid, s);
+  return n2s ? resident_t<4, M, true>(p, grid, s) : resident_t<4, M, false>(p, grid, s);
+}
+
+template <int KPL, class M, bool N2S>
+hipError_t paged_t(const PagedParams &pp, int grid, hipStream_t s) {
+  const size_t lds = pp.oversub * sizeof(QSlot<KPL>);
+  auto k = search_paged<KPL, M, N2S>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  k<<<grid, kWave, lds, s>>>(pp);
+  return hipGetLastError();
+}
+
+template <class M>
+hipError_t paged(const PagedParams &pp, int grid, hipStream_t s) {
+  const bool n2s = pp.geom.node_to_slot != nullptr;
+  if (pp.L <= 64) return n2s ? paged_t<1, M, true>(pp, grid, s) : paged_t<1, M, false>(pp, grid, s);
+  if (pp.L <= 128) return n2s ? paged_t<2, M, true>(pp, grid, s) : paged_t<2, M, false>(pp, grid, s);
+  return n2s ? paged_t<4, M, true>(pp, grid, s) : paged_t<4, M, false>(pp, grid, s);
+}
+
+}  // namespace detail
+}  // namespace gorio

@@ -1,0 +1,259 @@
+// Distance policies of the search kernels (squared L2, returned squared).
+//
+// A policy loads the query, evaluates the entry node, and turns a batch of
+// candidate records into 64-bit frontier keys (distance bits << 32 |
+// id << 1).  The kernels' traversal, filtering and merging do not depend on
+// the element type: uint8 distances are non-negative int32 values and float32
+// distances are >= +0, so both order correctly as unsigned 32-bit patterns.
+//
+//   MetricU8  - exact int32 distance: q.q + sum (x.x - 2 q.x) with
+//               v_dot4_u32_u8 on coalesced reads, 8 lanes per vector.
+//   MetricF32 - one lane per candidate; t = q_d - x_d, acc = acc + t*t for
+//               d = 0 .. D-1 in order, every operation rounded to nearest
+//               even with no fused multiply-add, so the result is the same
+//               float as a plain sequential loop.
+#pragma once
+
+#include "frontier.hpp"
+#include "page_cache.hpp"
+
+namespace gorio {
+
+// ---------------------------------------------------------------------------
+// uint8
+// ---------------------------------------------------------------------------
+template <int VDW, bool EXACT>
+struct MetricU8 {
+  // vectors in flight per resident gather batch: 256 for up to 16 B per lane,
+  // fewer for wider rows
+  static constexpr int kRounds = VDW <= 4 ? 32 : 128 / VDW;
+  static constexpr int kBatch = kRounds * 8;
+  static constexpr int kChunks = kBatch / kWave;
+  static constexpr int kQueryWords = 1;          // the query lives in registers
+  static constexpr uint32_t kPadDist = 0x7FFFFFFFu;  // INT32_MAX
+
+  U8Vec<VDW, EXACT> q;
+  int qq;
+  uint32_t dwords;
+
+  __device__ __forceinline__ void load_query(const void *queries, uint32_t qi, uint32_t D, uint32_t *) {
+    const int gl = lane_id() & 7;
+    dwords = D >> 2;
+    q.load(static_cast<const uint8_t *>(queries) + (uint64_t)qi * D, gl, dwords);
+    int s = 0;
+#pragma unroll
+    for (int t = 0; t < VDW; ++t) s += (int)__builtin_amdgcn_udot4(q.w[t], q.w[t], 0u, false);
+    qq = sum8(s);
+  }
+
+  // Distance bits of one record, computed by the whole wave (uniform result).
+  __device__ __forceinline__ uint32_t dist_one(const uint8_t *rec) const {
+    U8Vec<VDW, EXACT> x;
+    x.load(rec, lane_id() & 7, dwords);
+    return (uint32_t)(sum8(partial_u8(q, x)) + qq);
+  }
+
+  // Keys of candidates c0 .. c0 + kBatch - 1 of cand (kInfKey past cnt);
+  // rec_of(node) is the node's record address.  One round trip for the batch.
+  template <class RecOf>
+  __device__ __forceinline__ void resident_keys(RecOf rec_of, const uint32_t *cand, uint32_t c0, uint32_t cnt,
+                                                uint32_t fallback, uint64_t (&key)[kChunks]) const {
+    const int l = lane_id();
+    const int g = l >> 3;
+    const int gl = l & 7;
+    // candidate node -> record; lanes past the count read the fallback record
+    const uint8_t *rec[kRounds];
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) {
+      if (c0 + rr * 8 >= cnt) break;
+      const uint32_t idx = c0 + rr * 8 + g;
+      rec[rr] = rec_of(idx < cnt ? cand[idx] : fallback);
+    }
+    U8Vec<VDW, EXACT> x[kRounds];
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) {
+      if (c0 + rr * 8 >= cnt) break;
+      x[rr].load(rec[rr], gl, dwords);
+    }
+    int dist[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) dist[c] = 0;
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) {
+      if (c0 + rr * 8 >= cnt) break;
+      const int d = sum8(partial_u8(q, x[rr])) + qq;
+      if (gl == (rr & 7)) dist[rr / 8] = d;
+    }
+    // lane l of chunk c holds candidate c0 + 64c + 8*(l%8) + l/8
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const uint32_t my_idx = c0 + c * kWave + gl * 8 + g;
+      key[c] = my_idx < cnt ? (((uint64_t)(uint32_t)dist[c] << 32) | ((uint64_t)cand[my_idx] << 1)) : kInfKey;
+    }
+  }
+
+  // Paged: keys of the candidates whose pages are ready (rdy, slot per lane;
+  // candidate index = base + lane).  off_of(slot, node) is the record's byte
+  // offset in the cache.  The ready lanes are compacted and evaluated 8 per
+  // round; the key of the i-th ready candidate ends up in some lane, the others
+  // hold kInfKey.
+  template <class OffOf>
+  __device__ __forceinline__ uint64_t paged_keys(OffOf off_of, __amdgpu_buffer_rsrc_t crs, const uint32_t *cand,
+                                                 uint32_t base, bool rdy, uint32_t slot, uint64_t mr) const {
+    const int l = lane_id();
+    const int g = l >> 3;
+    const int gl = l & 7;
+    const uint32_t cnt = (uint32_t)__popcll(mr);
+    __shared__ uint32_t rc[kWave], rs[kWave];
+    if (rdy) {
+      const uint32_t my_rank = lanes_below(mr);
+      rc[my_rank] = base + l;
+      rs[my_rank] = slot;
+    }
+    __syncthreads();
+    U8Vec<VDW, EXACT> x[8];
+#pragma unroll
+    for (int rr = 0; rr < 8; ++rr) {
+      const uint32_t idx = rr * 8 + g;
+      const uint32_t ci = idx < cnt ? rc[idx] : rc[0];
+      const uint32_t si = idx < cnt ? rs[idx] : rs[0];
+      load_cached_u8(x[rr], crs, off_of(si, cand[ci]), gl);
+    }
+    int mine_d = 0;
+#pragma unroll
+    for (int rr = 0; rr < 8; ++rr) {
+      const int d = sum8(partial_u8(q, x[rr])) + qq;
+      if (gl == rr) mine_d = d;
+    }
+    const uint32_t my_idx = gl * 8 + g;
+    uint64_t key = kInfKey;
+    if (my_idx < cnt) key = ((uint64_t)(uint32_t)mine_d << 32) | ((uint64_t)cand[rc[my_idx]] << 1);
+    __syncthreads();
+    return key;
+  }
+
+ private:
+  // coherent read of a cached vector (see page_cache.hpp)
+  __device__ __forceinline__ void load_cached_u8(U8Vec<VDW, EXACT> &x, __amdgpu_buffer_rsrc_t r, uint32_t rec,
+                                                 int gl) const {
+    const uint32_t b = rec + (uint32_t)gl * VDW * 4u;
+    if constexpr (EXACT && VDW % 4 == 0) {
+#pragma unroll
+      for (int t = 0; t < VDW; t += 4) {
+        const uint4 u = coherent_load_u128(r, b + t * 4u);
+        x.w[t] = u.x; x.w[t + 1] = u.y; x.w[t + 2] = u.z; x.w[t + 3] = u.w;
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < VDW; ++t)
+        x.w[t] = (EXACT || (uint32_t)(gl * VDW + t) < dwords) ? coherent_load_u32(r, b + t * 4u) : 0u;
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// float32
+// ---------------------------------------------------------------------------
+// NV4: the vector has at most 4 * NV4 floats.  EXACT: exactly 4 * NV4, read
+// with 16-B loads all at once; otherwise dword loads of d < D, 16 at a time.
+template <int NV4, bool EXACT>
+struct MetricF32 {
+  static constexpr int kBatch = kWave;  // one candidate per lane
+  static constexpr int kChunks = 1;
+  static constexpr int kQueryWords = 4 * NV4;
+  static constexpr uint32_t kPadDist = 0x7F800000u;  // +inf
+  static constexpr int kStep = 16;                   // dwords per round trip (generic path)
+
+  const float *qs;  // the query in LDS (wave-uniform reads)
+  uint32_t D;
+
+  // Copies the query into LDS; the caller synchronizes before use.
+  __device__ __forceinline__ void load_query(const void *queries, uint32_t qi, uint32_t D_, uint32_t *qlds) {
+    D = D_;
+    const uint32_t *src = static_cast<const uint32_t *>(queries) + (uint64_t)qi * D_;
+    for (uint32_t d = lane_id(); d < (uint32_t)kQueryWords; d += kWave) qlds[d] = d < D_ ? src[d] : 0u;
+    qs = reinterpret_cast<const float *>(qlds);
+  }
+
+  // acc + (q_d - x_d)^2 for one element, each step rounded on its own
+  __device__ __forceinline__ static float step(float acc, float qd, float xd) {
+    const float t = __fsub_rn(qd, xd);
+    return __fadd_rn(acc, __fmul_rn(t, t));
+  }
+
+  // Sequential distance of this lane's vector; ld4(i) returns bytes
+  // [16i, 16i + 16) of the vector, ld1(d) the d-th float's bits.
+  template <class Ld4, class Ld1>
+  __device__ __forceinline__ float dist_lane(Ld4 ld4, Ld1 ld1) const {
+    float acc = 0.0f;
+    if constexpr (EXACT) {
+      uint4 x[NV4];
+#pragma unroll
+      for (int i = 0; i < NV4; ++i) x[i] = ld4(i);
+#pragma unroll
+      for (int i = 0; i < NV4; ++i) {
+        const float4 qv = *reinterpret_cast<const float4 *>(qs + 4 * i);
+        acc = step(acc, qv.x, __uint_as_float(x[i].x));
+        acc = step(acc, qv.y, __uint_as_float(x[i].y));
+        acc = step(acc, qv.z, __uint_as_float(x[i].z));
+        acc = step(acc, qv.w, __uint_as_float(x[i].w));
+      }
+    } else {
+      for (uint32_t d0 = 0; d0 < D; d0 += kStep) {
+        uint32_t x[kStep];
+#pragma unroll
+        for (int j = 0; j < kStep; ++j) x[j] = d0 + j < D ? ld1(d0 + j) : 0u;
+#pragma unroll
+        for (int j = 0; j < kStep; ++j)
+          if (d0 + j < D) acc = step(acc, qs[d0 + j], __uint_as_float(x[j]));
+      }
+    }
+    return acc;
+  }
+
+  __device__ __forceinline__ float dist_global(const uint8_t *rec) const {
+    const uint32_t *w = reinterpret_cast<const uint32_t *>(rec);
+    return dist_lane(
+        [&](int i) {
+          uint4 u;
+          __builtin_memcpy(&u, __builtin_assume_aligned(w + 4 * i, 4), 16);
+          return u;
+        },
+        [&](uint32_t d) { return w[d]; });
+  }
+
+  __device__ __forceinline__ float dist_cached(__amdgpu_buffer_rsrc_t r, uint32_t off) const {
+    return dist_lane([&](int i) { return coherent_load_u128(r, off + 16u * (uint32_t)i); },
+                     [&](uint32_t d) { return coherent_load_u32(r, off + 4u * d); });
+  }
+
+  // Distance bits of one record (lane 0 computes, the result is broadcast).
+  __device__ __forceinline__ uint32_t dist_one(const uint8_t *rec) const {
+    uint32_t b = 0;
+    if (lane_id() == 0) b = __float_as_uint(dist_global(rec));
+    return first_lane_value(b);
+  }
+
+  template <class RecOf>
+  __device__ __forceinline__ void resident_keys(RecOf rec_of, const uint32_t *cand, uint32_t c0, uint32_t cnt,
+                                                uint32_t fallback, uint64_t (&key)[kChunks]) const {
+    const uint32_t idx = c0 + lane_id();
+    const uint32_t node = idx < cnt ? cand[idx] : fallback;
+    const float d = dist_global(rec_of(node));
+    key[0] = idx < cnt ? (((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)node << 1)) : kInfKey;
+  }
+
+  template <class OffOf>
+  __device__ __forceinline__ uint64_t paged_keys(OffOf off_of, __amdgpu_buffer_rsrc_t crs, const uint32_t *cand,
+                                                 uint32_t base, bool rdy, uint32_t slot, uint64_t) const {
+    uint64_t key = kInfKey;
+    if (rdy) {
+      const uint32_t node = cand[base + lane_id()];
+      const float d = dist_cached(crs, off_of(slot, node));
+      key = ((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)node << 1);
+    }
+    return key;
+  }
+};
+
+}  // namespace gorio

@@ -1,0 +1,11 @@
+// Paged search kernels for float32 rows (same variant choice as the resident ones).
+#include "launch.hpp"
+
+namespace gorio {
+
+hipError_t launch_paged_f32(const PagedParams &pp, int grid, hipStream_t s) {
+  if (pp.D == 96) return detail::paged<MetricF32<24, true>>(pp, grid, s);
+  return detail::paged<MetricF32<64, false>>(pp, grid, s);
+}
+
+}  // namespace gorio

@@ -1,0 +1,14 @@
+// Paged search kernels for uint8 rows (same variant choice as the resident ones).
+#include "launch.hpp"
+
+namespace gorio {
+
+hipError_t launch_paged_u8(const PagedParams &pp, int grid, hipStream_t s) {
+  if (pp.D == 128) return detail::paged<MetricU8<4, true>>(pp, grid, s);
+  const uint32_t vdw = (pp.D / 4 + 7) / 8;
+  if (vdw <= 1) return detail::paged<MetricU8<1, false>>(pp, grid, s);
+  if (vdw <= 4) return detail::paged<MetricU8<4, false>>(pp, grid, s);
+  return detail::paged<MetricU8<16, false>>(pp, grid, s);
+}
+
+}  // namespace gorio

@@ -23,8 +23,7 @@
 // paper compares against).
 #pragma once
 
-#include "frontier.hpp"
-#include "page_cache.hpp"
+#include "metric.hpp"
 
 namespace gorio {
 
@@ -55,12 +54,12 @@ struct PagedParams {
   unsigned int *poll_lock;                // shared ring: try-lock for the one host read of the tail
   const unsigned int *abort_flag;         // host memory; nonzero ends the search
   unsigned int *abort_seen;               // device mirror of abort_flag
-  const uint8_t *queries;
+  const void *queries;                    // nq x D elements
   uint32_t nq, k, L, W;
   unsigned int *next_query;
   unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
   uint32_t *out_ids;
-  int32_t *out_dists;
+  uint32_t *out_dists;                    // distance bits (int32 or float32)
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
   uint32_t oversub, max_pending;
   int blocking;
@@ -92,24 +91,6 @@ __device__ __forceinline__ uint32_t cached_record(const PagedParams &p, uint32_t
   const uint32_t sl = slot_ct<N2S>(p.geom, v);
   const uint32_t within = sl - fastdiv(sl, p.geom.rpp) * p.geom.rpp.d;
   return s * (uint32_t)p.cache.page_bytes + within * p.geom.record_bytes;
-}
-
-// The query-side vector read of a cached record (coherent, see page_cache.hpp).
-template <int VDW, bool EXACT>
-__device__ __forceinline__ void load_cached_vec(U8Vec<VDW, EXACT> &x, __amdgpu_buffer_rsrc_t r, uint32_t rec,
-                                                int gl, uint32_t dwords) {
-  const uint32_t base = rec + (uint32_t)gl * VDW * 4u;
-  if constexpr (EXACT && VDW % 4 == 0) {
-#pragma unroll
-    for (int t = 0; t < VDW; t += 4) {
-      const uint4 u = coherent_load_u128(r, base + t * 4u);
-      x.w[t] = u.x; x.w[t + 1] = u.y; x.w[t + 2] = u.z; x.w[t + 3] = u.w;
-    }
-  } else {
-#pragma unroll
-    for (int t = 0; t < VDW; ++t)
-      x.w[t] = (EXACT || (uint32_t)(gl * VDW + t) < dwords) ? coherent_load_u32(r, base + t * 4u) : 0u;
-  }
 }
 
 template <bool N2S>
@@ -282,23 +263,17 @@ __device__ __forceinline__ bool query_runnable(const PagedParams &p, const QSlot
 }
 
 // Runs one query until it finishes (returns true) or parks (false).
-template <int KPL, int VDW, bool EXACT, bool N2S>
-__device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, PagedCounters &ctr) {
+template <int KPL, class M, bool N2S>
+__device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uint32_t *qbuf, PagedCounters &ctr) {
   using HT = VisitedHbm<kPagedHtLog2>;
   const int l = lane_id();
-  const int g = l >> 3;
-  const int gl = l & 7;
-  const uint32_t dwords = p.D >> 2;
   const uint32_t GB = min(kCandCap / p.R, (uint32_t)kPagedMaxW);
   constexpr int kIdsPerLane = kCandCap / kWave;
   const __amdgpu_buffer_rsrc_t crs = cache_rsrc(p.cache);
 
-  U8Vec<VDW, EXACT> q;
-  q.load(p.queries + (uint64_t)S.qi * p.D, gl, dwords);
-  int qq = 0;
-#pragma unroll
-  for (int t = 0; t < VDW; ++t) qq += (int)__builtin_amdgcn_udot4(q.w[t], q.w[t], 0u, false);
-  qq = sum8(qq);
+  M m;
+  m.load_query(p.queries, S.qi, p.D, qbuf);
+  __syncthreads();
   uint64_t F[KPL];
   load_frontier(S, F);
 
@@ -326,7 +301,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
           if (e < p.k) {
             const bool ok = F[r] != kInfKey;
             p.out_ids[(uint64_t)S.qi * p.k + e] = ok ? key_id(F[r]) : kNoEdge;
-            p.out_dists[(uint64_t)S.qi * p.k + e] = ok ? (int32_t)(F[r] >> 32) : INT32_MAX;
+            p.out_dists[(uint64_t)S.qi * p.k + e] = ok ? (uint32_t)(F[r] >> 32) : M::kPadDist;
           }
         }
         return true;
@@ -460,33 +435,9 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, Pag
         for (int t = 0; t < kIdsPerLane; ++t) {
           const uint64_t mr = ballot(rdy[t]);
           if (mr == 0) continue;
-          // candidate of lane src: t*64 + src; evaluate in 8 rounds of 8 vectors
           const uint32_t cnt = (uint32_t)__popcll(mr);
-          // compact ready lanes: the i-th ready lane's candidate index and slot
-          const uint32_t my_rank = lanes_below(mr);
-          __shared__ uint32_t rc[kWave], rs[kWave];
-          if (rdy[t]) {
-            rc[my_rank] = t * kWave + l;
-            rs[my_rank] = rslot[t];
-          }
-          __syncthreads();
-          U8Vec<VDW, EXACT> x[8];
-#pragma unroll
-          for (int rr = 0; rr < 8; ++rr) {
-            const uint32_t idx = rr * 8 + g;
-            const uint32_t ci = idx < cnt ? rc[idx] : rc[0];
-            const uint32_t si = idx < cnt ? rs[idx] : rs[0];
-            load_cached_vec(x[rr], crs, cached_record<N2S>(p, si, S.cand[ci]), gl, dwords);
-          }
-          int mine_d = 0;
-#pragma unroll
-          for (int rr = 0; rr < 8; ++rr) {
-            const int d = sum8(partial_u8(q, x[rr])) + qq;
-            if (gl == rr) mine_d = d;
-          }
-          const uint32_t my_idx = gl * 8 + g;
-          uint64_t key = kInfKey;
-          if (my_idx < cnt) key = ((uint64_t)(uint32_t)mine_d << 32) | ((uint64_t)S.cand[rc[my_idx]] << 1);
+          uint64_t key = m.paged_keys([&](uint32_t si, uint32_t v) { return cached_record<N2S>(p, si, v); }, crs,
+                                      S.cand, t * kWave, rdy[t], rslot[t], mr);
           ctr.eval += cnt;
           const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
           const bool pass = key < thr;
@@ -572,8 +523,8 @@ __device__ void fill_loop(const PagedParams &p, uint32_t k) {
   if (l == 0) atomicAdd(&p.stats[6], served);
 }
 
-template <int KPL, int VDW, bool EXACT, bool N2S>
-__global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
+template <int KPL, class M, bool N2S>
+__global__ __launch_bounds__(kWave) void search_paged(PagedParams p) {
   // fill waves take the lowest block indices, so they are dispatched first
   if (blockIdx.x < p.fill_waves) {
     fill_loop(p, blockIdx.x);
@@ -581,6 +532,7 @@ __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
   }
   const uint32_t qb = blockIdx.x - p.fill_waves;
   extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
   QSlot<KPL> *slots = reinterpret_cast<QSlot<KPL> *>(lds);
   const int l = lane_id();
   for (uint32_t j = 0; j < p.oversub; ++j) {
@@ -638,7 +590,7 @@ __global__ __launch_bounds__(kWave) void search_paged_u8(PagedParams p) {
         ++ctr.resume;
       }
       any_active = true;
-      const bool done = run_query<KPL, VDW, EXACT, N2S>(p, S, ht, ctr);
+      const bool done = run_query<KPL, M, N2S>(p, S, ht, qbuf, ctr);
       progressed = true;
       if (l == 0) {
         if (done) {

@@ -1,8 +1,8 @@
-// HBM-resident beam search for uint8 vectors: one wavefront per query.
+// HBM-resident beam search: one wavefront per query.
 //
 // Per query the wave keeps the frontier F (the L best keys of the evaluated
 // set, ascending) in registers, 64 * KPL slots, slot e = r * 64 + lane, and its
-// visited filter in LDS.  Key = (squared distance << 32) | (node id << 1) |
+// visited filter in LDS.  Key = (distance bits << 32) | (node id << 1) |
 // expanded bit: ties order by id, and the flag rides along through the
 // sorting networks.  One iteration (GORIO Sec. 1 / Sec. 2.2: expand nodes,
 // compute distances, update the frontier):
@@ -11,15 +11,16 @@
 //             node of a beam group (up to 256 ids, 4 per lane);
 //   filter  - ids already in the visited filter are dropped (LDS atomics),
 //             the rest compacted into an LDS candidate list;
-//   evaluate- one round trip gathers up to 256 vectors: 8 lanes per 128-B
-//             vector, 16 B per lane, v_dot4_u32_u8 on the coalesced reads,
-//             sum (q - x)^2 = q.q + sum (x.x - 2 q.x) exact in int32;
+//   evaluate- one round trip gathers a batch of candidate vectors; the
+//             distance policy (metric.hpp) turns them into keys: uint8 with
+//             8 lanes per 128-B vector and v_dot4_u32_u8, float32 with one
+//             lane per vector and the sequential rounded sum;
 //   merge   - only keys below F's L-th key can enter: a few are inserted by
 //             rank (ballot + DPP shift), many are bitonic-sorted per 64-lane
 //             chunk and bitonic-merged into F.
 #pragma once
 
-#include "frontier.hpp"
+#include "metric.hpp"
 
 namespace gorio {
 
@@ -27,47 +28,40 @@ struct ResidentParams {
   const uint8_t *pages;    // num_pages * page_bytes, HBM
   PageGeom geom;
   uint32_t n;
-  uint32_t D;              // uint8 dimensions (multiple of 4)
+  uint32_t D;              // vector elements (uint8: a multiple of 4)
   uint32_t R;              // id slots per record
   FastDiv Rdiv;            // division by R
   uint32_t entry;
-  const uint8_t *queries;  // nq x D
+  const void *queries;     // nq x D elements
   uint32_t nq;
   uint32_t k, L, W;
   uint32_t *out_ids;       // nq x k
-  int32_t *out_dists;      // nq x k
+  uint32_t *out_dists;     // nq x k distance bits (int32 or float32)
   unsigned long long *stats;  // [evaluations, reevaluations, expansions, iterations]
 };
 
-template <int KPL, int VDW, bool EXACT, int HT_LOG2, bool N2S>
-__global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
+template <int KPL, class M, int HT_LOG2, bool N2S>
+__global__ __launch_bounds__(kWave) void search_resident(ResidentParams p) {
   using HT = VisitedLds<HT_LOG2>;
-  // vectors in flight per gather batch: 256 for up to 16 B per lane, fewer for wider rows
-  constexpr int kRounds = VDW <= 4 ? 32 : 128 / VDW;
-  constexpr int kBatch = kRounds * 8;
-  constexpr int kChunks = kBatch / kWave;
+  constexpr int kChunks = M::kChunks;
+  constexpr int kBatch = M::kBatch;
   constexpr int kIdsPerLane = kCandCap / kWave;
 
   __shared__ uint32_t ht[HT::kSize];
   __shared__ uint32_t cand[kCandCap];
   __shared__ uint32_t beam[kMaxW];
+  __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
 
   const int l = lane_id();
-  const int g = l >> 3;
-  const int gl = l & 7;
-  const uint32_t dwords = p.D >> 2;
   const uint32_t beams_per_group = min(kCandCap / p.R, (uint32_t)kWave);
+  const auto rec_of = [&](uint32_t node) { return p.pages + record_offset(p.geom, slot_ct<N2S>(p.geom, node)); };
 
   unsigned long long n_eval = 0, n_reeval = 0, n_exp = 0, n_iter = 0;
 
   for (uint32_t qi = blockIdx.x; qi < p.nq; qi += gridDim.x) {
     HT::clear(ht);
-    U8Vec<VDW, EXACT> q;
-    q.load(p.queries + (uint64_t)qi * p.D, gl, dwords);
-    int qq = 0;
-#pragma unroll
-    for (int t = 0; t < VDW; ++t) qq += (int)__builtin_amdgcn_udot4(q.w[t], q.w[t], 0u, false);
-    qq = sum8(qq);
+    M m;
+    m.load_query(p.queries, qi, p.D, qbuf);
     __syncthreads();
 
     uint32_t ht_used = 0;
@@ -78,11 +72,9 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
 #pragma unroll
     for (int r = 0; r < KPL; ++r) F[r] = kInfKey;
     {
-      U8Vec<VDW, EXACT> x;
-      x.load(p.pages + record_offset(p.geom, slot_ct<N2S>(p.geom, p.entry)), gl, dwords);
-      int d = sum8(partial_u8(q, x)) + qq;
+      const uint32_t d = m.dist_one(rec_of(p.entry));
       if (l == 0) {
-        F[0] = ((uint64_t)(uint32_t)d << 32) | ((uint64_t)p.entry << 1);
+        F[0] = ((uint64_t)d << 32) | ((uint64_t)p.entry << 1);
         bool rec;
         HT::test_and_set(ht, p.entry, true, rec);
       }
@@ -161,40 +153,13 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
 
         // ---- evaluate: gather a batch of vectors in one round trip -------------
         for (uint32_t c0 = 0; c0 < cnt; c0 += kBatch) {
-          // candidate node -> record; lanes past the count read the entry record
-          uint64_t rec[kRounds];
-#pragma unroll
-          for (int rr = 0; rr < kRounds; ++rr) {
-            if (c0 + rr * 8 >= cnt) break;
-            const uint32_t idx = c0 + rr * 8 + g;
-            const uint32_t node = idx < cnt ? cand[idx] : p.entry;
-            rec[rr] = record_offset(p.geom, slot_ct<N2S>(p.geom, node));
-          }
-          U8Vec<VDW, EXACT> x[kRounds];
-#pragma unroll
-          for (int rr = 0; rr < kRounds; ++rr) {
-            if (c0 + rr * 8 >= cnt) break;
-            x[rr].load(p.pages + rec[rr], gl, dwords);
-          }
-          int dist[kChunks];
-#pragma unroll
-          for (int c = 0; c < kChunks; ++c) dist[c] = 0;
-#pragma unroll
-          for (int rr = 0; rr < kRounds; ++rr) {
-            if (c0 + rr * 8 >= cnt) break;
-            const int d = sum8(partial_u8(q, x[rr])) + qq;
-            if (gl == (rr & 7)) dist[rr / 8] = d;
-          }
-          // lane l of chunk c holds candidate c0 + 64c + 8*(l%8) + l/8
-          const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
           uint64_t key[kChunks];
+          m.resident_keys(rec_of, cand, c0, cnt, p.entry, key);
+          const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
           uint64_t pass_mask[kChunks];
           uint32_t survivors = 0;
 #pragma unroll
           for (int c = 0; c < kChunks; ++c) {
-            const uint32_t my_idx = c0 + c * kWave + gl * 8 + g;
-            key[c] = my_idx < cnt ? (((uint64_t)(uint32_t)dist[c] << 32) | ((uint64_t)cand[my_idx] << 1))
-                                  : kInfKey;
             const bool pass = key[c] < thr;
             pass_mask[c] = ballot(pass);
             if (!pass) key[c] = kInfKey;
@@ -205,10 +170,10 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
           if (survivors <= kInsertMax) {
 #pragma unroll
             for (int c = 0; c < kChunks; ++c) {
-              uint64_t m = pass_mask[c];
-              while (m) {
-                const int lane = __builtin_ctzll(m);
-                m &= m - 1;
+              uint64_t pm = pass_mask[c];
+              while (pm) {
+                const int lane = __builtin_ctzll(pm);
+                pm &= pm - 1;
                 insert_key<KPL>(F, readlane64(key[c], lane));
               }
             }
@@ -242,7 +207,7 @@ __global__ __launch_bounds__(kWave) void search_resident_u8(ResidentParams p) {
       if (e < p.k) {
         const bool ok = F[r] != kInfKey;
         p.out_ids[(uint64_t)qi * p.k + e] = ok ? key_id(F[r]) : kNoEdge;
-        p.out_dists[(uint64_t)qi * p.k + e] = ok ? (int32_t)(F[r] >> 32) : INT32_MAX;
+        p.out_dists[(uint64_t)qi * p.k + e] = ok ? (uint32_t)(F[r] >> 32) : M::kPadDist;
       }
     }
   }

@@ -1,13 +1,16 @@
 """GPU parity of the paged search (HBM page cache + host backing store + proxy).
 
 Results must equal the CPU oracle bit-exact whatever the cache size, the
-injected latency, the query-slot oversubscription or the blocking mode.
+injected latency, the query-slot oversubscription or the blocking mode
+(float32 distances compared as uint32 bit patterns).
 """
 import numpy as np
 import pytest
 
 import paper_2607_04415_amd as g
-from workload import IndexSpec, QuerySpec, WORKLOADS, index_arrays, query_array
+import os
+
+from workload import IndexSpec, QuerySpec, WORKLOADS, index_arrays, index_cached, query_array
 
 pytestmark = pytest.mark.gpu
 
@@ -39,6 +42,8 @@ def search(torch, ix, q, k, L, W):
 
 
 def assert_same(gi, gd, oids, od):
+    if gd.dtype == np.float32:
+        gd, od = gd.view(np.uint32), od.view(np.uint32)
     bad = np.flatnonzero((gi != oids).any(1) | (gd != od).any(1))
     assert bad.size == 0, f"{bad.size} queries differ, first {bad[:5]}"
 
@@ -161,3 +166,76 @@ def test_paged_1m_index_slice(orc, torch_dev):
     hr = st["hits"] / max(1, st["hits"] + st["misses"])
     print(f"[1m paged] {st['kernel_ms']:.1f} ms, hit rate {hr:.3f}, served {st['pages_served']}, "
           f"{st['bytes_served'] / st['kernel_ms'] / 1e6:.2f} GB/s", flush=True)
+
+
+F32_SPEC = IndexSpec(n=12000, D=96, dtype="f32", clusters=8, sigma=0.05, r_near=32, r_rand=32, seed=45)
+
+
+@pytest.fixture(scope="module")
+def small_f32(orc):
+    a = index_arrays(F32_SPEC, use_cache=False)
+    q = query_array(F32_SPEC, QuerySpec(300, 46))
+    e = orc.medoid(a["x"])
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"]).search(q, 10, 128, 8, e, threads=8)
+    return a, q, oids, od, oc
+
+
+@pytest.mark.parametrize("frac,latency,oversub,blocking", [
+    (0.05, 20.0, 4, 0), (0.10, 0.0, 1, 1), (0.30, 5.0, 8, 0),
+], ids=["c5-l20-o4", "c10-l0-blocking", "c30-l5-o8"])
+def test_paged_f32_matches_oracle(torch_dev, small_f32, frac, latency, oversub, blocking):
+    a, q, oids, od, oc = small_f32
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(max(int(frac * ix.info["index_bytes"]), 128 * 4096))
+    ix.set_backing(latency_us=latency, oversub=oversub, blocking=bool(blocking))
+    gi, gd, st = search(torch_dev, ix, q, 10, 128, 8)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+    assert st["iterations"] == int(oc["iterations"].sum())
+    assert st["hits"] + st["misses"] == st["expansions"] + st["evaluations"]
+    assert st["misses"] > 0
+
+
+def test_paged_f32_generic_dims(orc, torch_dev):
+    spec = IndexSpec(n=6000, D=37, dtype="f32", clusters=4, sigma=0.05, r_near=12, r_rand=12, seed=47)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(200, 48))
+    e = orc.medoid(a["x"])
+    oids, od, _, _ = orc.pack(a["x"], a["graph"]).search(q, 10, 64, 4, e, threads=8)
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(max(int(0.1 * ix.info["index_bytes"]), 128 * 4096))
+    ix.set_backing(latency_us=0.0, oversub=4)
+    gi, gd, _ = search(torch_dev, ix, q, 10, 64, 4)
+    assert_same(gi, gd, oids, od)
+
+
+F32_10M = WORKLOADS["f32-10m-cache5-lat20"]
+
+
+@pytest.mark.skipif(not (os.environ.get("GORIO_BIG") == "1" or index_cached(F32_10M.index)),
+                    reason="the 10M float32 index is not generated yet (minutes of CPU time); "
+                           "set GORIO_BIG=1 to generate it")
+def test_workload_f32_10m_paged(orc, torch_dev):
+    """The 10M x 96-d float32 index at full size: 5% cache, 20 us latency, 4 query
+    slots per wave, on the first 1,000 queries; the paged answers equal the
+    resident kernel's, and both equal the oracle's on the first 100."""
+    w = F32_10M
+    a = index_arrays(w.index)
+    q = query_array(w.index, w.queries)[:1000]
+    ix = g.Index(a["x"], a["graph"])
+    e = ix.info["entry"]
+    assert e == orc.medoid(a["x"])
+    ri, rd, rst = search(torch_dev, ix, q, w.k, w.L, w.W)
+    ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))
+    assert ix.info["cache_slots"] == int(w.cache_frac * ix.info["index_bytes"]) // 4096
+    ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
+    gi, gd, st = search(torch_dev, ix, q, w.k, w.L, w.W)
+    assert_same(gi, gd, ri, rd)
+    assert st["expansions"] == rst["expansions"]
+    print(f"[f32 10m] resident {rst['kernel_ms']:.1f} ms, paged {st['kernel_ms']:.1f} ms for {len(q)} queries, "
+          f"hit rate {st['hits'] / max(1, st['hits'] + st['misses']):.3f}, "
+          f"{st['bytes_served'] / st['kernel_ms'] / 1e6:.2f} GB/s", flush=True)
+    ix.close()
+    packed = orc.pack(a["x"], a["graph"])
+    oids, od, oc, _ = packed.search(q[:100], w.k, w.L, w.W, e, threads=16)
+    assert_same(gi[:100], gd[:100], oids, od)

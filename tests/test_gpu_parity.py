@@ -3,6 +3,12 @@
 uint8 data: ids and int32 distances must match bit-exact (ties broken by id),
 and the per-search counters (expansions, iterations, first-time evaluations)
 must equal the oracle's summed counts.
+
+float32 data: both sides sum (q_d - x_d)^2 sequentially in d with every
+operation rounded (no fused multiply-add), so distances match bit for bit as
+well (compared as uint32 patterns) and so do the ids; the 1e-5 relative
+tolerance and 0.999 id overlap are checked first as the acceptance bound,
+then exactness.
 """
 import json
 import os
@@ -35,6 +41,17 @@ def run_gpu(torch, ix, q, k, L, W):
     return ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), st
 
 
+def f32_acceptance(gi, gd, oids, od, rel=1e-5, overlap=0.999):
+    """The float32 bound: distances within `rel` relative, ids overlapping at
+    least `overlap` (per-row set intersection over all rows)."""
+    fin = np.isfinite(od)
+    assert np.array_equal(np.isfinite(gd), fin)
+    assert np.all(np.abs(gd[fin] - od[fin]) <= rel * np.abs(od[fin]))
+    common = sum(len(np.intersect1d(a[a != NO_EDGE], b[b != NO_EDGE])) for a, b in zip(gi, oids))
+    total = int((oids != NO_EDGE).sum())
+    assert total == 0 or common / total >= overlap
+
+
 def check_parity(orc, torch, x, graph, q, k, L, W, layout=None, entry=None, counts=True):
     layout = layout or {}
     ix = g.Index(x, graph, entry=entry, **layout)
@@ -44,6 +61,9 @@ def check_parity(orc, torch, x, graph, q, k, L, W, layout=None, entry=None, coun
     okw = {kk: v for kk, v in layout.items() if v is not None and not (np.isscalar(v) and v == 0)}
     oids, od, oc, _ = orc.pack(x, graph, **okw).search(q, k, L, W, e, threads=8)
     gi, gd, st = run_gpu(torch, ix, q, k, L, W)
+    if gd.dtype == np.float32:
+        f32_acceptance(gi, gd, oids, od)
+        gd, od = gd.view(np.uint32), od.view(np.uint32)
     bad = np.flatnonzero((gi != oids).any(1) | (gd != od).any(1))
     assert bad.size == 0, f"{bad.size} queries differ, first {bad[:5]}: gpu {gi[bad[0]]} {gd[bad[0]]} " \
                           f"oracle {oids[bad[0]]} {od[bad[0]]}"
@@ -177,6 +197,63 @@ def test_empty_batch_and_bad_arguments(torch_dev):
         with pytest.raises(g.GorioError) as e:
             ix.search(q, k, L, W)
         assert e.value.status == g.EINVAL
+
+
+F32_CASES = [
+    # n, D, R, clusters, k, L, W
+    (2000, 96, 32, 4, 10, 64, 4),
+    (3000, 96, 64, 8, 10, 128, 8),        # the 10M workload's shape at a small n
+    (1500, 37, 24, 3, 12, 100, 5),        # generic path, D not a multiple of 4
+    (1000, 256, 16, 4, 5, 200, 16),
+    (800, 1, 8, 2, 4, 16, 2),
+    (1200, 20, 40, 3, 256, 256, 64),
+]
+
+
+@pytest.mark.parametrize("case", F32_CASES,
+                         ids=[f"n{c[0]}-D{c[1]}-R{c[2]}-k{c[4]}-L{c[5]}-W{c[6]}" for c in F32_CASES])
+def test_parity_f32_mixture(orc, torch_dev, case):
+    n, D, R, C, k, L, W = case
+    spec = IndexSpec(n=n, D=D, dtype="f32", clusters=C, sigma=0.05, r_near=R // 2, r_rand=R - R // 2,
+                     seed=300 + n)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(300, 17 + n))
+    check_parity(orc, torch_dev, a["x"], a["graph"], q, k, L, W)
+
+
+def test_parity_f32_layout_perm_and_wide_records(orc, torch_dev):
+    rng = np.random.default_rng(21)
+    spec = IndexSpec(n=2500, D=96, dtype="f32", clusters=5, sigma=0.05, r_near=32, r_rand=32, seed=22)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(200, 23))
+    for layout in (dict(node_to_slot=rng.permutation(2500).astype(np.uint32)), dict(record_bytes=700),
+                   dict(page_bytes=8192, records_per_page=5)):
+        check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 128, 8, layout=layout)
+
+
+def test_f32_ties_zero_distance_and_padding(orc, torch_dev):
+    rng = np.random.default_rng(24)
+    base = rng.standard_normal((40, 12)).astype(np.float32)
+    x = base[rng.integers(0, 40, 900)]                # identical vectors: equal distances
+    graph = random_graph(rng, 900, 16, sentinel_frac=0.2)
+    q = np.concatenate([base[:20], rng.standard_normal((20, 12)).astype(np.float32)])
+    check_parity(orc, torch_dev, x, graph, q, 16, 64, 4)
+    # a 5-node component: the tail of every row is padding (+inf)
+    x2 = rng.standard_normal((50, 8)).astype(np.float32)
+    g2 = np.full((50, 2), NO_EDGE, np.uint32)
+    for i in range(5):
+        g2[i] = [(i + 1) % 5, (i + 3) % 5]
+    ix, _ = check_parity(orc, torch_dev, x2, g2, x2[:3], 8, 16, 2, entry=0)
+    gi, gd, _ = run_gpu(torch_dev, ix, x2[:3], 8, 16, 2)
+    assert (gi[:, 5:] == NO_EDGE).all() and np.isposinf(gd[:, 5:]).all()
+
+
+def test_f32_visited_filter_overflow_still_exact(orc, torch_dev):
+    spec = IndexSpec(n=60000, D=16, dtype="f32", clusters=8, sigma=0.05, r_near=32, r_rand=32, seed=25)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(48, 26))
+    _, st = check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 256, 8)
+    assert st["reevaluations"] > 0, "the test did not exercise the overflow path"
 
 
 def test_entry_rule_matches_oracle_f32(orc, torch_dev):

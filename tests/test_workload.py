@@ -36,6 +36,22 @@ def test_edge_rule_small_clusters():
         assert row[:6] == want.tolist()
 
 
+def test_edge_rule_small_clusters_f32():
+    """float32 vectors: the near edges are the cluster's top-R_near by float64 distance."""
+    rng = np.random.default_rng(6)
+    n, D, C = 500, 13, 4
+    x = rng.standard_normal((n, D)).astype(np.float32)
+    labels = rng.integers(0, C, n).astype(np.uint32)
+    g = gen_graph(x, labels, C, 1024, 5, 3, seed=11)
+    for i in range(0, n, 5):
+        row = g[i].tolist()
+        assert i not in row and len(set(row)) == len(row)
+        same = np.flatnonzero((labels == labels[i]) & (np.arange(n) != i))
+        d = ((x[same].astype(np.float64) - x[i].astype(np.float64)) ** 2).sum(1)
+        want = same[np.lexsort((same, d))][:5]
+        assert row[:5] == want.tolist()
+
+
 def test_edge_rule_sampled_clusters():
     """Clusters larger than the sample: near edges are same-cluster and sorted by (dist, id)."""
     rng = np.random.default_rng(4)

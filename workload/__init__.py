@@ -6,7 +6,7 @@ search's own arithmetic and is the only code shared by the CPU oracle side and
 the GPU library side (both receive its arrays as plain inputs).
 """
 from .gen import (IndexSpec, QuerySpec, Workload, WORKLOADS, build_edges_lib,
-                  index_arrays, query_array, workload, cache_dir)
+                  index_arrays, index_cached, query_array, workload, cache_dir)
 
 __all__ = ["IndexSpec", "QuerySpec", "Workload", "WORKLOADS", "build_edges_lib",
-           "index_arrays", "query_array", "workload", "cache_dir"]
+           "index_arrays", "index_cached", "query_array", "workload", "cache_dir"]

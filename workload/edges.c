@@ -55,20 +55,30 @@ static double pair_dist(int dtype, const void *x, uint32_t D, uint64_t a, uint64
         }
         return (double)s;
     } else {
+        /* four interleaved float64 partial sums, combined in a fixed order: the
+           same value on every machine, and the loop vectorizes */
         const float *pa = (const float *)x + a * D, *pb = (const float *)x + b * D;
-        double s = 0.0;
-        for (uint32_t d = 0; d < D; ++d) {
+        double s[4] = {0.0, 0.0, 0.0, 0.0};
+        uint32_t d = 0;
+        for (; d + 4 <= D; d += 4)
+            for (int j = 0; j < 4; ++j) {
+                double t = (double)pa[d + j] - (double)pb[d + j];
+                s[j] += t * t;
+            }
+        for (; d < D; ++d) {
             double t = (double)pa[d] - (double)pb[d];
-            s += t * t;
+            s[0] += t * t;
         }
-        return s;
+        return (s[0] + s[1]) + (s[2] + s[3]);
     }
 }
 
 /*
- * dtype: 0 = uint8, 1 = float32; x is n x D row-major.
+ * dtype: 0 = uint8, 1 = float32.
  * cluster_start[C+1] / members[n]: nodes of cluster c are
  *   members[cluster_start[c] .. cluster_start[c+1]) in ascending id order.
+ * x: n x D row-major in members order (row t is the vector of node members[t]),
+ *   so each cluster's vectors are contiguous.
  * graph: n x (r_near + r_rand) output.
  * Returns 0 on success, -1 on bad arguments, -2 on allocation failure.
  */
@@ -96,10 +106,13 @@ int gen_edges(int dtype, const void *x, uint64_t n, uint32_t D,
 #pragma omp atomic write
             err = -2;
         }
+        /* nodes are visited cluster by cluster (members order), so the cluster a
+           node samples from stays in cache; each node's output depends only on
+           its own stream, not on the visiting order */
 #pragma omp for schedule(dynamic, 256)
         for (int64_t ii = 0; ii < (int64_t)n; ++ii) {
             if (err) continue;
-            const uint64_t i = (uint64_t)ii;
+            const uint64_t i = members[ii];
             uint64_t st = seed * 0xD1B54A32D192ED03ull ^ ((i + 1) * 0x8CB92BA72F3D8DD7ull);
             const uint32_t c = label[i];
             const uint64_t base = cluster_start[c];
@@ -111,6 +124,8 @@ int gen_edges(int dtype, const void *x, uint64_t n, uint32_t D,
                 if (members[base + mid] < i) lo = mid + 1; else hi = mid;
             }
             const uint64_t self_pos = lo;
+            /* row of node i in x */
+            const uint64_t xi = (uint64_t)ii;
             const uint64_t M = m - 1; /* cluster without i */
             uint64_t cnt = 0;
             if (M <= sample) {
@@ -128,8 +143,9 @@ int gen_edges(int dtype, const void *x, uint64_t n, uint32_t D,
             uint32_t nb = 0;
             for (uint64_t t = 0; t < cnt; ++t) {
                 uint64_t p = pick[t];
-                uint32_t v = members[base + (p < self_pos ? p : p + 1)];
-                near_t e = { pair_dist(dtype, x, D, i, v), v };
+                const uint64_t xv = base + (p < self_pos ? p : p + 1);
+                uint32_t v = members[xv];
+                near_t e = { pair_dist(dtype, x, D, xi, xv), v };
                 if (nb == r_near && !near_less(e, best[nb - 1])) continue;
                 uint32_t pos = (nb < r_near) ? nb++ : nb - 1;
                 while (pos > 0 && near_less(e, best[pos - 1])) { best[pos] = best[pos - 1]; --pos; }

@@ -20,6 +20,7 @@ import dataclasses
 import hashlib
 import json
 import os
+import sys
 import subprocess
 from pathlib import Path
 
@@ -172,7 +173,8 @@ def gen_graph(x: np.ndarray, labels: np.ndarray, clusters: int, sample: int,
     np.cumsum(counts, out=start[1:])
     graph = np.empty((n, r_near + r_rand), np.uint32)
     dtype = 0 if x.dtype == np.uint8 else 1
-    rc = _edges().gen_edges(dtype, x.ctypes.data, n, D, start.ctypes.data, members.ctypes.data,
+    xs = np.ascontiguousarray(x[members])   # cluster by cluster: a node's samples are close in memory
+    rc = _edges().gen_edges(dtype, xs.ctypes.data, n, D, start.ctypes.data, members.ctypes.data,
                             labels.ctypes.data, clusters, sample, r_near, r_rand, seed,
                             graph.ctypes.data)
     if rc != 0:
@@ -190,12 +192,19 @@ def _centres(rng: np.random.Generator, C: int, D: int, dtype: str) -> np.ndarray
     return c / np.linalg.norm(c, axis=1, keepdims=True)
 
 
+def _progress(msg: str):
+    """Progress of long generations on stderr (large workloads take minutes)."""
+    print(f"[workload] {msg}", file=sys.stderr, flush=True)
+
+
 def _draw(rng: np.random.Generator, centres: np.ndarray, count: int, sigma: float,
           dtype: str):
     C, D = centres.shape
     labels = rng.integers(0, C, size=count).astype(np.uint32)
     out = np.empty((count, D), np.uint8 if dtype == "u8" else np.float32)
     for s in range(0, count, _CHUNK):
+        if count > 50 * _CHUNK and (s // _CHUNK) % 50 == 0:
+            _progress(f"drawing vectors {s:,}/{count:,}")
         e = min(count, s + _CHUNK)
         v = centres[labels[s:e]] + sigma * rng.standard_normal(size=(e - s, D))
         if dtype == "u8":
@@ -213,12 +222,26 @@ def _cached(tag: str, key_obj, make):
         return {k: np.load(d / f"{k}.npy", allow_pickle=False) for k in names}
     arrays = make()
     d.mkdir(parents=True, exist_ok=True)
+    big = sum(v.nbytes for v in arrays.values()) > (1 << 30)
     for k, v in arrays.items():
+        if big:
+            _progress(f"saving {k} ({v.nbytes / 1e9:.2f} GB) to {d}")
         tmp = d / f"{k}.{os.getpid()}.tmp.npy"
         np.save(tmp, v)
         os.replace(tmp, d / f"{k}.npy")
     done.write_text(" ".join(arrays))
     return arrays
+
+
+def _index_key(spec: IndexSpec) -> dict:
+    # the edge builder's source is part of the key: a change to it never
+    # reuses graphs it built before
+    return {**dataclasses.asdict(spec), "edges_src": hashlib.sha256(_EDGES_SRC.read_bytes()).hexdigest()[:16]}
+
+
+def index_cached(spec: IndexSpec) -> bool:
+    """Whether index_arrays(spec) would load from the cache instead of generating."""
+    return (cache_dir() / f"index-{_key(_index_key(spec))}" / "DONE").exists()
 
 
 def index_arrays(spec: IndexSpec, use_cache: bool = True) -> dict:
@@ -227,12 +250,14 @@ def index_arrays(spec: IndexSpec, use_cache: bool = True) -> dict:
         rng = np.random.default_rng(spec.seed)
         centres = _centres(rng, spec.clusters, spec.D, spec.dtype)
         labels, x = _draw(rng, centres, spec.n, spec.sigma, spec.dtype)
+        if spec.n >= 1_000_000:
+            _progress(f"building edges for {spec.n:,} nodes")
         graph = gen_graph(x, labels, spec.clusters, spec.sample, spec.r_near, spec.r_rand,
                           spec.seed)
         return {"x": x, "graph": graph, "labels": labels, "centres": centres}
     if not use_cache:
         return make()
-    return _cached("index", dataclasses.asdict(spec), make)
+    return _cached("index", _index_key(spec), make)
 
 
 def query_array(spec: IndexSpec, q: QuerySpec) -> np.ndarray:
