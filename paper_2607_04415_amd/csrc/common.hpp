@@ -72,89 +72,115 @@ __device__ __forceinline__ uint64_t record_offset(const PageGeom &g, uint32_t s)
 }
 
 // ---------------------------------------------------------------------------
-// Visited filter: open addressing in LDS, linear probing, one table per wave.
+// Visited filter in LDS, one table per wave: open addressing over buckets of
+// four 32-bit slots (16 bytes, read with one ds_read_b128), linear probing
+// from bucket to bucket.  An id is inserted into the first empty slot of the
+// first bucket on its probe path that has one; slots are never freed, so a
+// bucket seen with an empty slot and without the id proves the id absent.
 // It may forget (a full table stops recording) but never invents a member, so
 // a node is at worst evaluated twice; the frontier merge removes the copy.
 // ---------------------------------------------------------------------------
 template <int LOG2>
 struct VisitedLds {
-  static constexpr uint32_t kSize = 1u << LOG2;
+  static constexpr uint32_t kSize = 1u << LOG2;         // slots
+  static constexpr uint32_t kBuckets = kSize / 4;
   static constexpr uint32_t kLimit = kSize - kSize / 4;  // stop recording at 75% load
-  static constexpr int kMaxProbe = 64;
+  static constexpr int kMaxRounds = 64;
 
-  __device__ __forceinline__ static uint32_t hash(uint32_t id) {
-    return (id * 0x9E3779B1u) >> (32 - LOG2);
+  __device__ __forceinline__ static uint32_t bucket(uint32_t id) {
+    return (id * 0x9E3779B1u) >> (32 - (LOG2 - 2));
   }
 
   __device__ __forceinline__ static void clear(uint32_t *t) {
     uint4 *t4 = reinterpret_cast<uint4 *>(t);
     const uint4 e = make_uint4(kHtEmpty, kHtEmpty, kHtEmpty, kHtEmpty);
-    for (uint32_t i = lane_id(); i < kSize / 4; i += kWave) t4[i] = e;
+    for (uint32_t i = lane_id(); i < kBuckets; i += kWave) t4[i] = e;
   }
 
-  // Returns true when id was not recorded before (evaluate it).  `recorded`
-  // tells whether this call stored it.
+  // First slot of bucket word v that holds `id` (4: none) and first empty
+  // slot (4: none).
+  __device__ __forceinline__ static void scan(const uint4 &v, uint32_t id, uint32_t &hit, uint32_t &empty) {
+    hit = v.x == id ? 0u : v.y == id ? 1u : v.z == id ? 2u : v.w == id ? 3u : 4u;
+    empty = v.x == kHtEmpty ? 0u : v.y == kHtEmpty ? 1u : v.z == kHtEmpty ? 2u : v.w == kHtEmpty ? 3u : 4u;
+  }
+
+  // One id (wave-uniform call, any lane mask): true when id was not recorded
+  // before (evaluate it); `recorded` tells whether this call stored it.
   __device__ __forceinline__ static bool test_and_set(uint32_t *t, uint32_t id, bool may_store,
                                                        bool &recorded) {
-    uint32_t h = hash(id);
-    recorded = false;
-    for (int p = 0; p < kMaxProbe; ++p) {
-      uint32_t old;
-      if (may_store) {
-        old = atomicCAS(&t[h], kHtEmpty, id);
-        if (old == kHtEmpty) { recorded = true; return true; }
-      } else {
-        old = t[h];
-        if (old == kHtEmpty) return true;
-      }
-      if (old == id) return false;
-      h = (h + 1) & (kSize - 1);
-    }
-    return true;
+    uint32_t ids[1] = {id};
+    bool valid[1] = {true}, isnew[1], rec[1];
+    test_and_set_n<1>(t, ids, valid, may_store, isnew, rec);
+    recorded = rec[0];
+    return isnew[0];
   }
 
-  // N ids per lane at once (the LDS atomics of one probe round issue back to
-  // back).  isnew[i]: evaluate ids[i]; recorded[i]: this call stored it.
+  // N ids per lane at once: each round reads every pending id's bucket, then
+  // claims the first empty slot with one LDS CAS.  isnew[i]: evaluate
+  // ids[i]; recorded[i]: this call stored it.
   template <int N>
   __device__ __forceinline__ static void test_and_set_n(uint32_t *t, const uint32_t (&ids)[N],
                                                         const bool (&valid)[N], bool may_store,
                                                         bool (&isnew)[N], bool (&recorded)[N]) {
-    uint32_t h[N];
+    const uint4 *t4 = reinterpret_cast<const uint4 *>(t);
+    uint32_t b[N];
     bool pend[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      h[i] = hash(ids[i]);
+      b[i] = bucket(ids[i]);
       pend[i] = valid[i];
       isnew[i] = false;
       recorded[i] = false;
     }
-    for (int p = 0; p < kMaxProbe; ++p) {
+    for (int round = 0; round < kMaxRounds; ++round) {
       bool any = false;
 #pragma unroll
       for (int i = 0; i < N; ++i) any |= pend[i];
       if (ballot(any) == 0) break;
-      uint32_t old[N];
+      uint4 v[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        if (pend[i]) v[i] = t4[b[i]];
+      bool cas[N];
+      uint32_t slot[N];
 #pragma unroll
       for (int i = 0; i < N; ++i) {
-        if (pend[i]) old[i] = may_store ? atomicCAS(&t[h[i]], kHtEmpty, ids[i]) : t[h[i]];
-      }
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
+        cas[i] = false;
+        slot[i] = 0;
         if (!pend[i]) continue;
-        if (old[i] == kHtEmpty) {
-          isnew[i] = true;
-          recorded[i] = may_store;
-          pend[i] = false;
-        } else if (old[i] == ids[i]) {
+        uint32_t hit, empty;
+        scan(v[i], ids[i], hit, empty);
+        if (hit < 4) {
+          pend[i] = false;                       // already recorded
+        } else if (empty == 4) {
+          b[i] = (b[i] + 1) & (kBuckets - 1);    // bucket full: the next one
+        } else if (!may_store) {
+          isnew[i] = true;                       // absent; the table is no longer recording
           pend[i] = false;
         } else {
-          h[i] = (h[i] + 1) & (kSize - 1);
+          cas[i] = true;
+          slot[i] = b[i] * 4 + empty;
         }
+      }
+      uint32_t old[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        if (cas[i]) old[i] = atomicCAS(&t[slot[i]], kHtEmpty, ids[i]);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        if (!cas[i]) continue;
+        if (old[i] == kHtEmpty) {
+          isnew[i] = true;
+          recorded[i] = true;
+          pend[i] = false;
+        } else if (old[i] == ids[i]) {
+          pend[i] = false;                       // another lane recorded the same id
+        }                                        // else: lost the slot, read the bucket again
       }
     }
 #pragma unroll
     for (int i = 0; i < N; ++i)
-      if (pend[i]) isnew[i] = true;  // probe limit: evaluate, unrecorded
+      if (pend[i]) isnew[i] = true;  // round limit: evaluate, unrecorded
   }
 };
 

@@ -53,27 +53,28 @@ struct MetricU8 {
     return (uint32_t)(sum8(partial_u8(q, x)) + qq);
   }
 
-  // Keys of candidates c0 .. c0 + kBatch - 1 of cand (kInfKey past cnt);
-  // rec_of(node) is the node's record address.  One round trip for the batch.
-  template <class RecOf>
-  __device__ __forceinline__ void resident_keys(RecOf rec_of, const uint32_t *cand, uint32_t c0, uint32_t cnt,
-                                                uint32_t fallback, uint64_t (&key)[kChunks]) const {
+  // Keys of candidates c0 .. c0 + kBatch - 1 of cand (kInfKey past cnt), from
+  // the resident pages.  One round trip for the batch.
+  template <bool N2S>
+  __device__ __forceinline__ void resident_keys(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
+                                                uint32_t c0, uint32_t cnt, uint32_t fallback,
+                                                uint64_t (&key)[kChunks]) const {
     const int l = lane_id();
     const int g = l >> 3;
     const int gl = l & 7;
     // candidate node -> record; lanes past the count read the fallback record
-    const uint8_t *rec[kRounds];
+    uint64_t rec[kRounds];
 #pragma unroll
     for (int rr = 0; rr < kRounds; ++rr) {
       if (c0 + rr * 8 >= cnt) break;
       const uint32_t idx = c0 + rr * 8 + g;
-      rec[rr] = rec_of(idx < cnt ? cand[idx] : fallback);
+      rec[rr] = record_offset(geom, slot_ct<N2S>(geom, idx < cnt ? cand[idx] : fallback));
     }
     U8Vec<VDW, EXACT> x[kRounds];
 #pragma unroll
     for (int rr = 0; rr < kRounds; ++rr) {
       if (c0 + rr * 8 >= cnt) break;
-      x[rr].load(rec[rr], gl, dwords);
+      x[rr].load(pages + rec[rr], gl, dwords);
     }
     int dist[kChunks];
 #pragma unroll
@@ -234,12 +235,13 @@ struct MetricF32 {
     return first_lane_value(b);
   }
 
-  template <class RecOf>
-  __device__ __forceinline__ void resident_keys(RecOf rec_of, const uint32_t *cand, uint32_t c0, uint32_t cnt,
-                                                uint32_t fallback, uint64_t (&key)[kChunks]) const {
+  template <bool N2S>
+  __device__ __forceinline__ void resident_keys(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
+                                                uint32_t c0, uint32_t cnt, uint32_t fallback,
+                                                uint64_t (&key)[kChunks]) const {
     const uint32_t idx = c0 + lane_id();
     const uint32_t node = idx < cnt ? cand[idx] : fallback;
-    const float d = dist_global(rec_of(node));
+    const float d = dist_global(pages + record_offset(geom, slot_ct<N2S>(geom, node)));
     key[0] = idx < cnt ? (((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)node << 1)) : kInfKey;
   }
 

@@ -47,14 +47,13 @@ __global__ __launch_bounds__(kWave) void search_resident(ResidentParams p) {
   constexpr int kBatch = M::kBatch;
   constexpr int kIdsPerLane = kCandCap / kWave;
 
-  __shared__ uint32_t ht[HT::kSize];
+  __shared__ __align__(16) uint32_t ht[HT::kSize];
   __shared__ uint32_t cand[kCandCap];
   __shared__ uint32_t beam[kMaxW];
   __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
 
   const int l = lane_id();
   const uint32_t beams_per_group = min(kCandCap / p.R, (uint32_t)kWave);
-  const auto rec_of = [&](uint32_t node) { return p.pages + record_offset(p.geom, slot_ct<N2S>(p.geom, node)); };
 
   unsigned long long n_eval = 0, n_reeval = 0, n_exp = 0, n_iter = 0;
 
@@ -72,7 +71,7 @@ __global__ __launch_bounds__(kWave) void search_resident(ResidentParams p) {
 #pragma unroll
     for (int r = 0; r < KPL; ++r) F[r] = kInfKey;
     {
-      const uint32_t d = m.dist_one(rec_of(p.entry));
+      const uint32_t d = m.dist_one(p.pages + record_offset(p.geom, slot_ct<N2S>(p.geom, p.entry)));
       if (l == 0) {
         F[0] = ((uint64_t)d << 32) | ((uint64_t)p.entry << 1);
         bool rec;
@@ -154,7 +153,7 @@ __global__ __launch_bounds__(kWave) void search_resident(ResidentParams p) {
         // ---- evaluate: gather a batch of vectors in one round trip -------------
         for (uint32_t c0 = 0; c0 < cnt; c0 += kBatch) {
           uint64_t key[kChunks];
-          m.resident_keys(rec_of, cand, c0, cnt, p.entry, key);
+          m.template resident_keys<N2S>(p.pages, p.geom, cand, c0, cnt, p.entry, key);
           const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
           uint64_t pass_mask[kChunks];
           uint32_t survivors = 0;
