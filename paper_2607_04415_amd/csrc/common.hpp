@@ -97,11 +97,10 @@ struct VisitedLds {
     for (uint32_t i = lane_id(); i < kBuckets; i += kWave) t4[i] = e;
   }
 
-  // First slot of bucket word v that holds `id` (4: none) and first empty
-  // slot (4: none).
-  __device__ __forceinline__ static void scan(const uint4 &v, uint32_t id, uint32_t &hit, uint32_t &empty) {
-    hit = v.x == id ? 0u : v.y == id ? 1u : v.z == id ? 2u : v.w == id ? 3u : 4u;
-    empty = v.x == kHtEmpty ? 0u : v.y == kHtEmpty ? 1u : v.z == kHtEmpty ? 2u : v.w == kHtEmpty ? 3u : 4u;
+  // Bit j set: slot j of bucket v holds x.
+  __device__ __forceinline__ static uint32_t match4(const uint4 &v, uint32_t x) {
+    return (uint32_t)(v.x == x) | ((uint32_t)(v.y == x) << 1) | ((uint32_t)(v.z == x) << 2) |
+           ((uint32_t)(v.w == x) << 3);
   }
 
   // One id (wave-uniform call, any lane mask): true when id was not recorded
@@ -139,43 +138,38 @@ struct VisitedLds {
       if (ballot(any) == 0) break;
       uint4 v[N];
 #pragma unroll
-      for (int i = 0; i < N; ++i)
+      for (int i = 0; i < N; ++i) {
+        v[i] = make_uint4(kHtEmpty, kHtEmpty, kHtEmpty, kHtEmpty);
         if (pend[i]) v[i] = t4[b[i]];
+      }
+      // branch-free decision per id: recorded already / bucket full / absent
       bool cas[N];
       uint32_t slot[N];
 #pragma unroll
       for (int i = 0; i < N; ++i) {
-        cas[i] = false;
-        slot[i] = 0;
-        if (!pend[i]) continue;
-        uint32_t hit, empty;
-        scan(v[i], ids[i], hit, empty);
-        if (hit < 4) {
-          pend[i] = false;                       // already recorded
-        } else if (empty == 4) {
-          b[i] = (b[i] + 1) & (kBuckets - 1);    // bucket full: the next one
-        } else if (!may_store) {
-          isnew[i] = true;                       // absent; the table is no longer recording
-          pend[i] = false;
-        } else {
-          cas[i] = true;
-          slot[i] = b[i] * 4 + empty;
-        }
+        const uint32_t hitm = match4(v[i], ids[i]);
+        const uint32_t emptym = match4(v[i], kHtEmpty);
+        const bool absent = pend[i] && hitm == 0 && emptym != 0;
+        const bool full = pend[i] && hitm == 0 && emptym == 0;
+        cas[i] = absent && may_store;
+        isnew[i] = isnew[i] || (absent && !may_store);
+        slot[i] = b[i] * 4 + (uint32_t)__builtin_ctz(emptym | 16u);
+        b[i] = full ? ((b[i] + 1) & (kBuckets - 1)) : b[i];
+        pend[i] = full || cas[i];
       }
       uint32_t old[N];
 #pragma unroll
-      for (int i = 0; i < N; ++i)
+      for (int i = 0; i < N; ++i) {
+        old[i] = 0;
         if (cas[i]) old[i] = atomicCAS(&t[slot[i]], kHtEmpty, ids[i]);
+      }
 #pragma unroll
       for (int i = 0; i < N; ++i) {
-        if (!cas[i]) continue;
-        if (old[i] == kHtEmpty) {
-          isnew[i] = true;
-          recorded[i] = true;
-          pend[i] = false;
-        } else if (old[i] == ids[i]) {
-          pend[i] = false;                       // another lane recorded the same id
-        }                                        // else: lost the slot, read the bucket again
+        const bool won = cas[i] && old[i] == kHtEmpty;
+        const bool same = cas[i] && old[i] == ids[i];  // another lane recorded the same id
+        isnew[i] = isnew[i] || won;
+        recorded[i] = recorded[i] || won;
+        pend[i] = pend[i] && !won && !same;           // lost the slot: read the bucket again
       }
     }
 #pragma unroll
