@@ -83,6 +83,8 @@ __device__ __forceinline__ uint64_t record_offset(const PageGeom &g, uint32_t s)
 template <int LOG2>
 struct VisitedLds {
   static constexpr uint32_t kSize = 1u << LOG2;         // slots
+  static constexpr uint32_t kWords = kSize;             // 32-bit LDS words
+  static constexpr uint32_t kMaxId = 0xFFFFFFFFu;       // any id below kHtEmpty
   static constexpr uint32_t kBuckets = kSize / 4;
   static constexpr uint32_t kLimit = kSize - kSize / 4;  // stop recording at 75% load
   static constexpr int kMaxRounds = 64;
@@ -170,6 +172,132 @@ struct VisitedLds {
         isnew[i] = isnew[i] || won;
         recorded[i] = recorded[i] || won;
         pend[i] = pend[i] && !won && !same;           // lost the slot: read the bucket again
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (pend[i]) isnew[i] = true;  // round limit: evaluate, unrecorded
+  }
+};
+
+// Compact visited filter in LDS: 16-bit entries, buckets of eight (16 bytes,
+// one ds_read_b128), for ids below 2^(LOG2 + 11) (2^24 for 8192 entries).
+// h = (id * odd) mod 2^(LOG2 + 11) is a bijection; its top LOG2 - 3 bits
+// pick the home bucket, its low 14 bits r are stored as 1 + (d << 14 | r),
+// where d in {0, 1} is the bucket's distance from home (0 marks an empty
+// slot).  (bucket - d, r) gives back h, so an entry matches exactly one id:
+// the filter never invents a member.  An id whose home bucket and the next
+// are both full is not recorded.
+template <int LOG2>
+struct VisitedLds16 {
+  static constexpr uint32_t kSize = 1u << LOG2;          // 16-bit slots
+  static constexpr uint32_t kWords = kSize / 2;          // 32-bit LDS words
+  static constexpr uint32_t kBuckets = kSize / 8;
+  static constexpr uint32_t kLimit = kSize - kSize / 4;   // stop recording at 75% load
+  static constexpr int kHomeBits = LOG2 - 3;
+  static constexpr uint32_t kMaxId = 1u << (kHomeBits + 14);  // ids must be below this
+  static constexpr int kMaxRounds = 64;
+
+  __device__ __forceinline__ static uint32_t mix(uint32_t id) { return (id * 0x9E3779B1u) & (kMaxId - 1); }
+
+  __device__ __forceinline__ static void clear(uint32_t *t) {
+    uint4 *t4 = reinterpret_cast<uint4 *>(t);
+    for (uint32_t i = lane_id(); i < kBuckets; i += kWave) t4[i] = make_uint4(0u, 0u, 0u, 0u);
+  }
+
+  // Bits 15 and 31 of the result: the low / high half of w is zero.
+  __device__ __forceinline__ static uint32_t zero_halves(uint32_t w) {
+    return ~(((w & 0x7FFF7FFFu) + 0x7FFF7FFFu) | w | 0x7FFF7FFFu);
+  }
+  // Bit j set: half j (0..7, low half first) of bucket v equals e (e replicated in both halves).
+  __device__ __forceinline__ static uint32_t match8(const uint4 &v, uint32_t e2) {
+    const uint32_t a = zero_halves(v.x ^ e2), b = zero_halves(v.y ^ e2);
+    const uint32_t c = zero_halves(v.z ^ e2), d = zero_halves(v.w ^ e2);
+    return ((a >> 15) & 1u) | ((a >> 30) & 2u) | ((b >> 13) & 4u) | ((b >> 28) & 8u) |
+           ((c >> 11) & 16u) | ((c >> 26) & 32u) | ((d >> 9) & 64u) | ((d >> 24) & 128u);
+  }
+  __device__ __forceinline__ static uint32_t word_of(const uint4 &v, uint32_t k) {
+    return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
+  }
+
+  __device__ __forceinline__ static bool test_and_set(uint32_t *t, uint32_t id, bool may_store,
+                                                       bool &recorded) {
+    uint32_t ids[1] = {id};
+    bool valid[1] = {true}, isnew[1], rec[1];
+    test_and_set_n<1>(t, ids, valid, may_store, isnew, rec);
+    recorded = rec[0];
+    return isnew[0];
+  }
+
+  // Same contract as VisitedLds::test_and_set_n (ids < 2^24).
+  template <int N>
+  __device__ __forceinline__ static void test_and_set_n(uint32_t *t, const uint32_t (&ids)[N],
+                                                        const bool (&valid)[N], bool may_store,
+                                                        bool (&isnew)[N], bool (&recorded)[N]) {
+    const uint4 *t4 = reinterpret_cast<const uint4 *>(t);
+    uint32_t home[N], r[N], d[N];
+    bool pend[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const uint32_t h = mix(ids[i]);
+      home[i] = h >> 14;
+      r[i] = h & 0x3FFFu;
+      d[i] = 0;
+      pend[i] = valid[i];
+      isnew[i] = false;
+      recorded[i] = false;
+    }
+    for (int round = 0; round < kMaxRounds; ++round) {
+      bool any = false;
+#pragma unroll
+      for (int i = 0; i < N; ++i) any |= pend[i];
+      if (ballot(any) == 0) break;
+      // after the first round few ids are left: skip an id no lane still holds
+      bool live[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) live[i] = round == 0 || ballot(pend[i]) != 0;
+      uint4 v[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        v[i] = make_uint4(0u, 0u, 0u, 0u);
+        if (live[i] && pend[i]) v[i] = t4[(home[i] + d[i]) & (kBuckets - 1)];
+      }
+      bool cas[N];
+      uint32_t word[N], expect[N], want[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        cas[i] = false;
+        word[i] = expect[i] = want[i] = 0;
+        if (!live[i]) continue;
+        const uint32_t e = 1u + ((d[i] << 14) | r[i]);
+        const uint32_t hitm = match8(v[i], e | (e << 16));
+        const uint32_t emptym = match8(v[i], 0u);
+        const bool absent = pend[i] && hitm == 0 && emptym != 0;
+        const bool full = pend[i] && hitm == 0 && emptym == 0;
+        const bool next = full && d[i] == 0;
+        const bool lost = full && d[i] != 0;          // both buckets full: not recorded
+        cas[i] = absent && may_store;
+        isnew[i] = isnew[i] || (absent && !may_store) || lost;
+        const uint32_t j = (uint32_t)__builtin_ctz(emptym | 256u) & 7u;
+        const uint32_t w = word_of(v[i], j >> 1);
+        word[i] = ((home[i] + d[i]) & (kBuckets - 1)) * 4 + (j >> 1);
+        expect[i] = w;
+        want[i] = w | (e << ((j & 1u) * 16));
+        d[i] = next ? 1u : d[i];
+        pend[i] = next || cas[i];
+      }
+      uint32_t old[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        old[i] = 0;
+        if (cas[i]) old[i] = atomicCAS(&t[word[i]], expect[i], want[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const bool won = cas[i] && old[i] == expect[i];
+        isnew[i] = isnew[i] || won;
+        recorded[i] = recorded[i] || won;
+        pend[i] = pend[i] && !won;   // the word changed: read the bucket again
       }
     }
 #pragma unroll

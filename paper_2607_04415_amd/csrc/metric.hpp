@@ -24,9 +24,9 @@ namespace gorio {
 // ---------------------------------------------------------------------------
 template <int VDW, bool EXACT>
 struct MetricU8 {
-  // vectors in flight per resident gather batch: 256 for up to 16 B per lane,
-  // fewer for wider rows
-  static constexpr int kRounds = VDW <= 4 ? 32 : 128 / VDW;
+  // vectors in flight per resident gather batch: 128 for up to 16 B per lane,
+  // 64 for wider rows (kept small so that two waves fit each SIMD's registers)
+  static constexpr int kRounds = VDW <= 4 ? 16 : 8;
   static constexpr int kBatch = kRounds * 8;
   static constexpr int kChunks = kBatch / kWave;
   static constexpr int kQueryWords = 1;          // the query lives in registers

@@ -40,14 +40,15 @@ struct ResidentParams {
   unsigned long long *stats;  // [evaluations, reevaluations, expansions, iterations]
 };
 
-template <int KPL, class M, int HT_LOG2, bool N2S>
-__global__ __launch_bounds__(kWave) void search_resident(ResidentParams p) {
-  using HT = VisitedLds<HT_LOG2>;
+// Two waves per SIMD (registers <= 256 per lane, LDS <= 20 KB with the 16-bit
+// visited table): one wave's gathers overlap the other's filtering and merging.
+template <int KPL, class M, class HT, bool N2S>
+__global__ __launch_bounds__(kWave, 2) void search_resident(ResidentParams p) {
   constexpr int kChunks = M::kChunks;
   constexpr int kBatch = M::kBatch;
   constexpr int kIdsPerLane = kCandCap / kWave;
 
-  __shared__ __align__(16) uint32_t ht[HT::kSize];
+  __shared__ __align__(16) uint32_t ht[HT::kWords];
   __shared__ uint32_t cand[kCandCap];
   __shared__ uint32_t beam[kMaxW];
   __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];

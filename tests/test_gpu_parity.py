@@ -177,6 +177,18 @@ def test_visited_filter_overflow_still_exact(orc, torch_dev):
     assert st["reevaluations"] > 0, "the test did not exercise the overflow path"
 
 
+def test_more_than_2_24_nodes_uses_the_32bit_table(orc, torch_dev):
+    """Above 2^24 nodes the resident kernel's 16-bit visited table cannot hold
+    every id; the 32-bit table takes over and results stay exact."""
+    rng = np.random.default_rng(31)
+    n, D, R = (1 << 24) + 4099, 4, 4
+    x = rng.integers(0, 256, (n, D), dtype=np.uint8)
+    graph = rng.integers(0, n, (n, R), dtype=np.uint32)
+    graph[:, 0] = (np.arange(n, dtype=np.uint64) * 2654435761 % n).astype(np.uint32)  # long jumps
+    q = rng.integers(0, 256, (64, D), dtype=np.uint8)
+    check_parity(orc, torch_dev, x, graph, q, 10, 64, 4, entry=n - 1)
+
+
 def test_host_pointers(orc, torch_dev):
     spec = IndexSpec(n=1000, D=32, dtype="u8", clusters=3, sigma=20.0, r_near=8, r_rand=8, seed=11)
     a = index_arrays(spec, use_cache=False)
