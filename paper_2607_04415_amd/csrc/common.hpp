@@ -205,17 +205,6 @@ struct VisitedLds16 {
     for (uint32_t i = lane_id(); i < kBuckets; i += kWave) t4[i] = make_uint4(0u, 0u, 0u, 0u);
   }
 
-  // Bits 15 and 31 of the result: the low / high half of w is zero.
-  __device__ __forceinline__ static uint32_t zero_halves(uint32_t w) {
-    return ~(((w & 0x7FFF7FFFu) + 0x7FFF7FFFu) | w | 0x7FFF7FFFu);
-  }
-  // Bit j set: half j (0..7, low half first) of bucket v equals e (e replicated in both halves).
-  __device__ __forceinline__ static uint32_t match8(const uint4 &v, uint32_t e2) {
-    const uint32_t a = zero_halves(v.x ^ e2), b = zero_halves(v.y ^ e2);
-    const uint32_t c = zero_halves(v.z ^ e2), d = zero_halves(v.w ^ e2);
-    return ((a >> 15) & 1u) | ((a >> 30) & 2u) | ((b >> 13) & 4u) | ((b >> 28) & 8u) |
-           ((c >> 11) & 16u) | ((c >> 26) & 32u) | ((d >> 9) & 64u) | ((d >> 24) & 128u);
-  }
   __device__ __forceinline__ static uint32_t word_of(const uint4 &v, uint32_t k) {
     return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
   }
@@ -270,15 +259,23 @@ struct VisitedLds16 {
         word[i] = expect[i] = want[i] = 0;
         if (!live[i]) continue;
         const uint32_t e = 1u + ((d[i] << 14) | r[i]);
-        const uint32_t hitm = match8(v[i], e | (e << 16));
-        const uint32_t emptym = match8(v[i], 0u);
-        const bool absent = pend[i] && hitm == 0 && emptym != 0;
-        const bool full = pend[i] && hitm == 0 && emptym == 0;
+        // slot k is half k & 1 of word k >> 1: one 16-bit compare per slot
+        const uint32_t wv[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+        bool hit = false;
+        uint32_t j = 8;
+#pragma unroll
+        for (int k = 7; k >= 0; --k) {
+          const uint32_t h = (k & 1) ? (wv[k >> 1] >> 16) : (wv[k >> 1] & 0xFFFFu);
+          hit = hit || h == e;
+          j = h == 0 ? (uint32_t)k : j;
+        }
+        const bool absent = pend[i] && !hit && j < 8;
+        const bool full = pend[i] && !hit && j == 8;
         const bool next = full && d[i] == 0;
         const bool lost = full && d[i] != 0;          // both buckets full: not recorded
         cas[i] = absent && may_store;
         isnew[i] = isnew[i] || (absent && !may_store) || lost;
-        const uint32_t j = (uint32_t)__builtin_ctz(emptym | 256u) & 7u;
+        j &= 7u;
         const uint32_t w = word_of(v[i], j >> 1);
         word[i] = ((home[i] + d[i]) & (kBuckets - 1)) * 4 + (j >> 1);
         expect[i] = w;
