@@ -23,11 +23,19 @@
  * in which page requests complete.
  *
  * Page layout: node v is stored at slot s = node_to_slot ? node_to_slot[v] : v,
- * in page s / records_per_page at byte (s % records_per_page) * record_bytes.
- * A record is [vector: D x uint8 or D x float32][uint32 degree]
- * [R x uint32 ids, padded with UINT32_MAX]; the bytes after the last record of
- * a page are zero.  A graph row's UINT32_MAX entries mean "no edge"; the record
- * keeps the row's other ids in order and degree = their count.
+ * position i = s % records_per_page of page s / records_per_page.  Its record
+ * is a vector (D x uint8 or D x float32) and an adjacency block ([uint32
+ * degree][R x uint32 ids, padded with UINT32_MAX]).  A graph row's UINT32_MAX
+ * entries mean "no edge"; the block keeps the row's other ids in order and
+ * degree = their count.  Inside a page (bytes not covered below are zero):
+ *   contiguous (default): record i at byte i * record_bytes, the adjacency
+ *     block right after the vector;
+ *   vectors first: vector i at byte i * V, where V = vector bytes rounded up
+ *     to 16, then adjacency block i at byte records_per_page * V +
+ *     i * (record_bytes - V).  For 128-byte vectors every vector starts on a
+ *     128-byte line, so a distance evaluation reads one line instead of two.
+ * Both layouts put the same nodes in the same pages; only the bytes inside a
+ * page move.
  *
  * Conventions for every call:
  *   - Status codes, never exceptions; gorio_last_error() returns a
@@ -64,8 +72,11 @@ typedef enum { GORIO_U8 = 0, GORIO_F32 = 1 } gorio_dtype;
 /* Node-record placement in pages.  Zero fields take the default. */
 typedef struct {
     uint32_t page_bytes;          /* page size; default 4096; multiple of 16 */
-    uint32_t record_bytes;        /* default vec_bytes + 4 + 4R; >= that, multiple of 4 */
+    uint32_t record_bytes;        /* bytes per node; default V + 4 + 4R with V = vec_bytes
+                                     (contiguous) or vec_bytes rounded up to 16 (vectors
+                                     first); >= that default's minimum, multiple of 4 */
     uint32_t records_per_page;    /* default page_bytes / record_bytes */
+    uint32_t vectors_first;       /* 0: contiguous records (default); 1: vectors first */
     const uint32_t *node_to_slot; /* host array of n entries, a permutation of [0, n); NULL = identity */
 } gorio_page_layout;
 
@@ -93,6 +104,7 @@ typedef struct {
     uint64_t n;
     uint32_t D, R;
     uint32_t page_bytes, record_bytes, records_per_page;
+    int vectors_first;         /* page layout (see above) */
     uint64_t num_pages;
     uint64_t index_bytes;      /* num_pages * page_bytes */
     uint32_t entry;            /* entry node used by every search */

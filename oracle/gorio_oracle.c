@@ -28,11 +28,16 @@
  *
  * Records are read through this file's own page decoder from pages this file
  * packed itself:  node v lives at slot s = node_to_slot ? node_to_slot[v] : v,
- * in page s / rpp at byte offset (s % rpp) * record_bytes; a record is
- *   [ vector: D bytes (uint8) or D little-endian float32 ]
- *   [ uint32 degree ]  [ R x uint32 neighbour ids, UINT32_MAX-padded ]
- * Page space after the last record is zero.  Records never straddle pages
- * (the paper's graph pages are block-granular 4 KB units, Sec. 3.1 and Fig. 1).
+ * position i = s % rpp of page s / rpp.  Its record is
+ *   vector:          D bytes (uint8) or D little-endian float32
+ *   adjacency block: [ uint32 degree ] [ R x uint32 neighbour ids, UINT32_MAX-padded ]
+ * placed inside the page in one of two arrangements (the paper fixes the
+ * block-granular 4 KB page as the unit, Sec. 3.1 and Fig. 1, and says nothing
+ * about the bytes inside it):
+ *   contiguous:    record i at byte i * record_bytes, vector then block;
+ *   vectors first: vector i at byte i * V (V = vector bytes rounded up to 16),
+ *                  block i at byte rpp * V + i * (record_bytes - V).
+ * Every byte not written is zero.  Records never straddle pages.
  *
  * Distances are squared L2, returned squared:
  *   uint8:  exact integer sum of (q_d - x_d)^2;
@@ -65,6 +70,7 @@ typedef struct {
     uint32_t records_per_page;
     const uint32_t *node_to_slot; /* NULL: slot = node id */
     uint32_t entry;
+    int32_t vectors_first;        /* page arrangement, see above */
 } orc_index;
 
 typedef struct {
@@ -78,9 +84,16 @@ static uint32_t vec_bytes(int32_t dtype, uint32_t D)
     return dtype == ORC_U8 ? D : 4u * D;
 }
 
-uint32_t orc_record_bytes(int32_t dtype, uint32_t D, uint32_t R)
+/* vector slot width in a vectors-first page */
+static uint32_t vec_slot(int32_t dtype, uint32_t D)
 {
-    return vec_bytes(dtype, D) + 4u + 4u * R;
+    return (vec_bytes(dtype, D) + 15u) / 16u * 16u;
+}
+
+/* smallest record for the arrangement */
+uint32_t orc_record_bytes(int32_t dtype, uint32_t D, uint32_t R, int32_t vectors_first)
+{
+    return (vectors_first ? vec_slot(dtype, D) : vec_bytes(dtype, D)) + 4u + 4u * R;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -117,12 +130,32 @@ static uint32_t float_bits(float f)
 /* ------------------------------------------------------------------------ */
 /* page packing and decoding                                                 */
 /* ------------------------------------------------------------------------ */
-static const uint8_t *record_of(const orc_index *ix, uint64_t v)
+static const uint8_t *page_of(const orc_index *ix, uint64_t v, uint64_t *pos)
 {
     uint64_t s = ix->node_to_slot ? ix->node_to_slot[v] : v;
-    uint64_t page = s / ix->records_per_page;
-    uint64_t off = (s % ix->records_per_page) * (uint64_t)ix->record_bytes;
-    return ix->pages + page * ix->page_bytes + off;
+    *pos = s % ix->records_per_page;
+    return ix->pages + (s / ix->records_per_page) * ix->page_bytes;
+}
+
+/* node v's vector */
+static const uint8_t *vector_of(const orc_index *ix, uint64_t v)
+{
+    uint64_t i;
+    const uint8_t *page = page_of(ix, v, &i);
+    if (ix->vectors_first) return page + i * vec_slot(ix->dtype, ix->D);
+    return page + i * ix->record_bytes;
+}
+
+/* node v's adjacency block: degree, then R ids */
+static const uint8_t *adjacency_of(const orc_index *ix, uint64_t v)
+{
+    uint64_t i;
+    const uint8_t *page = page_of(ix, v, &i);
+    if (ix->vectors_first) {
+        const uint64_t V = vec_slot(ix->dtype, ix->D);
+        return page + ix->records_per_page * V + i * (ix->record_bytes - V);
+    }
+    return page + i * ix->record_bytes + vec_bytes(ix->dtype, ix->D);
 }
 
 static uint32_t load_u32(const uint8_t *p)
@@ -151,10 +184,12 @@ uint64_t orc_num_pages(uint64_t n, uint32_t records_per_page)
 int orc_pack(int32_t dtype, const void *vectors, uint64_t n, uint32_t D,
              const uint32_t *graph, uint32_t R,
              uint32_t page_bytes, uint32_t record_bytes, uint32_t records_per_page,
-             const uint32_t *node_to_slot, uint8_t *pages_out)
+             const uint32_t *node_to_slot, int32_t vectors_first, uint8_t *pages_out)
 {
     if ((dtype != ORC_U8 && dtype != ORC_F32) || n == 0 || D == 0 || R == 0) return ORC_EINVAL;
-    if (records_per_page == 0 || record_bytes < orc_record_bytes(dtype, D, R)) return ORC_EINVAL;
+    if (vectors_first != 0 && vectors_first != 1) return ORC_EINVAL;
+    if (records_per_page == 0 || record_bytes < orc_record_bytes(dtype, D, R, vectors_first))
+        return ORC_EINVAL;
     if ((uint64_t)record_bytes * records_per_page > page_bytes) return ORC_EINVAL;
     if (n >= 0x80000000ull) return ORC_EINVAL;
     for (uint64_t i = 0; i < n * R; ++i)
@@ -169,19 +204,19 @@ int orc_pack(int32_t dtype, const void *vectors, uint64_t n, uint32_t D,
         free(seen);
     }
     orc_index ix = { pages_out, n, D, R, dtype, page_bytes, record_bytes, records_per_page,
-                     node_to_slot, 0 };
+                     node_to_slot, 0, vectors_first };
     memset(pages_out, 0, orc_num_pages(n, records_per_page) * (uint64_t)page_bytes);
     const uint32_t vb = vec_bytes(dtype, D);
     for (uint64_t v = 0; v < n; ++v) {
-        uint8_t *rec = (uint8_t *)record_of(&ix, v);
-        memcpy(rec, (const uint8_t *)vectors + v * vb, vb);
+        memcpy((uint8_t *)vector_of(&ix, v), (const uint8_t *)vectors + v * vb, vb);
+        uint8_t *adj = (uint8_t *)adjacency_of(&ix, v);
         uint32_t deg = 0;
         for (uint32_t j = 0; j < R; ++j) {
             uint32_t u = graph[v * R + j];
-            if (u != ORC_NO_EDGE) store_u32(rec + vb + 4 + 4 * deg++, u);
+            if (u != ORC_NO_EDGE) store_u32(adj + 4 + 4 * deg++, u);
         }
-        for (uint32_t j = deg; j < R; ++j) store_u32(rec + vb + 4 + 4 * j, ORC_NO_EDGE);
-        store_u32(rec + vb, deg);
+        for (uint32_t j = deg; j < R; ++j) store_u32(adj + 4 + 4 * j, ORC_NO_EDGE);
+        store_u32(adj, deg);
     }
     return ORC_OK;
 }
@@ -248,7 +283,7 @@ typedef struct {
 
 static uint64_t key_of(const orc_index *ix, const void *q, uint32_t v)
 {
-    const uint8_t *rec = record_of(ix, v);
+    const uint8_t *rec = vector_of(ix, v);
     uint32_t dbits;
     if (ix->dtype == ORC_U8) {
         dbits = orc_dist_u8((const uint8_t *)q, rec, ix->D);
@@ -328,7 +363,7 @@ static int search_one(const orc_index *ix, workspace *w, const void *q,
             w->in_x[u] = 1;
             if (trace && nx < trace_cap) trace[nx] = u;
             ++nx;
-            const uint8_t *adj = record_of(ix, u) + vec_bytes(ix->dtype, ix->D);
+            const uint8_t *adj = adjacency_of(ix, u);
             uint32_t deg = load_u32(adj);
             if (deg > ix->R) deg = ix->R;
             for (uint32_t j = 0; j < deg; ++j) {

@@ -37,7 +37,7 @@ class _Index(ctypes.Structure):
                 ("R", ctypes.c_uint32), ("dtype", ctypes.c_int32),
                 ("page_bytes", ctypes.c_uint32), ("record_bytes", ctypes.c_uint32),
                 ("records_per_page", ctypes.c_uint32), ("node_to_slot", ctypes.c_void_p),
-                ("entry", ctypes.c_uint32)]
+                ("entry", ctypes.c_uint32), ("vectors_first", ctypes.c_int32)]
 
 
 class _Counts(ctypes.Structure):
@@ -60,7 +60,7 @@ class Oracle:
         lib = ctypes.CDLL(str(path))
         v, u32, u64, i32 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32
         lib.orc_record_bytes.restype = u32
-        lib.orc_record_bytes.argtypes = [i32, u32, u32]
+        lib.orc_record_bytes.argtypes = [i32, u32, u32, i32]
         lib.orc_num_pages.restype = u64
         lib.orc_num_pages.argtypes = [u64, u32]
         lib.orc_dist_u8.restype = u32
@@ -68,7 +68,7 @@ class Oracle:
         lib.orc_dist_f32.restype = ctypes.c_float
         lib.orc_dist_f32.argtypes = [v, v, u32]
         lib.orc_pack.restype = ctypes.c_int
-        lib.orc_pack.argtypes = [i32, v, u64, u32, v, u32, u32, u32, u32, v, v]
+        lib.orc_pack.argtypes = [i32, v, u64, u32, v, u32, u32, u32, u32, v, i32, v]
         lib.orc_medoid.restype = u32
         lib.orc_medoid.argtypes = [i32, v, u64, u32]
         lib.orc_search.restype = ctypes.c_int
@@ -86,8 +86,8 @@ class Oracle:
             return F32
         raise TypeError(f"unsupported vector dtype {x.dtype}")
 
-    def record_bytes(self, dtype: int, D: int, R: int) -> int:
-        return int(self.lib.orc_record_bytes(dtype, D, R))
+    def record_bytes(self, dtype: int, D: int, R: int, vectors_first: bool = False) -> int:
+        return int(self.lib.orc_record_bytes(dtype, D, R, int(bool(vectors_first))))
 
     def dist(self, a: np.ndarray, b: np.ndarray):
         a = np.ascontiguousarray(a)
@@ -102,35 +102,37 @@ class Oracle:
 
     def pack(self, x: np.ndarray, graph: np.ndarray, page_bytes: int = 4096,
              record_bytes: int | None = None, records_per_page: int | None = None,
-             node_to_slot: np.ndarray | None = None) -> "PackedIndex":
+             node_to_slot: np.ndarray | None = None, vectors_first: bool = False) -> "PackedIndex":
         x = np.ascontiguousarray(x)
         graph = np.ascontiguousarray(graph, dtype=np.uint32)
         n, D = x.shape
         R = graph.shape[1]
         dt = self.dtype_code(x)
-        rb = record_bytes or self.record_bytes(dt, D, R)
+        vf = int(bool(vectors_first))
+        rb = record_bytes or self.record_bytes(dt, D, R, vf)
         rpp = records_per_page or page_bytes // rb
         if node_to_slot is not None:
             node_to_slot = np.ascontiguousarray(node_to_slot, dtype=np.uint32)
         npages = int(self.lib.orc_num_pages(n, max(rpp, 1)))
         pages = np.zeros(npages * page_bytes, np.uint8)
         rc = self.lib.orc_pack(dt, x.ctypes.data, n, D, graph.ctypes.data, R, page_bytes, rb,
-                               rpp, _ptr(node_to_slot), pages.ctypes.data)
+                               rpp, _ptr(node_to_slot), vf, pages.ctypes.data)
         if rc != 0:
             raise ValueError(f"orc_pack: {ERRORS.get(rc, rc)}")
-        return PackedIndex(self, pages, n, D, R, dt, page_bytes, rb, rpp, node_to_slot)
+        return PackedIndex(self, pages, n, D, R, dt, page_bytes, rb, rpp, node_to_slot, vf)
 
 
 class PackedIndex:
     def __init__(self, orc: Oracle, pages, n, D, R, dtype, page_bytes, record_bytes, rpp,
-                 node_to_slot):
+                 node_to_slot, vectors_first=0):
         self.orc, self.pages, self.n, self.D, self.R = orc, pages, n, D, R
         self.dtype, self.page_bytes, self.record_bytes, self.rpp = dtype, page_bytes, record_bytes, rpp
         self.node_to_slot = node_to_slot
+        self.vectors_first = vectors_first
 
     def _struct(self, entry: int) -> _Index:
         return _Index(self.pages.ctypes.data, self.n, self.D, self.R, self.dtype, self.page_bytes,
-                      self.record_bytes, self.rpp, _ptr(self.node_to_slot), entry)
+                      self.record_bytes, self.rpp, _ptr(self.node_to_slot), entry, self.vectors_first)
 
     def search(self, queries: np.ndarray, k: int, L: int, W: int, entry: int,
                threads: int = 1, debug: bool = False, trace_cap: int = 0):

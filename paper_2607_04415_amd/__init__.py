@@ -28,7 +28,8 @@ class GorioError(RuntimeError):
 
 class PageLayout(ctypes.Structure):
     _fields_ = [("page_bytes", ctypes.c_uint32), ("record_bytes", ctypes.c_uint32),
-                ("records_per_page", ctypes.c_uint32), ("node_to_slot", ctypes.c_void_p)]
+                ("records_per_page", ctypes.c_uint32), ("vectors_first", ctypes.c_uint32),
+                ("node_to_slot", ctypes.c_void_p)]
 
 
 class Stats(ctypes.Structure):
@@ -45,7 +46,7 @@ class IndexInfo(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int), ("n", ctypes.c_uint64), ("D", ctypes.c_uint32),
                 ("R", ctypes.c_uint32), ("page_bytes", ctypes.c_uint32),
                 ("record_bytes", ctypes.c_uint32), ("records_per_page", ctypes.c_uint32),
-                ("num_pages", ctypes.c_uint64), ("index_bytes", ctypes.c_uint64),
+                ("vectors_first", ctypes.c_int), ("num_pages", ctypes.c_uint64), ("index_bytes", ctypes.c_uint64),
                 ("entry", ctypes.c_uint32), ("resident", ctypes.c_int),
                 ("cache_slots", ctypes.c_uint64), ("device", ctypes.c_int)]
 
@@ -109,7 +110,8 @@ class Index:
 
     def __init__(self, vectors: np.ndarray, graph: np.ndarray, page_bytes: int = 0,
                  record_bytes: int = 0, records_per_page: int = 0,
-                 node_to_slot: np.ndarray | None = None, entry: int | None = None):
+                 node_to_slot: np.ndarray | None = None, entry: int | None = None,
+                 vectors_first: bool = False):
         vectors = np.ascontiguousarray(vectors)
         graph = np.ascontiguousarray(graph, dtype=np.uint32)
         if vectors.dtype == np.uint8:
@@ -122,7 +124,8 @@ class Index:
         if graph.shape[0] != n:
             raise ValueError("graph must have one row per vector")
         self._n2s = None if node_to_slot is None else np.ascontiguousarray(node_to_slot, np.uint32)
-        layout = PageLayout(page_bytes, record_bytes, records_per_page, _ptr(self._n2s))
+        layout = PageLayout(page_bytes, record_bytes, records_per_page, int(bool(vectors_first)),
+                            _ptr(self._n2s))
         h = ctypes.c_void_p()
         _check(lib().gorio_build_index(self.dtype, vectors.ctypes.data, n, D, graph.ctypes.data,
                                        graph.shape[1], ctypes.byref(layout),

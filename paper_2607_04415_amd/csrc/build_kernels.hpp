@@ -34,13 +34,12 @@ __global__ __launch_bounds__(256) void pack_records(const uint8_t *vectors, uint
   const int l = lane_id();
   const uint32_t waves = gridDim.x * (blockDim.x / kWave);
   for (uint32_t v = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; v < n; v += waves) {
-    uint32_t page, off;
-    locate(geom, v, page, off);
-    uint8_t *rec = pages + page * geom.page_bytes + off;
+    const uint32_t s = slot_of(geom, v);
     const uint32_t *src = reinterpret_cast<const uint32_t *>(vectors + (uint64_t)v * vec_bytes);
-    uint32_t *dst = reinterpret_cast<uint32_t *>(rec);
+    uint32_t *dst = reinterpret_cast<uint32_t *>(pages + vec_offset(geom, s));
     for (uint32_t w = l; w < vec_bytes / 4; w += kWave) dst[w] = src[w];
-    uint32_t *ids = reinterpret_cast<uint32_t *>(rec + vec_bytes + 4);
+    uint8_t *adj = pages + adj_offset(geom, s);
+    uint32_t *ids = reinterpret_cast<uint32_t *>(adj + 4);
     uint32_t deg = 0;
     for (uint32_t j0 = 0; j0 < R; j0 += kWave) {
       uint32_t j = j0 + l;
@@ -52,7 +51,7 @@ __global__ __launch_bounds__(256) void pack_records(const uint8_t *vectors, uint
       deg += (uint32_t)__popcll(m);
     }
     for (uint32_t j = deg + l; j < R; j += kWave) ids[j] = kNoEdge;
-    if (l == 0) *reinterpret_cast<uint32_t *>(rec + vec_bytes) = deg;
+    if (l == 0) *reinterpret_cast<uint32_t *>(adj) = deg;
   }
 }
 

@@ -36,11 +36,20 @@ __host__ __device__ __forceinline__ uint32_t fastdiv(uint32_t x, FastDiv f) {
   return (uint32_t)(((uint64_t)x * f.mul) >> f.shift);
 }
 
-// Where records sit inside the packed page array.
+// Where a node's vector and adjacency block (degree, ids) sit inside the
+// packed page array.  Slot s is position i = s % rpp of page s / rpp:
+//   vector    at page * page_bytes + i * vec_stride
+//   adjacency at page * page_bytes + adj_base + i * adj_stride
+// Contiguous records: vec_stride = adj_stride = record_bytes, adj_base =
+// vec_bytes.  Vectors first: vec_stride = vec_bytes rounded up to 16,
+// adj_base = rpp * vec_stride, adj_stride = record_bytes - vec_stride.
 struct PageGeom {
   uint64_t page_bytes;
   uint32_t record_bytes;
-  uint32_t vec_bytes;      // vector bytes at the start of a record
+  uint32_t vec_bytes;
+  uint32_t vec_stride;
+  uint32_t adj_base;
+  uint32_t adj_stride;
   FastDiv rpp;             // records per page
   const uint32_t *node_to_slot;  // nullptr: slot = node id
 };
@@ -49,11 +58,10 @@ __device__ __forceinline__ uint32_t slot_of(const PageGeom &g, uint32_t v) {
   return g.node_to_slot ? g.node_to_slot[v] : v;
 }
 
-// Page index and byte offset inside that page of node v's record.
-__device__ __forceinline__ void locate(const PageGeom &g, uint32_t v, uint32_t &page, uint32_t &off) {
-  uint32_t s = slot_of(g, v);
+// Page of slot s and its position inside the page.
+__device__ __forceinline__ void locate(const PageGeom &g, uint32_t s, uint32_t &page, uint32_t &pos) {
   page = fastdiv(s, g.rpp);
-  off = (s - page * g.rpp.d) * g.record_bytes;
+  pos = s - page * g.rpp.d;
 }
 
 // Slot of node v when the caller knows at compile time whether a placement
@@ -65,10 +73,16 @@ __device__ __forceinline__ uint32_t slot_ct(const PageGeom &g, uint32_t v) {
   else return v;
 }
 
-// Byte offset of slot s's record in the packed page array.
-__device__ __forceinline__ uint64_t record_offset(const PageGeom &g, uint32_t s) {
-  const uint32_t page = fastdiv(s, g.rpp);
-  return (uint64_t)page * g.page_bytes + (uint64_t)((s - page * g.rpp.d) * g.record_bytes);
+// Byte offsets of slot s's vector and adjacency block in the packed page array.
+__device__ __forceinline__ uint64_t vec_offset(const PageGeom &g, uint32_t s) {
+  uint32_t page, pos;
+  locate(g, s, page, pos);
+  return (uint64_t)page * g.page_bytes + (uint64_t)(pos * g.vec_stride);
+}
+__device__ __forceinline__ uint64_t adj_offset(const PageGeom &g, uint32_t s) {
+  uint32_t page, pos;
+  locate(g, s, page, pos);
+  return (uint64_t)page * g.page_bytes + (uint64_t)(g.adj_base + pos * g.adj_stride);
 }
 
 // ---------------------------------------------------------------------------

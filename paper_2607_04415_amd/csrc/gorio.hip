@@ -107,7 +107,10 @@ extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors
   if (entry != UINT32_MAX && entry >= n) return fail(GORIO_EINVAL, "entry %u >= n", entry);
 
   const uint32_t vb = vec_bytes_of(dtype, D);
-  const uint32_t min_rec = vb + 4 + 4 * R;
+  const bool vfirst = layout && layout->vectors_first;
+  if (layout && layout->vectors_first > 1) return fail(GORIO_EINVAL, "vectors_first must be 0 or 1");
+  // vectors first: each vector slot is rounded up to 16 bytes
+  const uint32_t min_rec = (vfirst ? ((vb + 15u) & ~15u) : vb) + 4 + 4 * R;
   uint32_t page_bytes = layout && layout->page_bytes ? layout->page_bytes : 4096;
   uint32_t rec_bytes = layout && layout->record_bytes ? layout->record_bytes : min_rec;
   if (page_bytes % 16 != 0) return fail(GORIO_EINVAL, "page_bytes=%u is not a multiple of 16", page_bytes);
@@ -130,6 +133,7 @@ extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors
   ix->page_bytes = page_bytes;
   ix->rec_bytes = rec_bytes;
   ix->rpp = rpp;
+  ix->vectors_first = vfirst;
   ix->num_pages = (n + rpp - 1) / rpp;
 
   HIP_OR_FAIL(hipStreamCreateWithFlags(&ix->stream, hipStreamNonBlocking));
@@ -542,6 +546,7 @@ extern "C" gorio_status gorio_index_info_get(const gorio_index *ix, gorio_index_
   info->page_bytes = ix->page_bytes;
   info->record_bytes = ix->rec_bytes;
   info->records_per_page = ix->rpp;
+  info->vectors_first = ix->vectors_first ? 1 : 0;
   info->num_pages = ix->num_pages;
   info->index_bytes = ix->index_bytes();
   info->entry = ix->entry;

@@ -93,6 +93,7 @@ struct gorio_index {
   uint64_t n = 0;
   uint32_t D = 0, R = 0, vec_bytes = 0;
   uint32_t page_bytes = 4096, rec_bytes = 0, rpp = 0;
+  bool vectors_first = false;   // page layout: all vectors of a page, then all adjacency blocks
   uint64_t num_pages = 0;
   uint32_t entry = 0;
   uint32_t *d_node_to_slot = nullptr;
@@ -120,6 +121,15 @@ struct gorio_index {
     g.page_bytes = page_bytes;
     g.record_bytes = rec_bytes;
     g.vec_bytes = vec_bytes;
+    if (vectors_first) {
+      g.vec_stride = (vec_bytes + 15u) & ~15u;
+      g.adj_base = rpp * g.vec_stride;
+      g.adj_stride = rec_bytes - g.vec_stride;
+    } else {
+      g.vec_stride = rec_bytes;
+      g.adj_base = vec_bytes;
+      g.adj_stride = rec_bytes;
+    }
     g.rpp = gorio::make_fastdiv(rpp);
     g.node_to_slot = d_node_to_slot;
     return g;

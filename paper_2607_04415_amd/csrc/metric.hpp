@@ -68,7 +68,7 @@ struct MetricU8 {
     for (int rr = 0; rr < kRounds; ++rr) {
       if (c0 + rr * 8 >= cnt) break;
       const uint32_t idx = c0 + rr * 8 + g;
-      rec[rr] = record_offset(geom, slot_ct<N2S>(geom, idx < cnt ? cand[idx] : fallback));
+      rec[rr] = vec_offset(geom, slot_ct<N2S>(geom, idx < cnt ? cand[idx] : fallback));
     }
     U8Vec<VDW, EXACT> x[kRounds];
 #pragma unroll
@@ -241,7 +241,7 @@ struct MetricF32 {
                                                 uint64_t (&key)[kChunks]) const {
     const uint32_t idx = c0 + lane_id();
     const uint32_t node = idx < cnt ? cand[idx] : fallback;
-    const float d = dist_global(pages + record_offset(geom, slot_ct<N2S>(geom, node)));
+    const float d = dist_global(pages + vec_offset(geom, slot_ct<N2S>(geom, node)));
     key[0] = idx < cnt ? (((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)node << 1)) : kInfKey;
   }
 

@@ -37,7 +37,7 @@ enum : uint32_t { kPhSelect = 0, kPhExpand = 1, kPhEval = 2 };
 
 struct PagedParams {
   CacheView cache;
-  PageGeom geom;  // record geometry inside a page (page_bytes, record_bytes, rpp, node_to_slot)
+  PageGeom geom;  // where vectors and adjacency blocks sit inside a page
   uint32_t n, D, R;
   FastDiv Rdiv;
   uint32_t entry;
@@ -85,12 +85,18 @@ __device__ __forceinline__ bool aborted(const PagedParams &p) {
   return __hip_atomic_load(p.abort_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
 }
 
-// Byte offset of node v's record inside cache slot s.
+// Byte offsets of node v's vector and adjacency block inside cache slot s.
 template <bool N2S>
-__device__ __forceinline__ uint32_t cached_record(const PagedParams &p, uint32_t s, uint32_t v) {
-  const uint32_t sl = slot_ct<N2S>(p.geom, v);
-  const uint32_t within = sl - fastdiv(sl, p.geom.rpp) * p.geom.rpp.d;
-  return s * (uint32_t)p.cache.page_bytes + within * p.geom.record_bytes;
+__device__ __forceinline__ uint32_t cached_vec(const PagedParams &p, uint32_t s, uint32_t v) {
+  uint32_t page, pos;
+  locate(p.geom, slot_ct<N2S>(p.geom, v), page, pos);
+  return s * (uint32_t)p.cache.page_bytes + pos * p.geom.vec_stride;
+}
+template <bool N2S>
+__device__ __forceinline__ uint32_t cached_adj(const PagedParams &p, uint32_t s, uint32_t v) {
+  uint32_t page, pos;
+  locate(p.geom, slot_ct<N2S>(p.geom, v), page, pos);
+  return s * (uint32_t)p.cache.page_bytes + p.geom.adj_base + pos * p.geom.adj_stride;
 }
 
 template <bool N2S>
@@ -342,7 +348,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
           rmask &= rmask - 1;
           const uint32_t s_b = readlane(slot, b);
           const uint32_t u = S.beam[S.b0 + b];
-          const uint32_t adj = cached_record<N2S>(p, s_b, u) + p.geom.vec_bytes;
+          const uint32_t adj = cached_adj<N2S>(p, s_b, u);
           const uint32_t deg = min(coherent_load_u32(crs, adj), p.R);
           for (uint32_t j0 = 0; j0 < p.R; j0 += kCandCap) {
             uint32_t ids[kIdsPerLane];
@@ -436,7 +442,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
           const uint64_t mr = ballot(rdy[t]);
           if (mr == 0) continue;
           const uint32_t cnt = (uint32_t)__popcll(mr);
-          uint64_t key = m.paged_keys([&](uint32_t si, uint32_t v) { return cached_record<N2S>(p, si, v); }, crs,
+          uint64_t key = m.paged_keys([&](uint32_t si, uint32_t v) { return cached_vec<N2S>(p, si, v); }, crs,
                                       S.cand, t * kWave, rdy[t], rslot[t], mr);
           ctr.eval += cnt;
           const uint64_t thr = frontier_at<KPL>(F, p.L - 1);

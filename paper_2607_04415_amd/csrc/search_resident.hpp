@@ -72,7 +72,7 @@ __global__ __launch_bounds__(kWave, 2) void search_resident(ResidentParams p) {
 #pragma unroll
     for (int r = 0; r < KPL; ++r) F[r] = kInfKey;
     {
-      const uint32_t d = m.dist_one(p.pages + record_offset(p.geom, slot_ct<N2S>(p.geom, p.entry)));
+      const uint32_t d = m.dist_one(p.pages + vec_offset(p.geom, slot_ct<N2S>(p.geom, p.entry)));
       if (l == 0) {
         F[0] = ((uint64_t)d << 32) | ((uint64_t)p.entry << 1);
         bool rec;
@@ -111,8 +111,8 @@ __global__ __launch_bounds__(kWave, 2) void search_resident(ResidentParams p) {
         // Loads are unconditional (lanes past the group read the group's first
         // record) so that no branch separates them: one round trip in total.
         const uint32_t my_beam = beam[b0 + min((uint32_t)l, nb - 1)];
-        const uint64_t my_rec = record_offset(p.geom, slot_ct<N2S>(p.geom, my_beam));
-        const uint32_t my_deg = *reinterpret_cast<const uint32_t *>(p.pages + my_rec + p.geom.vec_bytes);
+        const uint64_t my_adj = adj_offset(p.geom, slot_ct<N2S>(p.geom, my_beam));
+        const uint32_t my_deg = *reinterpret_cast<const uint32_t *>(p.pages + my_adj);
         uint32_t ids[kIdsPerLane];
         uint32_t slot_beam[kIdsPerLane], slot_j[kIdsPerLane];
 #pragma unroll
@@ -124,8 +124,8 @@ __global__ __launch_bounds__(kWave, 2) void search_resident(ResidentParams p) {
         }
 #pragma unroll
         for (int t = 0; t < kIdsPerLane; ++t) {
-          const uint64_t rec = __shfl(my_rec, (int)slot_beam[t]);
-          ids[t] = reinterpret_cast<const uint32_t *>(p.pages + rec + p.geom.vec_bytes + 4)[slot_j[t]];
+          const uint64_t adj = __shfl(my_adj, (int)slot_beam[t]);
+          ids[t] = reinterpret_cast<const uint32_t *>(p.pages + adj + 4)[slot_j[t]];
         }
         bool valid[kIdsPerLane];
 #pragma unroll

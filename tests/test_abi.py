@@ -36,9 +36,9 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_struct_sizes_match_header():
-    # gorio_stats: 2 doubles + 11 uint64; gorio_page_layout: 3 uint32 + pointer
+    # gorio_stats: 2 doubles + 11 uint64; gorio_page_layout: 4 uint32 + pointer
     assert ctypes.sizeof(g.Stats) == 2 * 8 + 11 * 8
-    assert ctypes.sizeof(g.PageLayout) == 3 * 4 + 4 + 8
+    assert ctypes.sizeof(g.PageLayout) == 4 * 4 + 8
 
 
 def _build(lib, dtype=0, n=10, D=8, R=4, layout=None, entry=g.NO_EDGE, vectors=True, graph=True):
@@ -55,10 +55,12 @@ def _build(lib, dtype=0, n=10, D=8, R=4, layout=None, entry=g.NO_EDGE, vectors=T
 @pytest.mark.parametrize("kw", [
     dict(dtype=7), dict(n=0), dict(n=1 << 31), dict(R=0), dict(R=257), dict(D=0), dict(D=6),
     dict(D=516), dict(dtype=1, D=257), dict(entry=10), dict(vectors=False), dict(graph=False),
-    dict(layout=g.PageLayout(4100, 0, 0, None)),           # page size not a multiple of 16
-    dict(layout=g.PageLayout(4096, 10, 0, None)),          # record smaller than its contents
-    dict(layout=g.PageLayout(4096, 26, 0, None)),          # record not a multiple of 4
-    dict(layout=g.PageLayout(4096, 0, 1000, None)),        # too many records per page
+    dict(layout=g.PageLayout(4100, 0, 0, 0, None)),        # page size not a multiple of 16
+    dict(layout=g.PageLayout(4096, 10, 0, 0, None)),       # record smaller than its contents
+    dict(layout=g.PageLayout(4096, 26, 0, 0, None)),       # record not a multiple of 4
+    dict(layout=g.PageLayout(4096, 0, 1000, 0, None)),     # too many records per page
+    dict(layout=g.PageLayout(4096, 0, 0, 2, None)),        # unknown layout
+    dict(D=4, R=4, layout=g.PageLayout(4096, 24, 0, 1, None)),  # vectors first: 16 + 4 + 16 > 24
 ])
 def test_build_rejects_bad_arguments(lib, kw):
     st, h = _build(lib, **kw)

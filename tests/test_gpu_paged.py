@@ -48,12 +48,13 @@ def assert_same(gi, gd, oids, od):
     assert bad.size == 0, f"{bad.size} queries differ, first {bad[:5]}"
 
 
-@pytest.mark.parametrize("frac,latency,oversub,blocking", [
-    (0.10, 0.0, 1, 0), (0.10, 20.0, 4, 0), (0.30, 0.0, 2, 0), (0.10, 0.0, 1, 1), (0.50, 5.0, 8, 0),
-], ids=["c10-l0-o1", "c10-l20-o4", "c30-l0-o2", "c10-l0-blocking", "c50-l5-o8"])
-def test_paged_matches_oracle(torch_dev, small, frac, latency, oversub, blocking):
+@pytest.mark.parametrize("frac,latency,oversub,blocking,vfirst", [
+    (0.10, 0.0, 1, 0, 0), (0.10, 20.0, 4, 0, 0), (0.30, 0.0, 2, 0, 0), (0.10, 0.0, 1, 1, 0),
+    (0.50, 5.0, 8, 0, 0), (0.10, 20.0, 4, 0, 1),
+], ids=["c10-l0-o1", "c10-l20-o4", "c30-l0-o2", "c10-l0-blocking", "c50-l5-o8", "c10-l20-o4-vfirst"])
+def test_paged_matches_oracle(torch_dev, small, frac, latency, oversub, blocking, vfirst):
     a, q, oids, od, oc = small
-    ix = g.Index(a["x"], a["graph"])
+    ix = g.Index(a["x"], a["graph"], vectors_first=bool(vfirst))
     info = ix.info
     ix.set_cache(max(int(frac * info["index_bytes"]), 128 * 4096))
     ix.set_backing(latency_us=latency, oversub=oversub, blocking=bool(blocking))
@@ -185,7 +186,7 @@ def small_f32(orc):
 ], ids=["c5-l20-o4", "c10-l0-blocking", "c30-l5-o8"])
 def test_paged_f32_matches_oracle(torch_dev, small_f32, frac, latency, oversub, blocking):
     a, q, oids, od, oc = small_f32
-    ix = g.Index(a["x"], a["graph"])
+    ix = g.Index(a["x"], a["graph"], vectors_first=blocking == 0 and oversub == 8)
     ix.set_cache(max(int(frac * ix.info["index_bytes"]), 128 * 4096))
     ix.set_backing(latency_us=latency, oversub=oversub, blocking=bool(blocking))
     gi, gd, st = search(torch_dev, ix, q, 10, 128, 8)

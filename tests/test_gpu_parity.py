@@ -127,7 +127,8 @@ def test_parity_random_graph_with_missing_edges(orc, torch_dev):
 @pytest.mark.parametrize("layout", [
     dict(node_to_slot="perm"), dict(record_bytes=400), dict(records_per_page=3),
     dict(page_bytes=8192), dict(page_bytes=16),
-], ids=["perm", "rec400", "rpp3", "page8k", "page16-tiny"])
+    dict(vectors_first=True), dict(vectors_first=True, node_to_slot="perm", record_bytes=420),
+], ids=["perm", "rec400", "rpp3", "page8k", "page16-tiny", "vfirst", "vfirst-perm-rec420"])
 def test_parity_layouts(orc, torch_dev, layout):
     rng = np.random.default_rng(2)
     n, D, R = 2000, 128, 64
@@ -137,7 +138,7 @@ def test_parity_layouts(orc, torch_dev, layout):
     spec = IndexSpec(n=n, D=D, dtype="u8", clusters=4, sigma=20.0, r_near=R // 2, r_rand=R // 2, seed=5)
     a = index_arrays(spec, use_cache=False)
     if layout.get("node_to_slot") == "perm":
-        layout = dict(node_to_slot=rng.permutation(n).astype(np.uint32))
+        layout = dict(layout, node_to_slot=rng.permutation(n).astype(np.uint32))
     q = query_array(spec, QuerySpec(150, 3))
     ix, _ = check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 48, 4, layout=layout)
     okw = {kk: v for kk, v in layout.items() if v is not None and not (np.isscalar(v) and v == 0)}
@@ -239,7 +240,7 @@ def test_parity_f32_layout_perm_and_wide_records(orc, torch_dev):
     a = index_arrays(spec, use_cache=False)
     q = query_array(spec, QuerySpec(200, 23))
     for layout in (dict(node_to_slot=rng.permutation(2500).astype(np.uint32)), dict(record_bytes=700),
-                   dict(page_bytes=8192, records_per_page=5)):
+                   dict(page_bytes=8192, records_per_page=5), dict(vectors_first=True)):
         check_parity(orc, torch_dev, a["x"], a["graph"], q, 10, 128, 8, layout=layout)
 
 

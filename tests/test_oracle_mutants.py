@@ -38,8 +38,11 @@ MUTANTS = {
     "no_visited_check": (
         "if (v >= ix->n || w->in_v[v]) continue;", "if (v >= ix->n) continue;"),
     "pack_does_not_compact": (
-        "if (u != ORC_NO_EDGE) store_u32(rec + vb + 4 + 4 * deg++, u);",
-        "store_u32(rec + vb + 4 + 4 * j, u); if (u != ORC_NO_EDGE) deg++;"),
+        "if (u != ORC_NO_EDGE) store_u32(adj + 4 + 4 * deg++, u);",
+        "store_u32(adj + 4 + 4 * j, u); if (u != ORC_NO_EDGE) deg++;"),
+    "vectors_first_unpadded_block_base": (
+        "return page + ix->records_per_page * V + i * (ix->record_bytes - V);",
+        "return page + ix->records_per_page * vec_bytes(ix->dtype, ix->D) + i * (ix->record_bytes - V);"),
     "insert_keeps_stale_flag": (
         "f[p].expanded = 0;", ""),
 }

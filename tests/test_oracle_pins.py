@@ -136,18 +136,28 @@ def test_medoid_f32_closed_form(orc):
 # --------------------------------------------------------------------------- #
 # packing: an independent numpy decoder reads the oracle's pages
 # --------------------------------------------------------------------------- #
-def _decode(pages, n, D, R, vec_dtype, rec_bytes, rpp, page_bytes=4096, node_to_slot=None):
+def _decode(pages, n, D, R, vec_dtype, rec_bytes, rpp, page_bytes=4096, node_to_slot=None,
+            vectors_first=False):
+    """Reads the layout as the header documents it: contiguous records, or the
+    page's vectors (each padded to a multiple of 16 bytes) followed by its
+    adjacency blocks."""
     vb = D * np.dtype(vec_dtype).itemsize
+    V = -(-vb // 16) * 16
     xs = np.empty((n, D), vec_dtype)
     deg = np.empty(n, np.uint32)
     ids = np.empty((n, R), np.uint32)
     for v in range(n):
         s = v if node_to_slot is None else int(node_to_slot[v])
-        off = (s // rpp) * page_bytes + (s % rpp) * rec_bytes
-        rec = pages[off:off + rec_bytes]
-        xs[v] = rec[:vb].view(vec_dtype)
-        deg[v] = rec[vb:vb + 4].view("<u4")[0]
-        ids[v] = rec[vb + 4:vb + 4 + 4 * R].view("<u4")
+        page, i = (s // rpp) * page_bytes, s % rpp
+        if vectors_first:
+            vec_at = page + i * V
+            adj_at = page + rpp * V + i * (rec_bytes - V)
+        else:
+            vec_at = page + i * rec_bytes
+            adj_at = vec_at + vb
+        xs[v] = pages[vec_at:vec_at + vb].view(vec_dtype)
+        deg[v] = pages[adj_at:adj_at + 4].view("<u4")[0]
+        ids[v] = pages[adj_at + 4:adj_at + 4 + 4 * R].view("<u4")
     return xs, deg, ids
 
 
@@ -160,18 +170,21 @@ def test_pack_roundtrip(orc, dtype):
     g = random_graph(rng, n, R, sentinel_frac=0.3)
     perm = rng.permutation(n).astype(np.uint32)
     for node_to_slot in (None, perm):
-        ix = orc.pack(x, g, node_to_slot=node_to_slot)
-        xs, deg, ids = _decode(ix.pages, n, D, R, x.dtype, ix.record_bytes, ix.rpp,
-                               node_to_slot=node_to_slot)
-        assert np.array_equal(xs, x)
-        for v in range(n):
-            real = [e for e in g[v] if e != NO_EDGE]
-            assert deg[v] == len(real)
-            assert ids[v].tolist() == real + [NO_EDGE] * (R - len(real))
-        # unused page tail is zero
-        used = ix.rpp * ix.record_bytes
-        pg = ix.pages.reshape(-1, 4096)
-        assert not pg[:, used:].any()
+        for vf in (False, True):
+            ix = orc.pack(x, g, node_to_slot=node_to_slot, vectors_first=vf)
+            vb = D * x.dtype.itemsize
+            assert ix.record_bytes == (-(-vb // 16) * 16 if vf else vb) + 4 + 4 * R
+            xs, deg, ids = _decode(ix.pages, n, D, R, x.dtype, ix.record_bytes, ix.rpp,
+                                   node_to_slot=node_to_slot, vectors_first=vf)
+            assert np.array_equal(xs, x)
+            for v in range(n):
+                real = [e for e in g[v] if e != NO_EDGE]
+                assert deg[v] == len(real)
+                assert ids[v].tolist() == real + [NO_EDGE] * (R - len(real))
+            # unused page tail is zero
+            used = ix.rpp * ix.record_bytes
+            pg = ix.pages.reshape(-1, 4096)
+            assert not pg[:, used:].any()
 
 
 def test_pack_rejects(orc):
@@ -187,6 +200,8 @@ def test_pack_rejects(orc):
         orc.pack(x, g, record_bytes=40, records_per_page=200)
     with pytest.raises(ValueError):                    # not a permutation
         orc.pack(x, g, node_to_slot=np.zeros(20, np.uint32))
+    with pytest.raises(ValueError):                    # vectors first: 16 + 4 + 16 bytes needed
+        orc.pack(x, g, record_bytes=28, vectors_first=True)
 
 
 # --------------------------------------------------------------------------- #
@@ -357,7 +372,9 @@ def test_layout_invariance(orc):
     for kw in (dict(node_to_slot=rng.permutation(n).astype(np.uint32)),
                dict(record_bytes=rb + 12),
                dict(records_per_page=3),
-               dict(page_bytes=8192)):
+               dict(page_bytes=8192),
+               dict(vectors_first=True),
+               dict(vectors_first=True, records_per_page=5, node_to_slot=rng.permutation(n).astype(np.uint32))):
         got = orc.pack(x, g, **kw).search(qs, 10, 32, 4, e)
         for a, b in zip(ref[:3], got[:3]):
             assert np.array_equal(a, b)
