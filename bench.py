@@ -28,6 +28,8 @@ sys.path.insert(0, str(ROOT))
 
 METRIC = "queries/sec at k=10 (oracle-exact) + achieved HBM GB/s and miss-service GB/s"
 HBM_PEAK_GBS = 8000.0
+# page layouts (both put the same nodes in the same 4 KB pages; see include/gorio.h)
+LAYOUTS = ("vectors-first", "contiguous")
 PROFILES = ROOT / "profiles"
 KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp", "paper_2607_04415_amd/csrc/frontier.hpp",
                   "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
@@ -44,9 +46,9 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, layout: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
+    was taken on the current kernel source and page layout; else None."""
     f = PROFILES / f"traffic_{workload}.json"
     if not f.exists():
         return None
@@ -54,7 +56,7 @@ def measured_traffic(workload: str):
         t = json.loads(f.read_text())
     except ValueError:
         return None
-    if t.get("kernel_source_hash") != kernel_source_hash():
+    if t.get("kernel_source_hash") != kernel_source_hash() or t.get("layout") != layout:
         return None
     return t.get("hbm_bytes_per_launch")
 
@@ -93,11 +95,12 @@ def host_link_peak_gbs(torch) -> float:
     return best
 
 
-def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: bool = False):
+def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: bool = False,
+              vectors_first: bool = False):
     """One cold-cache paged search over the first nq_sample queries of workload w."""
     from workload import query_array
     q = query_array(w.index, w.queries)[:nq_sample]
-    ix = g.Index(a["x"], a["graph"])
+    ix = g.Index(a["x"], a["graph"], vectors_first=vectors_first)
     ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))      # empty cache
     ix.set_backing(latency_us=w.latency_us, oversub=1 if blocking else w.oversub, blocking=blocking)
     qd = torch.from_numpy(q).cuda()
@@ -131,6 +134,10 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="u8-1m-hbm")
+    ap.add_argument("--layout", choices=LAYOUTS, default="vectors-first",
+                    help="page layout of the timed index (the other one is timed too and reported)")
+    ap.add_argument("--no-other-layout", action="store_true",
+                    help="do not time the other page layout")
     ap.add_argument("--cpu-sample", type=int, default=10000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -169,31 +176,46 @@ def main():
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
     log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f} s")
-    ix = g.Index(a["x"], a["graph"])
-    info = ix.info
-    if w.cache_frac < 1.0:
-        ix.set_cache(int(w.cache_frac * info["index_bytes"]))
-        ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
     qd = torch.from_numpy(q).cuda()
     nq = len(q)
-    ids = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
-    dists = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
-    stream = torch.cuda.current_stream().cuda_stream
-    for _ in range(args.warmup):
-        ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
-    torch.cuda.synchronize()
-    kernel_ms, stats = [], []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        st = ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
-        kernel_ms.append(st["kernel_ms"])
-        stats.append(st)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+
+    def timed(layout: str):
+        """Build the index in `layout`, run the warm-up and the timed steps."""
+        ix = g.Index(a["x"], a["graph"], vectors_first=layout == "vectors-first")
+        info = ix.info
+        if w.cache_frac < 1.0:
+            ix.set_cache(int(w.cache_frac * info["index_bytes"]))
+            ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
+        ids = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
+        dists = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
+        stream = torch.cuda.current_stream().cuda_stream
+        for _ in range(args.warmup):
+            ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
+        kernel_ms, stats = [], []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            st = ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
+            kernel_ms.append(st["kernel_ms"])
+            stats.append(st)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        ix.close()
+        log(f"[bench] {layout}: {args.steps} steps: {elapsed * 1e3 / args.steps:.3f} ms/step, "
+            f"{nq * args.steps / elapsed:,.0f} queries/s")
+        return info, elapsed, kernel_ms, stats, ids, dists
+
+    info, elapsed, kernel_ms, stats, ids, dists = timed(args.layout)
     ms_per_step = elapsed * 1e3 / args.steps
     qps = nq * args.steps / elapsed
-    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, {qps:,.0f} queries/s")
+    other = None
+    if not args.no_other_layout:
+        o_layout = [x for x in LAYOUTS if x != args.layout][0]
+        _, o_el, o_kms, _, o_ids, o_d = timed(o_layout)
+        other = {"layout": o_layout, "value": round(nq * args.steps / o_el, 1),
+                 "ms_per_step": round(o_el * 1e3 / args.steps, 4),
+                 "kernel_ms_avg": round(float(np.mean(o_kms)), 4),
+                 "same_answers": bool(torch.equal(o_ids, ids) and torch.equal(o_d, dists))}
 
     st = stats[-1]
     R = info["R"]
@@ -202,11 +224,11 @@ def main():
     alg_bytes = st["expansions"] * (4 + 4 * R) + first_evals * vec_bytes
     avg_kernel_ms = float(np.mean(kernel_ms))
     achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
-    traffic = measured_traffic(w.name)
+    traffic = measured_traffic(w.name, args.layout)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
-                "kernel": "search_resident_u8", "kernel_ms_avg": round(avg_kernel_ms, 4),
+                "kernel": "search_resident<MetricU8>", "kernel_ms_avg": round(avg_kernel_ms, 4),
                 "algorithmic_bytes_per_launch": int(alg_bytes)}
 
     gi = ids.cpu().numpy().view(np.uint32)
@@ -227,7 +249,8 @@ def main():
         legs = []
         for name, blocking in (("u8-1m-cache10-lat0", False), ("u8-1m-cache10-lat0", True),
                                ("u8-1m-cache10-lat20", False)):
-            leg, pi, pd, pq = paged_leg(torch, g, a, WORKLOADS[name], args.paged_sample, qps, blocking)
+            leg, pi, pd, pq = paged_leg(torch, g, a, WORKLOADS[name], args.paged_sample, qps, blocking,
+                                        vectors_first=args.layout == "vectors-first")
             # the paged results must equal the resident results on the same queries
             if WORKLOADS[name].queries == w.queries:
                 leg["equals_resident"] = bool(np.array_equal(pi, gi[:len(pq)]) and np.array_equal(pd, gd[:len(pq)]))
@@ -244,13 +267,14 @@ def main():
         af = index_arrays(wf.index)
         qf = query_array(wf.index, wf.queries)[:args.f32_sample]
         # the same queries on the HBM-resident index: the reference answers and rate
-        ixr = g.Index(af["x"], af["graph"])
+        ixr = g.Index(af["x"], af["graph"], vectors_first=args.layout == "vectors-first")
         ri, rd, rst = ixr.search(torch.from_numpy(qf).cuda(), wf.k, wf.L, wf.W)
         torch.cuda.synchronize()
         ri, rd = ri.cpu().numpy().view(np.uint32), rd.cpu().numpy()
         rqps = len(qf) / (rst["kernel_ms"] * 1e-3)
         ixr.close()
-        leg, pi, pd, _ = paged_leg(torch, g, af, wf, args.f32_sample, rqps)
+        leg, pi, pd, _ = paged_leg(torch, g, af, wf, args.f32_sample, rqps,
+                                   vectors_first=args.layout == "vectors-first")
         leg["resident_kernel_qps"] = round(rqps, 1)
         leg["equals_resident"] = bool(np.array_equal(pi, ri) and np.array_equal(pd.view(np.uint32), rd.view(np.uint32)))
         log(f"[bench] paged {wf.name}: {leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, "
@@ -267,8 +291,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.index.n, "D": w.index.D, "R": R, "nq": nq,
                    "k": w.k, "L": w.L, "W": w.W, "record_bytes": info["record_bytes"],
-                   "records_per_page": info["records_per_page"], "cache_frac": w.cache_frac,
-                   "resident": bool(info["resident"])},
+                   "records_per_page": info["records_per_page"], "page_layout": args.layout,
+                   "cache_frac": w.cache_frac, "resident": bool(info["resident"])},
+        "other_layout": other,
         "oracle_exact": exact,
         "achieved_hbm_gbs": roofline["achieved"],
         "miss_service_gbs": miss_gbs,
