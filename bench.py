@@ -32,6 +32,7 @@ HBM_PEAK_GBS = 8000.0
 LAYOUTS = ("vectors-first", "contiguous")
 PROFILES = ROOT / "profiles"
 KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp", "paper_2607_04415_amd/csrc/frontier.hpp",
+                  "paper_2607_04415_amd/csrc/metric.hpp", "paper_2607_04415_amd/csrc/launch.hpp",
                   "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
 
 
