@@ -38,17 +38,17 @@ struct U8Vec {
   }
 };
 
-// Partial of sum (x.x - 2 q.x) over this lane's dwords.
+// Partial of sum (x.x - 2 q.x) over this lane's dwords (both dot products
+// accumulate through v_dot4_u32_u8's addend; no overflow: VDW * 4 * 255^2 < 2^31).
 template <int VDW, bool EXACT>
 __device__ __forceinline__ int partial_u8(const U8Vec<VDW, EXACT> &q, const U8Vec<VDW, EXACT> &x) {
-  int s = 0;
+  uint32_t xx = 0, qx = 0;
 #pragma unroll
   for (int t = 0; t < VDW; ++t) {
-    uint32_t xx = __builtin_amdgcn_udot4(x.w[t], x.w[t], 0u, false);
-    uint32_t qx = __builtin_amdgcn_udot4(q.w[t], x.w[t], 0u, false);
-    s += (int)xx - 2 * (int)qx;
+    xx = __builtin_amdgcn_udot4(x.w[t], x.w[t], xx, false);
+    qx = __builtin_amdgcn_udot4(q.w[t], x.w[t], qx, false);
   }
-  return s;
+  return (int)xx - 2 * (int)qx;
 }
 
 __device__ __forceinline__ uint32_t key_id(uint64_t key) { return (uint32_t)(key >> 1) & 0x7FFFFFFFu; }

@@ -29,6 +29,7 @@ struct MetricU8 {
   static constexpr int kRounds = VDW <= 4 ? 16 : 8;
   static constexpr int kBatch = kRounds * 8;
   static constexpr int kChunks = kBatch / kWave;
+  static_assert(kRounds % 8 == 0, "rounds are reduced eight at a time");
   static constexpr int kQueryWords = 1;          // the query lives in registers
   static constexpr uint32_t kPadDist = 0x7FFFFFFFu;  // INT32_MAX
 
@@ -76,14 +77,16 @@ struct MetricU8 {
       if (c0 + rr * 8 >= cnt) break;
       x[rr].load(pages + rec[rr], gl, dwords);
     }
+    // eight rounds at a time: lane gl of group g ends with round 8c + gl's distance
     int dist[kChunks];
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) dist[c] = 0;
+    for (int c = 0; c < kChunks; ++c) {
+      dist[c] = 0;
+      if (c0 + c * kWave >= cnt) break;
+      int part[8];
 #pragma unroll
-    for (int rr = 0; rr < kRounds; ++rr) {
-      if (c0 + rr * 8 >= cnt) break;
-      const int d = sum8(partial_u8(q, x[rr])) + qq;
-      if (gl == (rr & 7)) dist[rr / 8] = d;
+      for (int j = 0; j < 8; ++j) part[j] = c0 + (c * 8 + j) * 8 < cnt ? partial_u8(q, x[c * 8 + j]) : 0;
+      dist[c] = transpose_sum8(part) + qq;
     }
     // lane l of chunk c holds candidate c0 + 64c + 8*(l%8) + l/8
 #pragma unroll
@@ -120,12 +123,10 @@ struct MetricU8 {
       const uint32_t si = idx < cnt ? rs[idx] : rs[0];
       load_cached_u8(x[rr], crs, off_of(si, cand[ci]), gl);
     }
-    int mine_d = 0;
+    int part[8];
 #pragma unroll
-    for (int rr = 0; rr < 8; ++rr) {
-      const int d = sum8(partial_u8(q, x[rr])) + qq;
-      if (gl == rr) mine_d = d;
-    }
+    for (int rr = 0; rr < 8; ++rr) part[rr] = partial_u8(q, x[rr]);
+    const int mine_d = transpose_sum8(part) + qq;
     const uint32_t my_idx = gl * 8 + g;
     uint64_t key = kInfKey;
     if (my_idx < cnt) key = ((uint64_t)(uint32_t)mine_d << 32) | ((uint64_t)cand[rc[my_idx]] << 1);

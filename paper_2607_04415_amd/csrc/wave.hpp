@@ -71,6 +71,32 @@ __device__ __forceinline__ int sum8(int v) {
   return v;
 }
 
+// Eight rounds of per-group partials reduced at once: v[j] is this lane's
+// partial of round j; every group of 8 lanes sums each round, and lane gl of
+// the group receives round gl's total.  Three butterfly stages; at each, a
+// lane keeps the half of its rounds whose index bit matches its own lane bit
+// and adds the partner's other half (partner = the lane with that bit
+// flipped: row_half_mirror for bit 2, quad_perm for bits 1 and 0).  21
+// instructions for 8 totals instead of 8 sum8 calls and 8 selects.
+__device__ __forceinline__ int transpose_sum8(const int (&v)[8]) {
+  const int gl = lane_id() & 7;
+  const bool b2 = gl & 4, b1 = gl & 2, b0 = gl & 1;
+  int w[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int keep = b2 ? v[j + 4] : v[j], send = b2 ? v[j] : v[j + 4];
+    w[j] = keep + __builtin_amdgcn_update_dpp(0, send, 0x141, 0xF, 0xF, false);
+  }
+  int u[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int keep = b1 ? w[j + 2] : w[j], send = b1 ? w[j] : w[j + 2];
+    u[j] = keep + __builtin_amdgcn_update_dpp(0, send, 0x4E, 0xF, 0xF, false);
+  }
+  const int keep = b0 ? u[1] : u[0], send = b0 ? u[0] : u[1];
+  return keep + __builtin_amdgcn_update_dpp(0, send, 0xB1, 0xF, 0xF, false);
+}
+
 // Sum over the whole wave, result in every lane (used off the hot path).
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   for (int m = 1; m < kWave; m <<= 1) v += shfl_xor64(v, m);
