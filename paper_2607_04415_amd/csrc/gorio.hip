@@ -407,7 +407,11 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.blocking = ix->blocking;
   pp.stats = rp.stats;
 
-  P.proxy.begin(ix->latency_us, ix->max_outstanding, rings);
+  // test hooks: random extra delay per request (completions leave out of
+  // order) and a proxy that never completes (the watchdog must end the search)
+  const char *jit = getenv("GORIO_PROXY_JITTER_US");
+  P.proxy.begin(ix->latency_us, ix->max_outstanding, rings, jit ? atof(jit) : 0.0,
+                env_int("GORIO_PROXY_HOLD", 0) != 0);
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
   const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, grid, s) : launch_paged_u8(pp, grid, s);
   if (le != hipSuccess) {

@@ -3,6 +3,8 @@
 
 #include <chrono>
 #include <deque>
+#include <functional>
+#include <queue>
 #include <utility>
 #include <vector>
 
@@ -37,9 +39,11 @@ void Proxy::start(unsigned long long *mq, uint32_t mq_mask, unsigned long long *
   th_ = std::thread([this] { loop(); });
 }
 
-void Proxy::begin(double latency_us, uint32_t max_outstanding, uint32_t rings) {
+void Proxy::begin(double latency_us, uint32_t max_outstanding, uint32_t rings, double jitter_us, bool hold) {
   rings_.store(rings ? rings : 1);
   latency_ns_.store((uint64_t)(latency_us * 1000.0));
+  jitter_ns_.store(jitter_us > 0.0 ? (uint64_t)(jitter_us * 1000.0) : 0);
+  hold_.store(hold);
   max_outstanding_.store(max_outstanding ? max_outstanding : 4096);
   requests_.store(0);
   completed_.store(0);
@@ -66,6 +70,10 @@ void Proxy::loop() {
   // (descriptor, due time); latency is the same for every request, so FIFO
   // order is deadline order
   std::deque<std::pair<unsigned long long, uint64_t>> fifo;
+  // with jitter, requests leave by due time: (due time, descriptor), earliest first
+  using Due = std::pair<uint64_t, unsigned long long>;
+  std::priority_queue<Due, std::vector<Due>, std::greater<Due>> heap;
+  uint64_t rng = 0x9E3779B97F4A7C15ull;  // SplitMix64 state for the jitter draws
   std::vector<uint64_t> tails;  // completions published per ring
   uint64_t head = 0, dealt = 0, epoch = ~0ull;
   uint32_t rings = 1;
@@ -80,14 +88,17 @@ void Proxy::loop() {
     if (epoch != epoch_.load()) {  // a new search: rings were reset by the host
       epoch = epoch_.load();
       fifo.clear();
+      heap = decltype(heap)();
       rings = rings_.load();
       tails.assign(rings, 0);
       head = dealt = 0;
     }
     const uint64_t lat = latency_ns_.load(std::memory_order_relaxed);
+    const uint64_t jitter = jitter_ns_.load(std::memory_order_relaxed);
+    const bool hold = hold_.load(std::memory_order_relaxed);
     const uint32_t cap = max_outstanding_.load(std::memory_order_relaxed);
     uint32_t intake = 0;
-    while (fifo.size() < cap) {
+    while (fifo.size() + heap.size() < cap) {
       unsigned long long *slot = &mq_[head & mq_mask_];
       const unsigned long long e = __atomic_load_n(slot, __ATOMIC_ACQUIRE);
       if (e == 0) break;
@@ -100,16 +111,33 @@ void Proxy::loop() {
     // published plus the latency
     const uint64_t now = now_ns();
     for (size_t i = fifo.size() - intake; i < fifo.size(); ++i) fifo[i].second = now + lat;
+    if (jitter) {  // move the new requests into the due-time heap with their random delay
+      while (!fifo.empty()) {
+        uint64_t z = (rng += 0x9E3779B97F4A7C15ull);
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        z ^= z >> 31;
+        heap.emplace(fifo.front().second + z % (jitter + 1), fifo.front().first);
+        fifo.pop_front();
+      }
+    }
+    const size_t in_flight = fifo.size() + heap.size();
     if (intake) {
       requests_.fetch_add(intake, std::memory_order_relaxed);
-      if (fifo.size() > max_in_flight_.load(std::memory_order_relaxed))
-        max_in_flight_.store(fifo.size(), std::memory_order_relaxed);
+      if (in_flight > max_in_flight_.load(std::memory_order_relaxed))
+        max_in_flight_.store(in_flight, std::memory_order_relaxed);
     }
     uint32_t done = 0;
-    while (!fifo.empty() && fifo.front().second <= now) {
+    while (!hold && !fifo.empty() && fifo.front().second <= now) {
       const uint32_t r = (uint32_t)(dealt++ % rings);
       cq_[(uint64_t)r * (cq_mask_ + 1) + (tails[r]++ & cq_mask_)] = fifo.front().first;
       fifo.pop_front();
+      ++done;
+    }
+    while (!hold && !heap.empty() && heap.top().first <= now) {
+      const uint32_t r = (uint32_t)(dealt++ % rings);
+      cq_[(uint64_t)r * (cq_mask_ + 1) + (tails[r]++ & cq_mask_)] = heap.top().second;
+      heap.pop();
       ++done;
     }
     if (done) {

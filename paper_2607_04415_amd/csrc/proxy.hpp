@@ -30,7 +30,11 @@ class Proxy {
              unsigned long long *cq_tail, uint32_t tail_stride);
   // Reset ring indices and counters for a new search and begin serving over
   // `rings` completion rings (the caller has zeroed their tails).
-  void begin(double latency_us, uint32_t max_outstanding, uint32_t rings);
+  // Fault injection for tests: jitter_us adds a uniform random delay in
+  // [0, jitter_us] to each request, so completions leave out of request
+  // order; hold keeps every request in flight (none completes).
+  void begin(double latency_us, uint32_t max_outstanding, uint32_t rings, double jitter_us = 0.0,
+             bool hold = false);
   // Stop serving (the search ended); descriptors in flight are dropped.
   void end();
   void stop();
@@ -47,7 +51,8 @@ class Proxy {
   std::atomic<uint32_t> rings_{1};
   std::atomic<bool> quit_{false}, active_{false}, idle_{true};
   std::atomic<uint64_t> epoch_{0};
-  std::atomic<uint64_t> latency_ns_{0};
+  std::atomic<uint64_t> latency_ns_{0}, jitter_ns_{0};
+  std::atomic<bool> hold_{false};
   std::atomic<uint32_t> max_outstanding_{4096};
   std::atomic<uint64_t> requests_{0}, completed_{0}, max_in_flight_{0};
   std::thread th_;

@@ -3,7 +3,7 @@
 // exactly once, never before its injected latency, and that the proxy never
 // holds more requests than its cap.  Prints one JSON line with the result.
 //
-//   proxy_harness <requests> <latency_us> <max_outstanding> <slots> <producers> <rings>
+//   proxy_harness <requests> <latency_us> <max_outstanding> <slots> <producers> <rings> <jitter_us>
 //
 // With several completion rings, one consumer thread per ring plays the GPU
 // fill wave that owns that ring.
@@ -31,6 +31,7 @@ int main(int argc, char **argv) {
   const uint32_t slots = argc > 4 ? (uint32_t)atoi(argv[4]) : 10000;
   const int producers = argc > 5 ? atoi(argv[5]) : 4;
   const uint32_t rings = argc > 6 ? (uint32_t)atoi(argv[6]) : 1;
+  const double jitter_us = argc > 7 ? atof(argv[7]) : 0.0;
   const uint32_t tail_stride = 8;  // tails on separate 64-byte lines
 
   uint32_t ring = 1;
@@ -40,7 +41,7 @@ int main(int argc, char **argv) {
 
   gorio::Proxy proxy;
   proxy.start(mq.data(), ring - 1, cq.data(), ring - 1, cq_tail.data(), tail_stride);
-  proxy.begin(latency_us, cap, rings);
+  proxy.begin(latency_us, cap, rings, jitter_us);
 
   // slot s is "LOADING" while in flight; a producer may only use a free slot,
   // as the GPU may only publish a descriptor for a slot it claimed
@@ -49,7 +50,7 @@ int main(int argc, char **argv) {
   std::vector<std::atomic<uint32_t>> done_count(requests);
   for (auto &b : busy) b.store(0);
   for (auto &d : done_count) d.store(0);
-  std::atomic<uint64_t> next_req{0}, mq_tail{0}, completed{0}, early{0}, bad{0};
+  std::atomic<uint64_t> next_req{0}, mq_tail{0}, completed{0}, early{0}, bad{0}, reordered{0};
 
   auto producer = [&](int id) {
     uint32_t s = (uint32_t)id;
@@ -70,7 +71,7 @@ int main(int argc, char **argv) {
   };
 
   auto consumer = [&](uint32_t r0) {
-    uint64_t head = 0;
+    uint64_t head = 0, last_issue = 0;
     const unsigned long long *q = cq.data() + (size_t)r0 * ring;
     while (completed.load() < requests) {
       const uint64_t t = __atomic_load_n(&cq_tail[(size_t)r0 * tail_stride], __ATOMIC_ACQUIRE);
@@ -79,7 +80,11 @@ int main(int argc, char **argv) {
         const uint64_t r = (e >> 32) - 1;
         const uint32_t s = (uint32_t)e;
         if (r >= requests || s >= slots) { bad.fetch_add(1); continue; }
-        const uint64_t waited = now_ns() - issued_at[s].load(std::memory_order_relaxed);
+        const uint64_t at = issued_at[s].load(std::memory_order_relaxed);
+        // completed well before a request issued earlier on this ring
+        if (at + 20000 < last_issue) reordered.fetch_add(1);
+        last_issue = at > last_issue ? at : last_issue;
+        const uint64_t waited = now_ns() - at;
         if (waited + 2000 < (uint64_t)(latency_us * 1000.0)) early.fetch_add(1);
         done_count[r].fetch_add(1);
         busy[s].store(0);  // the fill made the slot READY; it can be reused
@@ -107,9 +112,10 @@ int main(int argc, char **argv) {
     if (c > 1) ++twice;
   }
   printf("{\"requests\": %llu, \"seconds\": %.4f, \"per_second\": %.0f, \"missing\": %llu, "
-         "\"duplicated\": %llu, \"early\": %llu, \"bad\": %llu, \"max_in_flight\": %llu, \"cap\": %u}\n",
+         "\"duplicated\": %llu, \"early\": %llu, \"bad\": %llu, \"max_in_flight\": %llu, \"cap\": %u, "
+         "\"reordered\": %llu}\n",
          (unsigned long long)requests, secs, requests / secs, (unsigned long long)missing,
          (unsigned long long)twice, (unsigned long long)early.load(), (unsigned long long)bad.load(),
-         (unsigned long long)proxy.max_in_flight(), cap);
+         (unsigned long long)proxy.max_in_flight(), cap, (unsigned long long)reordered.load());
   return (missing || twice || early.load() || bad.load() || proxy.max_in_flight() > cap) ? 1 : 0;
 }

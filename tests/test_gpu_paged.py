@@ -151,6 +151,38 @@ def test_watchdog_abort_then_recover(torch_dev, small, monkeypatch):
     assert_same(gi, gd, oids, od)
 
 
+def test_reordered_completions_same_answers(torch_dev, small, monkeypatch):
+    """The proxy adds a random 0-100 us delay per request, so pages arrive out
+    of request order; the answers do not change."""
+    a, q, oids, od, oc = small
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(max(int(0.10 * ix.info["index_bytes"]), 128 * 4096))
+    ix.set_backing(latency_us=5.0, oversub=4)
+    monkeypatch.setenv("GORIO_PROXY_JITTER_US", "100")
+    gi, gd, st = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+
+
+def test_held_proxy_trips_watchdog_then_recovers(torch_dev, small, monkeypatch):
+    """A proxy that never completes: the kernel ends at the watchdog with
+    GORIO_ETIMEOUT instead of hanging, and the next search is normal."""
+    a, q, oids, od, _ = small
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_cache(300 * 4096)
+    ix.set_backing(latency_us=0.0)
+    monkeypatch.setenv("GORIO_PROXY_HOLD", "1")
+    monkeypatch.setenv("GORIO_WATCHDOG_S", "1")
+    with pytest.raises(g.GorioError) as e:
+        search(torch_dev, ix, q, 10, 32, 4)
+    assert e.value.status == g.ETIMEOUT
+    assert e.value.stats["pages_served"] == 0
+    monkeypatch.delenv("GORIO_PROXY_HOLD")
+    monkeypatch.delenv("GORIO_WATCHDOG_S")
+    gi, gd, _ = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+
+
 def test_paged_1m_index_slice(orc, torch_dev):
     """The 1M-vector index with a 10% cache, on the first 2,000 queries."""
     w = WORKLOADS["u8-1m-cache10-lat0"]

@@ -37,6 +37,15 @@ def test_proxy_exactly_once_latency_cap(tmp_path, latency, cap, rings):
     assert r["max_in_flight"] <= cap
 
 
+def test_proxy_jitter_reorders_and_stays_exactly_once(tmp_path):
+    exe = build(tmp_path)
+    r = run(exe, 50000, 10.0, 4096, 10000, 4, 4, 200.0)
+    assert r["missing"] == 0 and r["duplicated"] == 0 and r["early"] == 0 and r["bad"] == 0
+    assert r["reordered"] > 0, "jitter did not reorder any completion"
+    r0 = run(exe, 50000, 10.0, 4096, 10000, 4, 1, 0.0)
+    assert r0["missing"] == 0 and r0["duplicated"] == 0
+
+
 def test_proxy_under_thread_sanitizer(tmp_path):
     exe = build(tmp_path, sanitize=True)
     r = run(exe, 20000, 5.0, 1024, 2000, 3, 4, timeout=300)
