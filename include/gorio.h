@@ -179,6 +179,23 @@ gorio_status gorio_index_info_get(const gorio_index *ix, gorio_index_info *info)
  */
 gorio_status gorio_copy_pages(const gorio_index *ix, uint64_t first, uint64_t count, void *dst);
 
+/*
+ * Locality-aware node placement (host only; no device is touched): fills
+ * node_to_slot (n entries, a permutation of [0, n)) so that graph neighbours
+ * share pages, for use as gorio_page_layout.node_to_slot.  Graph pages are the
+ * unit of I/O (Sec. 3.1); the disk-resident ANNS work the paper builds on
+ * places neighbours together for this reason (Sec. 6).  Rule: visit nodes
+ * breadth-first from `entry`, neighbours in adjacency order; a visited node
+ * without a slot takes the next slot and then fills the rest of its page
+ * (records_per_page slots) with its own slot-less neighbours, in adjacency
+ * order; unreached nodes follow in id order.  Deterministic.
+ *   graph: host, n x R row-major; UINT32_MAX = no edge; other ids must be < n.
+ * Errors: GORIO_EINVAL for NULL pointers, n, R or records_per_page out of range,
+ * entry >= n or a bad id.
+ */
+gorio_status gorio_locality_order(const uint32_t *graph, uint64_t n, uint32_t R, uint32_t entry,
+                                  uint32_t records_per_page, uint32_t *node_to_slot);
+
 /* Release everything the index owns.  NULL is a no-op. */
 void gorio_free_index(gorio_index *ix);
 

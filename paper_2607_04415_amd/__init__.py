@@ -56,7 +56,8 @@ class IndexInfo(ctypes.Structure):
 
 # every symbol include/gorio.h declares
 EXPORTS = ("gorio_build_index", "gorio_set_cache", "gorio_set_backing", "gorio_search",
-           "gorio_index_info_get", "gorio_copy_pages", "gorio_free_index", "gorio_last_error")
+           "gorio_index_info_get", "gorio_copy_pages", "gorio_locality_order", "gorio_free_index",
+           "gorio_last_error")
 
 _lib = None
 
@@ -83,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.gorio_index_info_get.argtypes = [v, ctypes.POINTER(IndexInfo)]
         L.gorio_copy_pages.restype = i32
         L.gorio_copy_pages.argtypes = [v, u64, u64, v]
+        L.gorio_locality_order.restype = i32
+        L.gorio_locality_order.argtypes = [v, u64, u32, u32, u32, v]
         L.gorio_free_index.restype = None
         L.gorio_free_index.argtypes = [v]
         L.gorio_last_error.restype = ctypes.c_char_p
@@ -103,6 +106,15 @@ def _ptr(a):
     if isinstance(a, np.ndarray):
         return a.ctypes.data
     return a.data_ptr()
+
+
+def locality_order(graph: np.ndarray, entry: int, records_per_page: int) -> np.ndarray:
+    """node_to_slot placing graph neighbours in the same pages (gorio_locality_order)."""
+    graph = np.ascontiguousarray(graph, dtype=np.uint32)
+    out = np.empty(graph.shape[0], np.uint32)
+    _check(lib().gorio_locality_order(graph.ctypes.data, graph.shape[0], graph.shape[1], int(entry),
+                                      int(records_per_page), out.ctypes.data))
+    return out
 
 
 class Index:
