@@ -343,7 +343,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   // waves that only copy arriving pages, each from a completion ring of its
   // own, so the fill rate does not depend on how many queries run at once
   // and no two waves contend for completions
-  const int fwaves = std::max(0, std::min((int)PagedState::kMaxRings, env_int("GORIO_FILL_WAVES", 16)));
+  const int fwaves = std::max(0, std::min((int)PagedState::kMaxRings, env_int("GORIO_FILL_WAVES", 32)));
   const uint32_t rings = (uint32_t)std::max(1, fwaves);
   const int grid = qwaves + fwaves;
   const uint64_t ht_entries = (uint64_t)qwaves * oversub << kPagedHtLog2;
