@@ -151,6 +151,42 @@ def test_watchdog_abort_then_recover(torch_dev, small, monkeypatch):
     assert_same(gi, gd, oids, od)
 
 
+@pytest.mark.parametrize("layout", [
+    dict(page_bytes=8192), dict(page_bytes=2048), dict(node_to_slot="perm"),
+    dict(node_to_slot="perm", vectors_first=True, page_bytes=8192),
+], ids=["page8k", "page2k", "perm", "perm-vfirst-page8k"])
+def test_paged_layouts(orc, torch_dev, layout):
+    """Pages other than 4 KB take the generic copy path; a placement
+    permutation takes the node-to-slot branch of every cache address."""
+    a = index_arrays(SPEC, use_cache=False)
+    q = query_array(SPEC, QuerySpec(200, 49))
+    if layout.get("node_to_slot") == "perm":
+        layout = dict(layout, node_to_slot=np.random.default_rng(50).permutation(SPEC.n).astype(np.uint32))
+    ix = g.Index(a["x"], a["graph"], **layout)
+    e = ix.info["entry"]
+    oids, od, _, _ = orc.pack(a["x"], a["graph"], **layout).search(q, 10, 32, 4, e, threads=8)
+    ix.set_cache(max(int(0.10 * ix.info["index_bytes"]), 128 * ix.info["page_bytes"]))
+    ix.set_backing(latency_us=5.0, oversub=4)
+    gi, gd, st = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    assert st["bytes_served"] == st["pages_served"] * ix.info["page_bytes"]
+
+
+def test_paged_widest_beam(orc, torch_dev):
+    """L = 256 (four frontier slots per lane) and W = 64, the paged kernel's limit."""
+    spec = IndexSpec(n=8000, D=32, dtype="u8", clusters=4, sigma=20.0, r_near=24, r_rand=24, seed=51)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(64, 52))
+    ix = g.Index(a["x"], a["graph"])
+    e = ix.info["entry"]
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"]).search(q, 100, 256, 64, e, threads=8)
+    ix.set_cache(max(int(0.2 * ix.info["index_bytes"]), 256 * 4096))
+    ix.set_backing(latency_us=2.0, oversub=2)
+    gi, gd, st = search(torch_dev, ix, q, 100, 256, 64)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+
+
 def test_reordered_completions_same_answers(torch_dev, small, monkeypatch):
     """The proxy adds a random 0-100 us delay per request, so pages arrive out
     of request order; the answers do not change."""

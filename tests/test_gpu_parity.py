@@ -190,6 +190,24 @@ def test_more_than_2_24_nodes_uses_the_32bit_table(orc, torch_dev):
     check_parity(orc, torch_dev, x, graph, q, 10, 64, 4, entry=n - 1)
 
 
+def test_single_node_and_widest_rows(orc, torch_dev):
+    # one node, no edges: the answer is that node, then padding
+    x1 = np.array([[7, 8, 9, 10]], np.uint8)
+    g1 = np.full((1, 3), NO_EDGE, np.uint32)
+    ix = g.Index(x1, g1)
+    gi, gd, st = run_gpu(torch_dev, ix, np.array([[7, 8, 9, 11]], np.uint8), 4, 8, 2)
+    assert gi[0].tolist() == [0, NO_EDGE, NO_EDGE, NO_EDGE]
+    assert gd[0].tolist() == [1, 2 ** 31 - 1, 2 ** 31 - 1, 2 ** 31 - 1]
+    assert st["expansions"] == 1 and st["evaluations"] == 1
+    # R = 256, the widest adjacency list
+    rng = np.random.default_rng(33)
+    n, D, R = 700, 16, 256
+    x = rng.integers(0, 256, (n, D), dtype=np.uint8)
+    graph = random_graph(rng, n, R, sentinel_frac=0.2)
+    q = rng.integers(0, 256, (100, D), dtype=np.uint8)
+    check_parity(orc, torch_dev, x, graph, q, 10, 64, 4)
+
+
 def test_host_pointers(orc, torch_dev):
     spec = IndexSpec(n=1000, D=32, dtype="u8", clusters=3, sigma=20.0, r_near=8, r_rand=8, seed=11)
     a = index_arrays(spec, use_cache=False)
