@@ -34,8 +34,9 @@ struct PagedState {
   uint8_t *d_cache = nullptr;                 // slots * page_bytes
   unsigned long long *d_slot_word = nullptr;  // slots
   uint32_t *d_page_slot = nullptr;            // num_pages
-  // device control words (one allocation): clock hand, mq tail, cq head,
-  // tail mirror, poll lock, abort mirror, next query
+  // device control words (one allocation): clock hand, descriptor tail, shared
+  // completion head and tail mirror, poll lock, abort mirror, next query,
+  // finished queries
   unsigned long long *d_ctrl = nullptr;
   // host rings (coherent pinned memory) and their device-visible addresses
   unsigned long long *h_mq = nullptr, *d_mq = nullptr;
