@@ -74,11 +74,13 @@ def cpu_baseline(a, q, w, gpu_ids, gpu_dists, sample_nq: int, threads: int):
     oids, od, oc, _ = packed.search(qs, w.k, w.L, w.W, entry, threads=threads)
     dt = time.perf_counter() - t0
     exact = bool(np.array_equal(oids, gpu_ids[:sample_nq]) and np.array_equal(od, gpu_dists[:sample_nq]))
+    counts = {"queries": len(qs), "evaluations": int(oc["evaluations"].sum()),
+              "expansions": int(oc["expansions"].sum())}
     return {
         "value": round(sample_nq / dt, 1), "unit": "queries/s", "cores": threads, "kind": "oracle",
         "sample": f"first {sample_nq} of {len(q)} queries of the same workload, "
                   f"{threads} threads on disjoint query shards, {dt:.2f} s wall",
-    }, exact, entry
+    }, exact, entry, counts
 
 
 def host_link_peak_gbs(torch) -> float:
@@ -218,10 +220,30 @@ def main():
                  "kernel_ms_avg": round(float(np.mean(o_kms)), 4),
                  "same_answers": bool(torch.equal(o_ids, ids) and torch.equal(o_d, dists))}
 
+    gi = ids.cpu().numpy().view(np.uint32)
+    gd = dists.cpu().numpy()
+    cpu = None
+    exact = None
+    ocounts = None
+    if not args.no_cpu_baseline:
+        threads = min(os.cpu_count() or 1, 16)
+        cpu, exact, entry, ocounts = cpu_baseline(a, q, w, gi, gd, min(args.cpu_sample, nq), threads)
+        assert entry == info["entry"], "entry node differs from the oracle's"
+        log(f"[bench] oracle on CPU: {cpu['value']:,.0f} queries/s with {threads} threads; "
+            f"GPU answers oracle-exact on the sample: {exact}")
+
+    # Algorithmic bytes: every expansion reads 4 + 4R bytes, every node of V
+    # (first-time evaluations) its vector.  |V| is exact from the oracle's
+    # counts when it ran on the whole batch; otherwise the GPU's evaluations
+    # minus those it could not record in its visited filter (a lower bound:
+    # an unrecorded evaluation may still be the node's first).
     st = stats[-1]
     R = info["R"]
     vec_bytes = w.index.vec_bytes
-    first_evals = st["evaluations"] - st["reevaluations"]
+    if ocounts is not None and ocounts["queries"] == nq:
+        first_evals, counts_source = ocounts["evaluations"], "oracle"
+    else:
+        first_evals, counts_source = st["evaluations"] - st["reevaluations"], "gpu lower bound"
     alg_bytes = st["expansions"] * (4 + 4 * R) + first_evals * vec_bytes
     avg_kernel_ms = float(np.mean(kernel_ms))
     achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
@@ -230,18 +252,10 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
                 "kernel": "search_resident<MetricU8>", "kernel_ms_avg": round(avg_kernel_ms, 4),
-                "algorithmic_bytes_per_launch": int(alg_bytes)}
-
-    gi = ids.cpu().numpy().view(np.uint32)
-    gd = dists.cpu().numpy()
-    cpu = None
-    exact = None
-    if not args.no_cpu_baseline:
-        threads = min(os.cpu_count() or 1, 16)
-        cpu, exact, entry = cpu_baseline(a, q, w, gi, gd, min(args.cpu_sample, nq), threads)
-        assert entry == info["entry"], "entry node differs from the oracle's"
-        log(f"[bench] oracle on CPU: {cpu['value']:,.0f} queries/s with {threads} threads; "
-            f"GPU answers oracle-exact on the sample: {exact}")
+                "algorithmic_bytes_per_launch": int(alg_bytes),
+                "algorithmic_counts": counts_source,
+                "expansions_match_oracle": (None if counts_source != "oracle"
+                                            else ocounts["expansions"] == st["expansions"])}
 
     paged = None
     miss_gbs = None

@@ -18,17 +18,17 @@ hipError_t launch_resident_f32(const ResidentParams &p, int grid, hipStream_t s)
 hipError_t launch_paged_u8(const PagedParams &pp, int grid, hipStream_t s);
 hipError_t launch_paged_f32(const PagedParams &pp, int grid, hipStream_t s);
 
-// Visited tables of the resident kernel: 8192 entries, 16-bit (16 KB of LDS)
-// when every id is below 2^24, else 32-bit (32 KB).
-using ResidentHtSmall = VisitedLds16<13>;
+// Visited tables of the resident kernel: 16-bit entries (2^M::kHtLog2 of
+// them) when every id fits that table's domain, else 8192 32-bit entries.
 using ResidentHtLarge = VisitedLds<13>;
 
 namespace detail {
 
 template <int KPL, class M, bool N2S>
 hipError_t resident_t(const ResidentParams &p, int grid, hipStream_t s) {
-  if (p.n <= ResidentHtSmall::kMaxId)
-    search_resident<KPL, M, ResidentHtSmall, N2S><<<grid, kWave, 0, s>>>(p);
+  using Small = VisitedLds16<M::kHtLog2>;
+  if (p.n <= Small::kMaxId)
+    search_resident<KPL, M, Small, N2S><<<grid, kWave, 0, s>>>(p);
   else
     search_resident<KPL, M, ResidentHtLarge, N2S><<<grid, kWave, 0, s>>>(p);
   return hipGetLastError();

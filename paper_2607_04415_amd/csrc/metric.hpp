@@ -31,6 +31,10 @@ struct MetricU8 {
   static constexpr int kChunks = kBatch / kWave;
   static_assert(kRounds % 8 == 0, "rounds are reduced eight at a time");
   static constexpr int kQueryWords = 1;          // the query lives in registers
+  // resident kernel: waves per SIMD and the 16-bit visited table that fits
+  // them (4 waves: <= 128 registers, 4096 entries in 8 KB of LDS)
+  static constexpr int kWavesPerSimd = VDW <= 4 ? 4 : 2;
+  static constexpr int kHtLog2 = VDW <= 4 ? 12 : 13;
   static constexpr uint32_t kPadDist = 0x7FFFFFFFu;  // INT32_MAX
 
   U8Vec<VDW, EXACT> q;
@@ -164,6 +168,9 @@ struct MetricF32 {
   static constexpr int kChunks = 1;
   static constexpr int kQueryWords = 4 * NV4;
   static constexpr uint32_t kPadDist = 0x7F800000u;  // +inf
+  // resident kernel: the whole-vector registers of a lane allow two waves per SIMD
+  static constexpr int kWavesPerSimd = 2;
+  static constexpr int kHtLog2 = 13;
   static constexpr int kStep = 16;                   // dwords per round trip (generic path)
 
   const float *qs;  // the query in LDS (wave-uniform reads)

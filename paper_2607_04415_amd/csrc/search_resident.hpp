@@ -40,10 +40,11 @@ struct ResidentParams {
   unsigned long long *stats;  // [evaluations, reevaluations, expansions, iterations]
 };
 
-// Two waves per SIMD (registers <= 256 per lane, LDS <= 20 KB with the 16-bit
-// visited table): one wave's gathers overlap the other's filtering and merging.
+// Several waves per SIMD (M::kWavesPerSimd: 4 for uint8 rows up to 128 bytes,
+// with an 8 KB visited table; 2 otherwise): one wave's gathers overlap the
+// others' filtering and merging.
 template <int KPL, class M, class HT, bool N2S>
-__global__ __launch_bounds__(kWave, 2) void search_resident(ResidentParams p) {
+__global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(ResidentParams p) {
   constexpr int kChunks = M::kChunks;
   constexpr int kBatch = M::kBatch;
   constexpr int kIdsPerLane = kCandCap / kWave;
