@@ -308,3 +308,42 @@ def test_workload_f32_10m_paged(orc, torch_dev):
     packed = orc.pack(a["x"], a["graph"])
     oids, od, oc, _ = packed.search(q[:100], w.k, w.L, w.W, e, threads=16)
     assert_same(gi[:100], gd[:100], oids, od)
+
+
+RANDOM_CONFIGS = 10
+
+
+@pytest.mark.parametrize("seed", range(RANDOM_CONFIGS))
+def test_paged_random_configuration(orc, torch_dev, seed):
+    """Seeded random configurations of the whole paged path: dtype, sizes,
+    beam, page size and layout, cache size, latency, slots, blocking mode."""
+    rng = np.random.default_rng(1000 + seed)
+    dtype = "u8" if rng.random() < 0.6 else "f32"
+    D = int(rng.choice([4, 16, 64, 128]) if dtype == "u8" else rng.choice([7, 32, 96]))
+    R = int(rng.choice([8, 24, 64]))
+    n = int(rng.integers(3000, 15000))
+    spec = IndexSpec(n=n, D=D, dtype=dtype, clusters=int(rng.integers(2, 9)),
+                     sigma=20.0 if dtype == "u8" else 0.05, r_near=R // 2, r_rand=R - R // 2,
+                     seed=int(rng.integers(1 << 30)))
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(int(rng.integers(50, 300)), int(rng.integers(1 << 30))))
+    L = int(rng.choice([16, 48, 64, 100, 128]))
+    k = int(rng.integers(1, min(L, 20) + 1))
+    W = int(rng.integers(1, min(L, 16) + 1))
+    layout = dict(page_bytes=int(rng.choice([4096, 4096, 8192])), vectors_first=bool(rng.random() < 0.5))
+    if rng.random() < 0.3:
+        layout["node_to_slot"] = rng.permutation(n).astype(np.uint32)
+    ix = g.Index(a["x"], a["graph"], **layout)
+    e = ix.info["entry"]
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"], **layout).search(q, k, L, W, e, threads=8)
+    pb = ix.info["page_bytes"]
+    ix.set_cache(max(int(rng.uniform(0.02, 0.6) * ix.info["index_bytes"]), 128 * pb))
+    blocking = bool(rng.random() < 0.25)
+    ix.set_backing(latency_us=float(rng.choice([0.0, 3.0, 20.0])), oversub=int(rng.choice([1, 2, 4, 8])),
+                   blocking=blocking)
+    print(f"[random {seed}] {dtype} n={n} D={D} R={R} k={k} L={L} W={W} {layout.get('page_bytes')} "
+          f"vfirst={layout['vectors_first']} perm={'node_to_slot' in layout} slots={ix.info['cache_slots']} "
+          f"blocking={blocking}", flush=True)
+    gi, gd, st = search(torch_dev, ix, q, k, L, W)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())

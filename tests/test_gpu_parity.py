@@ -324,3 +324,31 @@ def test_workload_u8_10k(orc, torch_dev):
 
 def test_workload_u8_1m(orc, torch_dev):
     _workload_parity(orc, torch_dev, "u8-1m-hbm")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_resident_random_configuration(orc, torch_dev, seed):
+    """Seeded random resident configurations: dtype, sizes, beam, page layout."""
+    rng = np.random.default_rng(2000 + seed)
+    dtype = "u8" if rng.random() < 0.6 else "f32"
+    D = int(rng.choice([4, 8, 32, 128, 256]) if dtype == "u8" else rng.choice([3, 24, 96, 160]))
+    R = int(rng.choice([4, 16, 40, 64, 128]))
+    n = int(rng.integers(max(R + 2, 500), 20000))
+    spec = IndexSpec(n=n, D=D, dtype=dtype, clusters=int(rng.integers(1, 9)),
+                     sigma=20.0 if dtype == "u8" else 0.05, r_near=R // 2, r_rand=R - R // 2,
+                     seed=int(rng.integers(1 << 30)))
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(int(rng.integers(20, 400)), int(rng.integers(1 << 30))))
+    L = int(rng.choice([1, 8, 33, 64, 65, 128, 200, 256]))
+    k = int(rng.integers(1, L + 1))
+    W = int(rng.integers(1, L + 1)) if rng.random() < 0.2 else int(rng.integers(1, min(L, 16) + 1))
+    layout = dict(vectors_first=bool(rng.random() < 0.5))
+    if rng.random() < 0.3:
+        layout["node_to_slot"] = rng.permutation(n).astype(np.uint32)
+    if rng.random() < 0.2:
+        layout["page_bytes"] = 8192
+    print(f"[resident random {seed}] {dtype} n={n} D={D} R={R} k={k} L={L} W={W} "
+          f"vfirst={layout['vectors_first']} perm={'node_to_slot' in layout} page={layout.get('page_bytes', 4096)}",
+          flush=True)
+    check_parity(orc, torch_dev, a["x"], a["graph"], q, k, L, W,
+                 layout={kk: v for kk, v in layout.items()})
