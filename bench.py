@@ -83,6 +83,27 @@ def cpu_baseline(a, q, w, gpu_ids, gpu_dists, sample_nq: int, threads: int):
     }, exact, entry, counts
 
 
+def recall_at_k(x: np.ndarray, q: np.ndarray, ids: np.ndarray, k: int, sample: int) -> dict:
+    """Recall@k of the search answers against exact top-k (squared L2, ties by
+    id) on the first `sample` queries; informational (the paper reports QPS
+    with Recall@10).  Distances are formed in float64: exact integers for uint8
+    data; for float32 data near-ties may order differently from float32 sums."""
+    qs, got = q[:sample], ids[:sample]
+    xf = x.astype(np.float64)
+    xx = (xf * xf).sum(1)
+    hits = 0
+    for i in range(0, len(qs), 50):
+        qf = qs[i:i + 50].astype(np.float64)
+        d = (qf * qf).sum(1)[:, None] + xx[None, :] - 2.0 * (qf @ xf.T)
+        if x.dtype == np.uint8:
+            d = np.rint(d).astype(np.int64)
+        for j in range(len(qf)):
+            cand = np.argpartition(d[j], k)[:k + 64]
+            exact = cand[np.lexsort((cand, d[j][cand]))][:k]
+            hits += len(np.intersect1d(exact, got[i + j][:k]))
+    return {"value": round(hits / (len(qs) * k), 4), "k": k, "queries": len(qs)}
+
+
 def host_link_peak_gbs(torch) -> float:
     """Pinned host -> HBM copy bandwidth (256 MiB, best of 5), the host-link ceiling."""
     src = torch.empty(1 << 28, dtype=torch.uint8).pin_memory()
@@ -142,6 +163,8 @@ def main():
     ap.add_argument("--no-other-layout", action="store_true",
                     help="do not time the other page layout")
     ap.add_argument("--cpu-sample", type=int, default=10000)
+    ap.add_argument("--recall-sample", type=int, default=100,
+                    help="queries whose recall@k against exact top-k is reported (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
@@ -257,6 +280,11 @@ def main():
                 "expansions_match_oracle": (None if counts_source != "oracle"
                                             else ocounts["expansions"] == st["expansions"])}
 
+    recall = None
+    if args.recall_sample > 0:
+        recall = recall_at_k(a["x"], q, gi, w.k, min(args.recall_sample, nq))
+        log(f"[bench] recall@{w.k} on {recall['queries']} queries: {recall['value']}")
+
     paged = None
     miss_gbs = None
     if args.paged_sample > 0 and w.name == "u8-1m-hbm":
@@ -310,6 +338,7 @@ def main():
                    "cache_frac": w.cache_frac, "resident": bool(info["resident"])},
         "other_layout": other,
         "oracle_exact": exact,
+        "recall": recall,
         "achieved_hbm_gbs": roofline["achieved"],
         "miss_service_gbs": miss_gbs,
         "counters": {k: st[k] for k in ("evaluations", "reevaluations", "expansions", "iterations")},

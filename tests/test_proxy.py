@@ -1,7 +1,8 @@
 """The transport proxy on the CPU, with host threads playing the GPU side.
 
 Exactly-once completion, the injected latency honoured, the outstanding cap
-respected; once more under ThreadSanitizer.
+respected, completions reordered under jitter; once more under
+ThreadSanitizer and AddressSanitizer.
 """
 import json
 import subprocess
@@ -13,11 +14,11 @@ ROOT = Path(__file__).resolve().parents[1]
 SRC = [ROOT / "tests" / "proxy_harness.cpp", ROOT / "paper_2607_04415_amd" / "csrc" / "proxy.cpp"]
 
 
-def build(tmp_path, sanitize=False):
-    exe = tmp_path / ("harness_tsan" if sanitize else "harness")
+def build(tmp_path, sanitize=None):
+    exe = tmp_path / f"harness_{sanitize or 'plain'}"
     cmd = ["g++", "-O2", "-std=c++17", "-pthread", "-o", str(exe), *map(str, SRC)]
     if sanitize:
-        cmd[1:1] = ["-fsanitize=thread", "-g"]
+        cmd[1:1] = [f"-fsanitize={sanitize}", "-g"]
     subprocess.run(cmd, check=True)
     return exe
 
@@ -46,7 +47,13 @@ def test_proxy_jitter_reorders_and_stays_exactly_once(tmp_path):
     assert r0["missing"] == 0 and r0["duplicated"] == 0
 
 
+def test_proxy_under_address_sanitizer(tmp_path):
+    exe = build(tmp_path, sanitize="address")
+    r = run(exe, 20000, 5.0, 1024, 2000, 3, 4, 20.0, timeout=300)
+    assert r["missing"] == 0 and r["duplicated"] == 0
+
+
 def test_proxy_under_thread_sanitizer(tmp_path):
-    exe = build(tmp_path, sanitize=True)
+    exe = build(tmp_path, sanitize="thread")
     r = run(exe, 20000, 5.0, 1024, 2000, 3, 4, timeout=300)
     assert r["missing"] == 0 and r["duplicated"] == 0
