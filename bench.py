@@ -175,7 +175,7 @@ def main():
                          "generating that index takes minutes the first time)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
+        print(f"bench.py: runs on one GPU only (asked for {args.gpus}); "
               "the search shards by query across GPUs but no multi-GPU path is built.",
               file=sys.stderr)
         sys.exit(2)

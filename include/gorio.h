@@ -64,7 +64,7 @@ typedef enum {
     GORIO_ENOMEM = 2,        /* device or pinned host allocation failed */
     GORIO_EDEVICE = 3,       /* a HIP runtime call or a kernel failed */
     GORIO_ETIMEOUT = 4,      /* paged search made no progress within the watchdog limit */
-    GORIO_EUNSUPPORTED = 5   /* valid request this build does not implement */
+    GORIO_EUNSUPPORTED = 5   /* valid request the library does not implement */
 } gorio_status;
 
 typedef enum { GORIO_U8 = 0, GORIO_F32 = 1 } gorio_dtype;
