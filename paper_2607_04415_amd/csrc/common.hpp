@@ -52,6 +52,12 @@ struct PageGeom {
   uint32_t adj_stride;
   FastDiv rpp;             // records per page
   const uint32_t *node_to_slot;  // nullptr: slot = node id
+  // 16-byte units: when every vector starts on a 16-byte boundary and the
+  // index has fewer than 2^31 units (units16 != 0), a vector is also named by
+  // its locator page * page16 + i * vec16, the index of its first unit.
+  uint32_t units16;
+  FastDiv page16;          // page_bytes / 16
+  FastDiv vec16;           // vec_stride / 16
 };
 
 __device__ __forceinline__ uint32_t slot_of(const PageGeom &g, uint32_t v) {
@@ -71,6 +77,29 @@ template <bool N2S>
 __device__ __forceinline__ uint32_t slot_ct(const PageGeom &g, uint32_t v) {
   if constexpr (N2S) return g.node_to_slot[v];
   else return v;
+}
+
+// 16-byte load through a structured buffer resource: address = base +
+// vindex * stride (the stride is part of the resource); an index at or past
+// the resource's record count reads zeros instead of faulting.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ u32x4_t struct_buffer_load_b128(__amdgpu_buffer_rsrc_t rsrc, int vindex, int voffset, int soffset,
+                                           int aux) __asm("llvm.amdgcn.struct.ptr.buffer.load.v4i32");
+
+// The packed pages as 16-byte records (units16 != 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t units16_rsrc(const uint8_t *pages, const PageGeom &g) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(pages), (short)16, (int)g.units16, 0x00020000);
+}
+
+// Locator of slot s's vector (units16 != 0) and the slot a locator names.
+__device__ __forceinline__ uint32_t vec_locator(const PageGeom &g, uint32_t s) {
+  uint32_t page, pos;
+  locate(g, s, page, pos);
+  return page * g.page16.d + pos * g.vec16.d;
+}
+__device__ __forceinline__ uint32_t slot_of_locator(const PageGeom &g, uint32_t loc) {
+  const uint32_t page = fastdiv(loc, g.page16);
+  return page * g.rpp.d + fastdiv(loc - page * g.page16.d, g.vec16);
 }
 
 // Byte offsets of slot s's vector and adjacency block in the packed page array.

@@ -37,10 +37,16 @@ hipError_t resident_t(const ResidentParams &p, int grid, hipStream_t s) {
 // frontier slots per lane (L <= 64 KPL) and node_to_slot presence
 template <class M>
 hipError_t resident(const ResidentParams &p, int grid, hipStream_t s) {
-  const bool n2s = p.geom.node_to_slot != nullptr;
-  if (p.L <= 64) return n2s ? resident_t<1, M, true>(p, grid, s) : resident_t<1, M, false>(p, grid, s);
-  if (p.L <= 128) return n2s ? resident_t<2, M, true>(p, grid, s) : resident_t<2, M, false>(p, grid, s);
-  return n2s ? resident_t<4, M, true>(p, grid, s) : resident_t<4, M, false>(p, grid, s);
+  if constexpr (M::kLocators) {  // identity placement only
+    if (p.L <= 64) return resident_t<1, M, false>(p, grid, s);
+    if (p.L <= 128) return resident_t<2, M, false>(p, grid, s);
+    return resident_t<4, M, false>(p, grid, s);
+  } else {
+    const bool n2s = p.geom.node_to_slot != nullptr;
+    if (p.L <= 64) return n2s ? resident_t<1, M, true>(p, grid, s) : resident_t<1, M, false>(p, grid, s);
+    if (p.L <= 128) return n2s ? resident_t<2, M, true>(p, grid, s) : resident_t<2, M, false>(p, grid, s);
+    return n2s ? resident_t<4, M, true>(p, grid, s) : resident_t<4, M, false>(p, grid, s);
+  }
 }
 
 template <int KPL, class M, bool N2S>

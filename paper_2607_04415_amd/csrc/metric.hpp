@@ -22,7 +22,12 @@ namespace gorio {
 // ---------------------------------------------------------------------------
 // uint8
 // ---------------------------------------------------------------------------
-template <int VDW, bool EXACT>
+// LOC16: the kernel keeps each candidate as its vector's 16-byte locator
+// (identity placement, units16 != 0) instead of its id, stored so that the
+// kRounds candidates of each group of 8 lanes are consecutive words: the
+// batch's addresses arrive with kRounds / 4 LDS reads and no per-round
+// address arithmetic, and ids are recovered from locators for the keys.
+template <int VDW, bool EXACT, bool LOC16 = false>
 struct MetricU8 {
   // vectors in flight per resident gather batch: 128 for up to 16 B per lane,
   // 64 for wider rows (kept small so that two waves fit each SIMD's registers)
@@ -36,6 +41,30 @@ struct MetricU8 {
   static constexpr int kWavesPerSimd = VDW <= 4 ? 4 : 2;
   static constexpr int kHtLog2 = VDW <= 4 ? 12 : 13;
   static constexpr uint32_t kPadDist = 0x7FFFFFFFu;  // INT32_MAX
+  static_assert(!LOC16 || (EXACT && VDW % 4 == 0), "locators address whole 16-byte units");
+  static constexpr bool kLocators = LOC16;
+
+  // Where the kernel's compaction puts the i-th new candidate, and the word
+  // it stores for node v (its id, or with LOC16 its vector's locator).
+  __device__ __forceinline__ static uint32_t cand_pos(uint32_t i) {
+    if constexpr (LOC16)
+      return (i & ~(uint32_t)(kBatch - 1)) | ((i & 7u) * kRounds) | ((i >> 3) & (uint32_t)(kRounds - 1));
+    else
+      return i;
+  }
+  __device__ __forceinline__ static uint32_t cand_word(const PageGeom &geom, uint32_t v) {
+    if constexpr (LOC16) return vec_locator(geom, v);
+    else return v;
+  }
+
+  // After compaction of cnt candidates: give the rest of the last round of 8
+  // the fallback node's word, so that every lane of a round loads a vector.
+  __device__ __forceinline__ static void pad_round(uint32_t *cand, uint32_t cnt, uint32_t fallback_word) {
+    if constexpr (LOC16) {
+      const uint32_t i = cnt + (uint32_t)lane_id();
+      if (lane_id() < 8 && i < ((cnt + 7u) & ~7u)) cand[cand_pos(i)] = fallback_word;
+    }
+  }
 
   U8Vec<VDW, EXACT> q;
   int qq;
@@ -64,6 +93,11 @@ struct MetricU8 {
   __device__ __forceinline__ void resident_keys(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
                                                 uint32_t c0, uint32_t cnt, uint32_t fallback,
                                                 uint64_t (&key)[kChunks]) const {
+    if constexpr (LOC16) {
+      static_assert(!N2S, "locators name slots of the identity placement");
+      resident_keys_loc(pages, geom, cand, c0, cnt, fallback, key);
+      return;
+    }
     const int l = lane_id();
     const int g = l >> 3;
     const int gl = l & 7;
@@ -97,6 +131,61 @@ struct MetricU8 {
     for (int c = 0; c < kChunks; ++c) {
       const uint32_t my_idx = c0 + c * kWave + gl * 8 + g;
       key[c] = my_idx < cnt ? (((uint64_t)(uint32_t)dist[c] << 32) | ((uint64_t)cand[my_idx] << 1)) : kInfKey;
+    }
+  }
+
+  // resident_keys with LOC16: lane group g reads its kRounds locators as
+  // consecutive words, loads through a 16-byte-stride buffer resource.  The
+  // caller has filled the positions of the last round past cnt with the
+  // fallback node's word (pad_round).
+  __device__ __forceinline__ void resident_keys_loc(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
+                                                    uint32_t c0, uint32_t cnt, uint32_t fallback,
+                                                    uint64_t (&key)[kChunks]) const {
+    const int l = lane_id();
+    const int g = l >> 3;
+    const int gl = l & 7;
+    const __amdgpu_buffer_rsrc_t rs = units16_rsrc(pages, geom);
+    uint32_t loc[kRounds];
+    const uint4 *src = reinterpret_cast<const uint4 *>(cand + c0 + g * kRounds);
+#pragma unroll
+    for (int i = 0; i < kRounds / 4; ++i) {
+      const uint4 v = src[i];
+      loc[4 * i] = v.x; loc[4 * i + 1] = v.y; loc[4 * i + 2] = v.z; loc[4 * i + 3] = v.w;
+    }
+    // keep the wide reads here, ahead of the rounds (the compiler would
+    // otherwise sink one narrow read, and its wait, into each round)
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) asm volatile("" : "+v"(loc[rr]));
+    U8Vec<VDW, EXACT> x[kRounds];
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) {
+      if (c0 + rr * 8 >= cnt) break;
+      // (positions past cnt in the last round hold the fallback's locator)
+      const uint32_t u = loc[rr] + (uint32_t)gl * (VDW / 4);
+#pragma unroll
+      for (int t = 0; t < VDW; t += 4) {
+        const u32x4_t v = struct_buffer_load_b128(rs, (int)(u + t / 4), 0, 0, 0);
+        x[rr].w[t] = v.x; x[rr].w[t + 1] = v.y; x[rr].w[t + 2] = v.z; x[rr].w[t + 3] = v.w;
+      }
+    }
+    int dist[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      dist[c] = 0;
+      if (c0 + c * kWave >= cnt) break;
+      int part[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) part[j] = c0 + (c * 8 + j) * 8 < cnt ? partial_u8(q, x[c * 8 + j]) : 0;
+      dist[c] = transpose_sum8(part) + qq;
+    }
+    // lane (g, gl) of chunk c holds round 8c + gl of group g: candidate
+    // c0 + (8c + gl) * 8 + g, stored at c0 + g * kRounds + 8c + gl
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const uint32_t rr = (uint32_t)(c * 8 + gl);
+      const bool ok = c0 + rr * 8 + g < cnt;
+      const uint32_t v = ok ? slot_of_locator(geom, cand[c0 + g * kRounds + rr]) : 0u;
+      key[c] = ok ? (((uint64_t)(uint32_t)dist[c] << 32) | ((uint64_t)v << 1)) : kInfKey;
     }
   }
 
@@ -175,6 +264,11 @@ struct MetricF32 {
 
   const float *qs;  // the query in LDS (wave-uniform reads)
   uint32_t D;
+
+  static constexpr bool kLocators = false;
+  __device__ __forceinline__ static void pad_round(uint32_t *, uint32_t, uint32_t) {}
+  __device__ __forceinline__ static uint32_t cand_pos(uint32_t i) { return i; }
+  __device__ __forceinline__ static uint32_t cand_word(const PageGeom &, uint32_t v) { return v; }
 
   // Copies the query into LDS; the caller synchronizes before use.
   __device__ __forceinline__ void load_query(const void *queries, uint32_t qi, uint32_t D_, uint32_t *qlds) {

@@ -50,12 +50,13 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
   constexpr int kIdsPerLane = kCandCap / kWave;
 
   __shared__ __align__(16) uint32_t ht[HT::kWords];
-  __shared__ uint32_t cand[kCandCap];
+  __shared__ __align__(16) uint32_t cand[kCandCap];
   __shared__ uint32_t beam[kMaxW];
   __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
 
   const int l = lane_id();
   const uint32_t beams_per_group = min(kCandCap / p.R, (uint32_t)kWave);
+  const uint32_t entry_word = M::cand_word(p.geom, p.entry);
 
   unsigned long long n_eval = 0, n_reeval = 0, n_exp = 0, n_iter = 0;
 
@@ -142,13 +143,14 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
         for (int t = 0; t < kIdsPerLane; ++t) {
           const uint64_t mnew = ballot(isnew[t]);
           const uint64_t mrec = ballot(recorded[t]);
-          if (isnew[t]) cand[cnt + lanes_below(mnew)] = ids[t];
+          if (isnew[t]) cand[M::cand_pos(cnt + lanes_below(mnew))] = M::cand_word(p.geom, ids[t]);
           cnt += (uint32_t)__popcll(mnew);
           ht_used += (uint32_t)__popcll(mrec);
           const uint32_t lost = (uint32_t)__popcll(mnew & ~mrec);
           n_reeval += lost;
           forgot |= lost != 0;
         }
+        M::pad_round(cand, cnt, entry_word);
         __syncthreads();
         n_eval += cnt;
 
