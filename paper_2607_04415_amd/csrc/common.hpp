@@ -223,6 +223,21 @@ struct VisitedLds {
   }
 };
 
+// Per-half unsigned minimum of two words (v_pk_min_u16), and a 24-bit
+// multiply (v_mul_u32_u24: full rate, where a 32-bit multiply is not).
+// Written as instructions so that the compiler keeps them as one operation
+// instead of expanding them per half.
+__device__ __forceinline__ uint32_t pk_min_u16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ uint32_t mul_u24(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_mul_u32_u24 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Compact visited filter in LDS: 16-bit entries, buckets of eight (16 bytes,
 // one ds_read_b128), for ids below 2^(LOG2 + 11) (2^24 for 8192 entries).
 // h = (id * odd) mod 2^(LOG2 + 11) is a bijection; its top LOG2 - 3 bits
@@ -241,15 +256,9 @@ struct VisitedLds16 {
   static constexpr uint32_t kMaxId = 1u << (kHomeBits + 14);  // ids must be below this
   static constexpr int kMaxRounds = 64;
 
-  __device__ __forceinline__ static uint32_t mix(uint32_t id) { return (id * 0x9E3779B1u) & (kMaxId - 1); }
-
   __device__ __forceinline__ static void clear(uint32_t *t) {
     uint4 *t4 = reinterpret_cast<uint4 *>(t);
     for (uint32_t i = lane_id(); i < kBuckets; i += kWave) t4[i] = make_uint4(0u, 0u, 0u, 0u);
-  }
-
-  __device__ __forceinline__ static uint32_t word_of(const uint4 &v, uint32_t k) {
-    return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
   }
 
   __device__ __forceinline__ static bool test_and_set(uint32_t *t, uint32_t id, bool may_store,
@@ -261,19 +270,26 @@ struct VisitedLds16 {
     return isnew[0];
   }
 
-  // Same contract as VisitedLds::test_and_set_n (ids < 2^24).
+  // Same contract as VisitedLds::test_and_set_n (ids below kMaxId).
+  // Slots of a bucket fill in order (an id only ever claims the first empty
+  // slot, by compare-and-swap), so the occupied slots are a prefix and the
+  // first empty slot is their count.  Bucket tests are branch-free and work
+  // on both halves of a word at once: a half equals e iff that half of
+  // w ^ (e * 0x10001) is zero, and min(half, 1) is 1 iff it is occupied.
   template <int N>
   __device__ __forceinline__ static void test_and_set_n(uint32_t *t, const uint32_t (&ids)[N],
                                                         const bool (&valid)[N], bool may_store,
                                                         bool (&isnew)[N], bool (&recorded)[N]) {
     const uint4 *t4 = reinterpret_cast<const uint4 *>(t);
-    uint32_t home[N], r[N], d[N];
+    uint32_t home[N], e0[N], d[N];
     bool pend[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const uint32_t h = mix(ids[i]);
+      // v_mul_u32_u24 reads the low 24 bits of each operand: exact for ids
+      // below 2^24; an invalid lane's id only picks some bucket to read
+      const uint32_t h = mul_u24(ids[i], 0x9E3779B1u & 0xFFFFFFu) & (kMaxId - 1);
       home[i] = h >> 14;
-      r[i] = h & 0x3FFFu;
+      e0[i] = 1u + (h & 0x3FFFu);
       d[i] = 0;
       pend[i] = valid[i];
       isnew[i] = false;
@@ -290,10 +306,8 @@ struct VisitedLds16 {
       for (int i = 0; i < N; ++i) live[i] = round == 0 || ballot(pend[i]) != 0;
       uint4 v[N];
 #pragma unroll
-      for (int i = 0; i < N; ++i) {
-        v[i] = make_uint4(0u, 0u, 0u, 0u);
-        if (live[i] && pend[i]) v[i] = t4[(home[i] + d[i]) & (kBuckets - 1)];
-      }
+      for (int i = 0; i < N; ++i)
+        if (live[i]) v[i] = t4[(home[i] + d[i]) & (kBuckets - 1)];
       bool cas[N];
       uint32_t word[N], expect[N], want[N];
 #pragma unroll
@@ -301,28 +315,26 @@ struct VisitedLds16 {
         cas[i] = false;
         word[i] = expect[i] = want[i] = 0;
         if (!live[i]) continue;
-        const uint32_t e = 1u + ((d[i] << 14) | r[i]);
-        // slot k is half k & 1 of word k >> 1: one 16-bit compare per slot
-        const uint32_t wv[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-        bool hit = false;
-        uint32_t j = 8;
-#pragma unroll
-        for (int k = 7; k >= 0; --k) {
-          const uint32_t h = (k & 1) ? (wv[k >> 1] >> 16) : (wv[k >> 1] & 0xFFFFu);
-          hit = hit || h == e;
-          j = h == 0 ? (uint32_t)k : j;
-        }
+        const uint32_t e = e0[i] + (d[i] << 14);
+        const uint32_t ee = e * 0x10001u;
+        const uint32_t m = pk_min_u16(pk_min_u16(v[i].x ^ ee, v[i].y ^ ee), pk_min_u16(v[i].z ^ ee, v[i].w ^ ee));
+        const bool hit = (m & 0xFFFFu) == 0 || (m >> 16) == 0;
+        const uint32_t one = 0x10001u;
+        const uint32_t occ = pk_min_u16(v[i].x, one) | (pk_min_u16(v[i].y, one) << 1) |
+                             (pk_min_u16(v[i].z, one) << 2) | (pk_min_u16(v[i].w, one) << 3);
+        const uint32_t j = (uint32_t)__popc(occ);  // first empty slot, 8 if full
         const bool absent = pend[i] && !hit && j < 8;
         const bool full = pend[i] && !hit && j == 8;
         const bool next = full && d[i] == 0;
         const bool lost = full && d[i] != 0;          // both buckets full: not recorded
         cas[i] = absent && may_store;
         isnew[i] = isnew[i] || (absent && !may_store) || lost;
-        j &= 7u;
-        const uint32_t w = word_of(v[i], j >> 1);
-        word[i] = ((home[i] + d[i]) & (kBuckets - 1)) * 4 + (j >> 1);
-        expect[i] = w;
-        want[i] = w | (e << ((j & 1u) * 16));
+        const uint32_t k = (j >> 1) & 3u;             // word of slot j
+        const uint32_t lo = (k & 1u) ? v[i].y : v[i].x;
+        const uint32_t hi = (k & 1u) ? v[i].w : v[i].z;
+        expect[i] = (k & 2u) ? hi : lo;
+        want[i] = expect[i] | (e << ((j & 1u) << 4));
+        word[i] = ((home[i] + d[i]) & (kBuckets - 1)) * 4 + k;
         d[i] = next ? 1u : d[i];
         pend[i] = next || cas[i];
       }
