@@ -238,23 +238,33 @@ __device__ __forceinline__ uint32_t mul_u24(uint32_t a, uint32_t b) {
   return r;
 }
 
-// Compact visited filter in LDS: 16-bit entries, buckets of eight (16 bytes,
-// one ds_read_b128), for ids below 2^(LOG2 + 11) (2^24 for 8192 entries).
-// h = (id * odd) mod 2^(LOG2 + 11) is a bijection; its top LOG2 - 3 bits
-// pick the home bucket, its low 14 bits r are stored as 1 + (d << 14 | r),
-// where d in {0, 1} is the bucket's distance from home (0 marks an empty
-// slot).  (bucket - d, r) gives back h, so an entry matches exactly one id:
-// the filter never invents a member.  An id whose home bucket and the next
-// are both full is not recorded.
+// Compact visited filter in LDS: 16-bit entries, buckets of eight half-words
+// (16 bytes, one ds_read_b128): seven id slots and, in the top half of the
+// last word, a count of the claims made on the bucket.  Ids must be below
+// 2^(LOG2 + 11) (2^23 for 4096 entries).  h = (id * odd) mod 2^(LOG2 + 11) is
+// a bijection; its top LOG2 - 3 bits pick the home bucket, its low 14 bits r
+// are stored as 1 + (d << 14 | r), where d in {0, 1} is the bucket's distance
+// from home (0 marks an empty slot).  (bucket - d, r) gives back h, so an
+// entry matches exactly one id: the filter never invents a member.
+//
+// An id lives in its home bucket unless that bucket was full when it was
+// inserted, then in the next one; claims never decrease, so a home bucket
+// with fewer than seven claims that lacks the id proves it absent.  Lanes
+// that insert into the same bucket take distinct slots from one LDS atomic
+// add on the claim count (no retries); lanes holding the same id then see,
+// on reading the bucket back, whether a lower slot already holds it, and
+// only the lowest keeps it.  Both buckets are read up front, so every call
+// takes one round.  An id whose two buckets are full is not recorded (it may
+// be evaluated again; the frontier merge drops the copy).
 template <int LOG2>
 struct VisitedLds16 {
-  static constexpr uint32_t kSize = 1u << LOG2;          // 16-bit slots
+  static constexpr uint32_t kSize = 1u << LOG2;          // 16-bit half-words
   static constexpr uint32_t kWords = kSize / 2;          // 32-bit LDS words
   static constexpr uint32_t kBuckets = kSize / 8;
-  static constexpr uint32_t kLimit = kSize - kSize / 4;   // stop recording at 75% load
+  static constexpr uint32_t kSlots = 7;                  // id slots per bucket
+  static constexpr uint32_t kLimit = kBuckets * kSlots;  // records at most this many ids
   static constexpr int kHomeBits = LOG2 - 3;
   static constexpr uint32_t kMaxId = 1u << (kHomeBits + 14);  // ids must be below this
-  static constexpr int kMaxRounds = 64;
 
   __device__ __forceinline__ static void clear(uint32_t *t) {
     uint4 *t4 = reinterpret_cast<uint4 *>(t);
@@ -270,91 +280,92 @@ struct VisitedLds16 {
     return isnew[0];
   }
 
+  // Whether a bucket's id slots below `below` (0..7) hold entry e: a half
+  // equals e iff that half of w ^ (e * 0x10001) is zero; halves at or above
+  // `below`, and the claim count, are forced to 0xFFFF (never an entry).
+  __device__ __forceinline__ static bool holds(const uint4 &v, uint32_t e, uint32_t below) {
+    const uint32_t ee = e * 0x10001u;
+    const uint64_t lo = ((uint64_t)v.y << 32) | v.x;                     // slots 0..3
+    const uint64_t hi = ((uint64_t)(v.w | 0xFFFF0000u) << 32) | v.z;     // slots 4..6, count
+    const uint32_t bl = below < 4u ? below : 4u, bh = below > 4u ? below - 4u : 0u;
+    const uint64_t mlo = bl >= 4u ? 0ull : ~0ull << (16u * bl);
+    const uint64_t mhi = ~0ull << (16u * bh);
+    const uint64_t xlo = (lo | mlo) ^ (((uint64_t)ee << 32) | ee);
+    const uint64_t xhi = (hi | mhi) ^ (((uint64_t)ee << 32) | ee);
+    const uint32_t m = pk_min_u16(pk_min_u16((uint32_t)xlo, (uint32_t)(xlo >> 32)),
+                                  pk_min_u16((uint32_t)xhi, (uint32_t)(xhi >> 32)));
+    return (m & 0xFFFFu) == 0 || (m >> 16) == 0;
+  }
+
   // Same contract as VisitedLds::test_and_set_n (ids below kMaxId).
-  // Slots of a bucket fill in order (an id only ever claims the first empty
-  // slot, by compare-and-swap), so the occupied slots are a prefix and the
-  // first empty slot is their count.  Bucket tests are branch-free and work
-  // on both halves of a word at once: a half equals e iff that half of
-  // w ^ (e * 0x10001) is zero, and min(half, 1) is 1 iff it is occupied.
   template <int N>
   __device__ __forceinline__ static void test_and_set_n(uint32_t *t, const uint32_t (&ids)[N],
                                                         const bool (&valid)[N], bool may_store,
                                                         bool (&isnew)[N], bool (&recorded)[N]) {
     const uint4 *t4 = reinterpret_cast<const uint4 *>(t);
-    uint32_t home[N], e0[N], d[N];
-    bool pend[N];
+    uint16_t *t16 = reinterpret_cast<uint16_t *>(t);
+    uint32_t bk[N], e[N], slot[N];
+    bool claim[N], won[N], over[N];
+    uint4 v0[N], v1[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       // v_mul_u32_u24 reads the low 24 bits of each operand: exact for ids
       // below 2^24; an invalid lane's id only picks some bucket to read
       const uint32_t h = mul_u24(ids[i], 0x9E3779B1u & 0xFFFFFFu) & (kMaxId - 1);
-      home[i] = h >> 14;
-      e0[i] = 1u + (h & 0x3FFFu);
-      d[i] = 0;
-      pend[i] = valid[i];
-      isnew[i] = false;
+      bk[i] = h >> 14;
+      e[i] = 1u + (h & 0x3FFFu);
+      v0[i] = t4[bk[i]];
+      v1[i] = t4[(bk[i] + 1) & (kBuckets - 1)];
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const bool hit0 = holds(v0[i], e[i], kSlots);
+      const bool hit1 = holds(v1[i], e[i] + (1u << 14), kSlots);
+      const bool full0 = (v0[i].w >> 16) >= kSlots, full1 = (v1[i].w >> 16) >= kSlots;
+      // present: in home, or in the next bucket when home was full
+      const bool present = hit0 || (full0 && hit1);
+      const bool absent = valid[i] && !present;
+      const bool lost = absent && full0 && full1;          // nowhere to record it
+      claim[i] = absent && !lost && may_store;
+      isnew[i] = absent && (lost || !may_store);
       recorded[i] = false;
+      // claim in home when it had room, else in the next bucket
+      const uint32_t d = full0 ? 1u : 0u;
+      bk[i] = (bk[i] + d) & (kBuckets - 1);
+      e[i] += d << 14;
     }
-    for (int round = 0; round < kMaxRounds; ++round) {
-      bool any = false;
+    asm volatile("" ::: "memory");  // the claims follow the bucket reads
+    uint32_t old[N];
 #pragma unroll
-      for (int i = 0; i < N; ++i) any |= pend[i];
-      if (ballot(any) == 0) break;
-      // after the first round few ids are left: skip an id no lane still holds
-      bool live[N];
-#pragma unroll
-      for (int i = 0; i < N; ++i) live[i] = round == 0 || ballot(pend[i]) != 0;
-      uint4 v[N];
-#pragma unroll
-      for (int i = 0; i < N; ++i)
-        if (live[i]) v[i] = t4[(home[i] + d[i]) & (kBuckets - 1)];
-      bool cas[N];
-      uint32_t word[N], expect[N], want[N];
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        cas[i] = false;
-        word[i] = expect[i] = want[i] = 0;
-        if (!live[i]) continue;
-        const uint32_t e = e0[i] + (d[i] << 14);
-        const uint32_t ee = e * 0x10001u;
-        const uint32_t m = pk_min_u16(pk_min_u16(v[i].x ^ ee, v[i].y ^ ee), pk_min_u16(v[i].z ^ ee, v[i].w ^ ee));
-        const bool hit = (m & 0xFFFFu) == 0 || (m >> 16) == 0;
-        const uint32_t one = 0x10001u;
-        const uint32_t occ = pk_min_u16(v[i].x, one) | (pk_min_u16(v[i].y, one) << 1) |
-                             (pk_min_u16(v[i].z, one) << 2) | (pk_min_u16(v[i].w, one) << 3);
-        const uint32_t j = (uint32_t)__popc(occ);  // first empty slot, 8 if full
-        const bool absent = pend[i] && !hit && j < 8;
-        const bool full = pend[i] && !hit && j == 8;
-        const bool next = full && d[i] == 0;
-        const bool lost = full && d[i] != 0;          // both buckets full: not recorded
-        cas[i] = absent && may_store;
-        isnew[i] = isnew[i] || (absent && !may_store) || lost;
-        const uint32_t k = (j >> 1) & 3u;             // word of slot j
-        const uint32_t lo = (k & 1u) ? v[i].y : v[i].x;
-        const uint32_t hi = (k & 1u) ? v[i].w : v[i].z;
-        expect[i] = (k & 2u) ? hi : lo;
-        want[i] = expect[i] | (e << ((j & 1u) << 4));
-        word[i] = ((home[i] + d[i]) & (kBuckets - 1)) * 4 + k;
-        d[i] = next ? 1u : d[i];
-        pend[i] = next || cas[i];
-      }
-      uint32_t old[N];
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        old[i] = 0;
-        if (cas[i]) old[i] = atomicCAS(&t[word[i]], expect[i], want[i]);
-      }
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        const bool won = cas[i] && old[i] == expect[i];
-        isnew[i] = isnew[i] || won;
-        recorded[i] = recorded[i] || won;
-        pend[i] = pend[i] && !won;   // the word changed: read the bucket again
-      }
+    for (int i = 0; i < N; ++i) {
+      old[i] = 0;
+      if (claim[i]) old[i] = atomicAdd(&t[bk[i] * 4 + 3], 0x10000u);
     }
 #pragma unroll
-    for (int i = 0; i < N; ++i)
-      if (pend[i]) isnew[i] = true;  // round limit: evaluate, unrecorded
+    for (int i = 0; i < N; ++i) {
+      slot[i] = old[i] >> 16;
+      won[i] = claim[i] && slot[i] < kSlots;
+      over[i] = claim[i] && slot[i] >= kSlots;              // lanes filled the bucket first
+      if (won[i]) t16[bk[i] * 8 + slot[i]] = (uint16_t)e[i];
+    }
+    // LDS operations of one wave complete in order; keep the compiler from
+    // moving the read-back above the 16-bit stores
+    asm volatile("" ::: "memory");
+    bool any = false;
+#pragma unroll
+    for (int i = 0; i < N; ++i) any |= claim[i];
+    if (ballot(any) == 0) return;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (ballot(claim[i]) == 0) continue;
+      const uint4 v = t4[bk[i]];
+      // a lower slot holding the same entry belongs to another lane with this
+      // id; a lane that found the bucket full keeps its id only if no lane
+      // recorded it there
+      const bool dup = holds(v, e[i], won[i] ? slot[i] : kSlots);
+      isnew[i] = isnew[i] || (claim[i] && !dup);
+      recorded[i] = won[i] && !dup;
+    }
   }
 };
 

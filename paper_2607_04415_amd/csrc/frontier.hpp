@@ -113,7 +113,7 @@ __device__ __forceinline__ void merge_dedupe(uint64_t (&F)[KPL], uint64_t c_desc
 #pragma unroll
   for (int r = 0; r < 2 * KPL; ++r)
     if (big[r] != kInfKey && next[r] != kInfKey && (next[r] >> 1) == (big[r] >> 1)) big[r] = kInfKey;
-  bitonic_sort<2 * KPL>(big, false);
+  bitonic_sort<2 * KPL, false>(big);
 #pragma unroll
   for (int r = 0; r < KPL; ++r) F[r] = big[r];
 }

@@ -458,7 +458,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
               }
             } else {
               uint64_t cc[1] = {key};
-              bitonic_sort<1>(cc, true);
+              bitonic_sort<1, true>(cc);
               if (!S.forgot) {
                 F[KPL - 1] = min64(F[KPL - 1], cc[0]);
                 bitonic_merge_up<KPL>(F);

@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
             for (int c = 0; c < kChunks; ++c) {
               if (pass_mask[c] == 0) continue;
               uint64_t cc[1] = {key[c]};
-              bitonic_sort<1>(cc, true);
+              bitonic_sort<1, true>(cc);
               if (!forgot) {
                 // no node can repeat: the P smallest of F and C are min(F, C reversed)
                 F[KPL - 1] = min64(F[KPL - 1], cc[0]);

@@ -110,28 +110,23 @@ __device__ __forceinline__ uint64_t max64(uint64_t a, uint64_t b) { return a < b
 // Bitonic networks over P = 64 * KPL keys held as v[r] at element r*64 + lane.
 // ---------------------------------------------------------------------------
 
-// Value of lane ^ M, M a power of two below 64, without the LDS crossbar:
-// DPP for M <= 8 (quad_perm, half-row mirror, row rotate), the gfx950
-// v_permlane16/32_swap for 16 and 32.
+// Value of lane ^ M for M <= 8 by DPP (quad_perm, half-row mirror, row
+// rotate), without the LDS crossbar.  Every lane's source exists, so the
+// moves need no old value.  (Distances 16 and 32 use v_permlane16/32_swap in
+// exchange_lanes.)
 template <int M>
 __device__ __forceinline__ uint32_t xor_lanes(uint32_t v) {
   const int iv = (int)v;
   if constexpr (M == 1) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, iv, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+    return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
   } else if constexpr (M == 2) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, iv, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+    return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
   } else if constexpr (M == 4) {
-    int t = __builtin_amdgcn_update_dpp(0, iv, 0x141, 0xF, 0xF, false);          // i -> 7 - i in 8
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, t, 0x1B, 0xF, 0xF, false);   // reverse each quad
-  } else if constexpr (M == 8) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, iv, 0x128, 0xF, 0xF, false); // row_ror:8
-  } else if constexpr (M == 16) {
-    auto r = __builtin_amdgcn_permlane16_swap(iv, iv, false, false);
-    return (uint32_t)(((lane_id() >> 4) & 1) ? r[0] : r[1]);
+    int t = __builtin_amdgcn_mov_dpp(iv, 0x141, 0xF, 0xF, false);          // i -> 7 - i in 8
+    return (uint32_t)__builtin_amdgcn_mov_dpp(t, 0x1B, 0xF, 0xF, false);   // reverse each quad
   } else {
-    static_assert(M == 32, "lane distance");
-    auto r = __builtin_amdgcn_permlane32_swap(iv, iv, false, false);
-    return (uint32_t)(lane_id() >= 32 ? r[0] : r[1]);
+    static_assert(M == 8, "lane distance");
+    return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0x128, 0xF, 0xF, false); // row_ror:8
   }
 }
 
@@ -142,17 +137,6 @@ __device__ __forceinline__ uint64_t xor_lanes64(uint64_t v) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t xor_lanes64_rt(uint64_t v, int m) {
-  switch (m) {
-    case 1: return xor_lanes64<1>(v);
-    case 2: return xor_lanes64<2>(v);
-    case 4: return xor_lanes64<4>(v);
-    case 8: return xor_lanes64<8>(v);
-    case 16: return xor_lanes64<16>(v);
-    default: return xor_lanes64<32>(v);
-  }
-}
-
 // Value of lane - 1 for a whole wave (DPP wave_shr:1); lane 0 gets `fill`.
 __device__ __forceinline__ uint64_t wave_shr1_64(uint64_t v, uint64_t fill) {
   uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)fill, (int)(uint32_t)v, 0x138, 0xF, 0xF, false);
@@ -161,52 +145,117 @@ __device__ __forceinline__ uint64_t wave_shr1_64(uint64_t v, uint64_t fill) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// One compare-exchange stage with partner distance j.  Element e keeps the
-// smaller key when (e is the lower of the pair) == (its block sorts upward).
-// j and k are compile-time constants after unrolling.
+// Lanes (bit l of register r's mask) that keep the smaller key of their pair
+// at the stage with partner distance J inside blocks of K: element
+// e = r * 64 + l sorts upward when ((e & K) == 0) != DESC and is the lower of
+// its pair when (e & J) == 0.
 template <int KPL>
-__device__ __forceinline__ void bitonic_stage(uint64_t (&v)[KPL], int j, int k, bool descending) {
-  const int l = lane_id();
-  if (j >= kWave) {
-    const int rj = j / kWave;
-#pragma unroll
-    for (int r = 0; r < KPL; ++r) {
-      if (r & rj) continue;
+struct LaneMasks {
+  uint64_t m[KPL];
+};
+template <int KPL, int J, int K, bool DESC>
+__host__ __device__ constexpr LaneMasks<KPL> keep_min_lanes() {
+  LaneMasks<KPL> x{};
+  for (int r = 0; r < KPL; ++r) {
+    uint64_t m = 0;
+    for (int l = 0; l < kWave; ++l) {
       const int e = r * kWave + l;
-      bool up = ((e & k) == 0) != descending;
-      uint64_t a = v[r], b = v[r | rj];
-      v[r] = up ? min64(a, b) : max64(a, b);
-      v[r | rj] = up ? max64(a, b) : min64(a, b);
+      if ((((e & K) == 0) != DESC) == ((e & J) == 0)) m |= 1ull << l;
     }
+    x.m[r] = m;
+  }
+  return x;
+}
+
+// m ^ (HI:LO) by two scalar XORs with literal operands.  Written as
+// instructions so that the constants are not hoisted out of loops into
+// registers (which then spill to VGPR lanes).
+template <uint32_t LO, uint32_t HI>
+__device__ __forceinline__ uint64_t xor_mask(uint64_t m) {
+  uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+  if constexpr (LO != 0) asm volatile("s_xor_b32 %0, %0, %1" : "+s"(lo) : "i"(LO));
+  if constexpr (HI != 0) asm volatile("s_xor_b32 %0, %0, %1" : "+s"(hi) : "i"(HI));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// One compare-exchange of a lane pair at distance J < 64.  Each lane sees
+// both keys of its pair, (a, b) = (lower lane's, upper lane's), and takes b
+// when (b < a) equals its keep-min bit (KEEP_MIN), else a: one 64-bit
+// compare whose lane mask is XORed with the constant, then two selects.
+template <int J, uint64_t KEEP_MIN>
+__device__ __forceinline__ uint64_t exchange_lanes(uint64_t v) {
+  constexpr uint64_t kFlip = ~KEEP_MIN;  // take b where lt ^ flip is set
+  if constexpr (J >= 16) {
+    // permlane swap: the first result holds the pair's lower element in every
+    // lane, the second its upper element
+    const int vl = (int)(uint32_t)v, vh = (int)(uint32_t)(v >> 32);
+    const auto lo = J == 16 ? __builtin_amdgcn_permlane16_swap(vl, vl, false, false)
+                            : __builtin_amdgcn_permlane32_swap(vl, vl, false, false);
+    const auto hi = J == 16 ? __builtin_amdgcn_permlane16_swap(vh, vh, false, false)
+                            : __builtin_amdgcn_permlane32_swap(vh, vh, false, false);
+    const uint64_t a = ((uint64_t)(uint32_t)hi[0] << 32) | (uint32_t)lo[0];
+    const uint64_t b = ((uint64_t)(uint32_t)hi[1] << 32) | (uint32_t)lo[1];
+    const uint64_t t = xor_mask<(uint32_t)kFlip, (uint32_t)(kFlip >> 32)>(ballot(b < a));
+    return __builtin_amdgcn_inverse_ballot_w64(t) ? b : a;
   } else {
-#pragma unroll
-    for (int r = 0; r < KPL; ++r) {
-      const int e = r * kWave + l;
-      bool up = ((e & k) == 0) != descending;
-      bool lower = (l & j) == 0;
-      uint64_t o = xor_lanes64_rt(v[r], j);
-      v[r] = (lower == up) ? min64(v[r], o) : max64(v[r], o);
-    }
+    // the partner's value o stands in for the other element: the lower lane
+    // sees (v, o), the upper (o, v), and "take o" covers both
+    const uint64_t o = xor_lanes64<J>(v);
+    const uint64_t t = xor_mask<(uint32_t)kFlip, (uint32_t)(kFlip >> 32)>(ballot(o < v));
+    return __builtin_amdgcn_inverse_ballot_w64(t) ? o : v;
   }
 }
 
-// Full sort of P keys (ascending unless `descending`).
-template <int KPL>
-__device__ __forceinline__ void bitonic_sort(uint64_t (&v)[KPL], bool descending) {
-  constexpr int P = KPL * kWave;
+template <int KPL, int J, int K, bool DESC, int R>
+__device__ __forceinline__ void exchange_registers_from(uint64_t (&v)[KPL]) {
+  v[R] = exchange_lanes<J, keep_min_lanes<KPL, J, K, DESC>().m[R]>(v[R]);
+  if constexpr (R + 1 < KPL) exchange_registers_from<KPL, J, K, DESC, R + 1>(v);
+}
+
+// One stage with partner distance J of the network over blocks of K.
+template <int KPL, int J, int K, bool DESC>
+__device__ __forceinline__ void bitonic_stage(uint64_t (&v)[KPL]) {
+  if constexpr (J >= kWave) {
+    constexpr LaneMasks<KPL> km = keep_min_lanes<KPL, J, K, DESC>();
+    constexpr int rj = J / kWave;
 #pragma unroll
-  for (int k = 2; k <= P; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) bitonic_stage<KPL>(v, j, k, descending);
+    for (int r = 0; r < KPL; ++r) {
+      if (r & rj) continue;
+      // both elements sort the same way (the block direction is uniform per register)
+      const bool up = (km.m[r] & 1ull) != 0;
+      const uint64_t a = v[r], b = v[r | rj];
+      const bool lt = b < a;
+      v[r] = (lt == up) ? b : a;
+      v[r | rj] = (lt == up) ? a : b;
+    }
+  } else {
+    exchange_registers_from<KPL, J, K, DESC, 0>(v);
   }
+}
+
+template <int KPL, int J, int K, bool DESC>
+__device__ __forceinline__ void bitonic_stages(uint64_t (&v)[KPL]) {
+  bitonic_stage<KPL, J, K, DESC>(v);
+  if constexpr (J > 1) bitonic_stages<KPL, J / 2, K, DESC>(v);
+}
+
+template <int KPL, int K, bool DESC>
+__device__ __forceinline__ void bitonic_sort_from(uint64_t (&v)[KPL]) {
+  bitonic_stages<KPL, K / 2, K, DESC>(v);
+  if constexpr (K < KPL * kWave) bitonic_sort_from<KPL, 2 * K, DESC>(v);
+}
+
+// Full sort of P = 64 * KPL keys held as v[r] at element r * 64 + lane
+// (ascending unless DESC).
+template <int KPL, bool DESC>
+__device__ __forceinline__ void bitonic_sort(uint64_t (&v)[KPL]) {
+  bitonic_sort_from<KPL, 2, DESC>(v);
 }
 
 // Sorts a bitonic sequence of P keys ascending.
 template <int KPL>
 __device__ __forceinline__ void bitonic_merge_up(uint64_t (&v)[KPL]) {
-  constexpr int P = KPL * kWave;
-#pragma unroll
-  for (int j = P >> 1; j > 0; j >>= 1) bitonic_stage<KPL>(v, j, 2 * P, false);
+  bitonic_stages<KPL, KPL * kWave / 2, 2 * KPL * kWave, false>(v);
 }
 
 }  // namespace gorio
