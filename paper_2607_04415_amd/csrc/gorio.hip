@@ -499,6 +499,7 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   p.out_ids = d_ids;
   p.out_dists = static_cast<uint32_t *>(d_dists);
   p.stats = ix->d_stats;
+  p.next_query = ix->d_stats + kStatNextQuery;
 
   gorio_status st;
   bool timed_out = false;

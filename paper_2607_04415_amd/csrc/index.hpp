@@ -25,6 +25,7 @@ enum StatWord : int {
   kStatServed,
   kStatPark,
   kStatResume,
+  kStatNextQuery,  // resident kernel: queries handed out past the first grid
   kStatWords = 16
 };
 

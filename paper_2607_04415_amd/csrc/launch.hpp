@@ -5,12 +5,15 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "search_paged.hpp"
 #include "search_resident.hpp"
 
 namespace gorio {
 
-// Resident search, one workgroup per query (grid <= nq, queries strided).
+// Resident search: one wave per query at a time, at most `grid` workgroups
+// (queries past the grid are handed out by the kernel's counter).
 hipError_t launch_resident_u8(const ResidentParams &p, int grid, hipStream_t s);
 hipError_t launch_resident_f32(const ResidentParams &p, int grid, hipStream_t s);
 
@@ -24,14 +27,29 @@ using ResidentHtLarge = VisitedLds<13>;
 
 namespace detail {
 
+// One workgroup per wave slot the device holds at once (queries beyond the
+// grid are taken from the kernel's counter), at most `grid`.
+template <auto Kernel>
+hipError_t launch_resident_grid(const ResidentParams &p, int grid, hipStream_t s) {
+  static int slots = 0;  // per kernel
+  if (slots == 0) {
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(Kernel), kWave, 0);
+    if (e != hipSuccess) return e;
+    slots = std::max(1, cus * per_cu);
+  }
+  Kernel<<<std::min(grid, slots), kWave, 0, s>>>(p);
+  return hipGetLastError();
+}
+
 template <int KPL, class M, bool N2S>
 hipError_t resident_t(const ResidentParams &p, int grid, hipStream_t s) {
   using Small = VisitedLds16<M::kHtLog2>;
-  if (p.n <= Small::kMaxId)
-    search_resident<KPL, M, Small, N2S><<<grid, kWave, 0, s>>>(p);
-  else
-    search_resident<KPL, M, ResidentHtLarge, N2S><<<grid, kWave, 0, s>>>(p);
-  return hipGetLastError();
+  if (p.n <= Small::kMaxId) return launch_resident_grid<search_resident<KPL, M, Small, N2S>>(p, grid, s);
+  return launch_resident_grid<search_resident<KPL, M, ResidentHtLarge, N2S>>(p, grid, s);
 }
 
 // frontier slots per lane (L <= 64 KPL) and node_to_slot presence

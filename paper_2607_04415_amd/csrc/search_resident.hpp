@@ -38,11 +38,16 @@ struct ResidentParams {
   uint32_t *out_ids;       // nq x k
   uint32_t *out_dists;     // nq x k distance bits (int32 or float32)
   unsigned long long *stats;  // [evaluations, reevaluations, expansions, iterations]
+  unsigned long long *next_query;  // zero at launch: queries handed out past the first grid
 };
 
 // Several waves per SIMD (M::kWavesPerSimd: 4 for uint8 rows up to 128 bytes,
 // with an 8 KB visited table; 2 otherwise): one wave's gathers overlap the
-// others' filtering and merging.
+// others' filtering and merging.  The grid is as large as the chip holds at
+// once; workgroup b starts with query b and then takes the next unclaimed
+// query from a global counter, so the XCDs and CUs that finish early take
+// more queries and the batch ends when the last queries end, wherever they
+// run.
 template <int KPL, class M, class HT, bool N2S>
 __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(ResidentParams p) {
   constexpr int kChunks = M::kChunks;
@@ -60,7 +65,7 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
 
   unsigned long long n_eval = 0, n_reeval = 0, n_exp = 0, n_iter = 0;
 
-  for (uint32_t qi = blockIdx.x; qi < p.nq; qi += gridDim.x) {
+  for (uint32_t qi = blockIdx.x; qi < p.nq;) {
     HT::clear(ht);
     M m;
     m.load_query(p.queries, qi, p.D, qbuf);
@@ -213,6 +218,9 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
         p.out_dists[(uint64_t)qi * p.k + e] = ok ? (uint32_t)(F[r] >> 32) : M::kPadDist;
       }
     }
+    uint32_t next = 0;
+    if (l == 0) next = (uint32_t)atomicAdd(p.next_query, 1ull);
+    qi = gridDim.x + first_lane_value(next);
   }
 
   if (l == 0) {
