@@ -118,9 +118,61 @@ __device__ __forceinline__ void merge_dedupe(uint64_t (&F)[KPL], uint64_t c_desc
   for (int r = 0; r < KPL; ++r) F[r] = big[r];
 }
 
+
 // Up to this many keys below the L-th frontier key are inserted one by one;
-// more go through the sorting network (measured on the 1M uint8 index: 6,
-// 12, 20, 32, 64 -> 1.20, 1.11, 1.09, 1.08, 1.10 ms per 10k-query launch).
-constexpr uint32_t kInsertMax = 32;
+// more go through the sorting network (measured on the 1M uint8 index, 64-key
+// chunks: 6, 12, 32 -> 0.848, 0.836, 0.846 ms per 10k-query launch).
+constexpr uint32_t kInsertMax = 12;
+
+// Sort-and-merge path for a one-register frontier, kept out of line: it is
+// rare after the first iterations, and one copy keeps the kernel small.
+static __device__ __noinline__ uint64_t sort_merge_1(uint64_t f, uint64_t key, bool forgot) {
+  uint64_t F[1] = {f};
+  uint64_t cc[1] = {key};
+  bitonic_sort<1, true>(cc);
+  if (!forgot) {
+    F[0] = min64(F[0], cc[0]);
+    bitonic_merge_up<1>(F);
+  } else {
+    merge_dedupe<1>(F, cc[0]);
+  }
+  return F[0];
+}
+
+// Merge one key per lane (kInfKey = none) into F: keys at or above F's L-th
+// key cannot enter; a few survivors are inserted by rank, more are sorted
+// and bitonic-merged (with dedupe once the visited filter has forgotten a
+// node).  Slots past L are cleared.
+template <int KPL>
+__device__ __forceinline__ void merge_keys(uint64_t (&F)[KPL], uint64_t key, bool forgot, uint32_t L) {
+  const uint64_t thr = frontier_at<KPL>(F, L - 1);
+  const bool pass = key < thr;
+  uint64_t pm = ballot(pass);
+  if (pm == 0) return;
+  if (!pass) key = kInfKey;
+  if ((uint32_t)__popcll(pm) <= kInsertMax) {
+    while (pm) {
+      const int lane = __builtin_ctzll(pm);
+      pm &= pm - 1;
+      insert_key<KPL>(F, readlane64(key, lane));
+    }
+  } else if constexpr (KPL == 1) {
+    F[0] = sort_merge_1(F[0], key, forgot);
+  } else {
+    uint64_t cc[1] = {key};
+    bitonic_sort<1, true>(cc);
+    if (!forgot) {
+      // no node can repeat: the P smallest of F and C are min(F, C reversed)
+      F[KPL - 1] = min64(F[KPL - 1], cc[0]);
+      bitonic_merge_up<KPL>(F);
+    } else {
+      merge_dedupe<KPL>(F, cc[0]);
+    }
+  }
+  const uint32_t l = lane_id();
+#pragma unroll
+  for (int r = 0; r < KPL; ++r)
+    if ((uint32_t)(r * kWave + l) >= L) F[r] = kInfKey;
+}
 
 }  // namespace gorio

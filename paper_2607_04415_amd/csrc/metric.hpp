@@ -57,12 +57,13 @@ struct MetricU8 {
     else return v;
   }
 
-  // After compaction of cnt candidates: give the rest of the last round of 8
-  // the fallback node's word, so that every lane of a round loads a vector.
+  // After compaction of cnt candidates: give the rest of the last chunk of 64
+  // the fallback node's word, so that every lane of every round of a chunk
+  // loads a vector (the chunk's load count is then fixed).
   __device__ __forceinline__ static void pad_round(uint32_t *cand, uint32_t cnt, uint32_t fallback_word) {
     if constexpr (LOC16) {
       const uint32_t i = cnt + (uint32_t)lane_id();
-      if (lane_id() < 8 && i < ((cnt + 7u) & ~7u)) cand[cand_pos(i)] = fallback_word;
+      if (i < ((cnt + kWave - 1) & ~(uint32_t)(kWave - 1))) cand[cand_pos(i)] = fallback_word;
     }
   }
 
@@ -93,11 +94,7 @@ struct MetricU8 {
   __device__ __forceinline__ void resident_keys(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
                                                 uint32_t c0, uint32_t cnt, uint32_t fallback,
                                                 uint64_t (&key)[kChunks]) const {
-    if constexpr (LOC16) {
-      static_assert(!N2S, "locators name slots of the identity placement");
-      resident_keys_loc(pages, geom, cand, c0, cnt, fallback, key);
-      return;
-    }
+    static_assert(!LOC16, "with locators the kernel streams chunks (chunk_issue, chunk_key)");
     const int l = lane_id();
     const int g = l >> 3;
     const int gl = l & 7;
@@ -134,59 +131,52 @@ struct MetricU8 {
     }
   }
 
-  // resident_keys with LOC16: lane group g reads its kRounds locators as
-  // consecutive words, loads through a 16-byte-stride buffer resource.  The
-  // caller has filled the positions of the last round past cnt with the
-  // fallback node's word (pad_round).
-  __device__ __forceinline__ void resident_keys_loc(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
-                                                    uint32_t c0, uint32_t cnt, uint32_t fallback,
-                                                    uint64_t (&key)[kChunks]) const {
+  // Streaming gather (LOC16): the candidate list is evaluated in chunks of
+  // 64, eight rounds of eight vectors; the kernel keeps two chunks in flight
+  // (issues the next while reducing and merging the current one).  Group g's
+  // eight locators of chunk c0 / 64 are consecutive words of the compacted
+  // list (cand_pos).  Every chunk issues the same number of loads, so the
+  // compiler's waits before a chunk's use leave the other chunk in flight.
+  struct Chunk {
+    U8Vec<VDW, EXACT> x[8];
+  };
+  __device__ __forceinline__ void chunk_issue(__amdgpu_buffer_rsrc_t rs, const uint32_t *cand, uint32_t c0,
+                                              Chunk &ck) const {
+    static_assert(LOC16 && kRounds == 16, "streaming needs locators and 16 rounds per 128 candidates");
     const int l = lane_id();
     const int g = l >> 3;
     const int gl = l & 7;
-    const __amdgpu_buffer_rsrc_t rs = units16_rsrc(pages, geom);
-    uint32_t loc[kRounds];
-    const uint4 *src = reinterpret_cast<const uint4 *>(cand + c0 + g * kRounds);
+    const uint4 *src = reinterpret_cast<const uint4 *>(cand + (c0 & ~127u) + g * kRounds + ((c0 >> 6) & 1u) * 8u);
+    const uint4 a = src[0], b = src[1];
+    uint32_t loc[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-    for (int i = 0; i < kRounds / 4; ++i) {
-      const uint4 v = src[i];
-      loc[4 * i] = v.x; loc[4 * i + 1] = v.y; loc[4 * i + 2] = v.z; loc[4 * i + 3] = v.w;
-    }
-    // keep the wide reads here, ahead of the rounds (the compiler would
-    // otherwise sink one narrow read, and its wait, into each round)
+    for (int rr = 0; rr < 8; ++rr) asm volatile("" : "+v"(loc[rr]));
+    // all eight rounds: positions past the count hold the fallback's locator
 #pragma unroll
-    for (int rr = 0; rr < kRounds; ++rr) asm volatile("" : "+v"(loc[rr]));
-    U8Vec<VDW, EXACT> x[kRounds];
-#pragma unroll
-    for (int rr = 0; rr < kRounds; ++rr) {
-      if (c0 + rr * 8 >= cnt) break;
-      // (positions past cnt in the last round hold the fallback's locator)
+    for (int rr = 0; rr < 8; ++rr) {
       const uint32_t u = loc[rr] + (uint32_t)gl * (VDW / 4);
 #pragma unroll
       for (int t = 0; t < VDW; t += 4) {
         const u32x4_t v = struct_buffer_load_b128(rs, (int)(u + t / 4), 0, 0, 0);
-        x[rr].w[t] = v.x; x[rr].w[t + 1] = v.y; x[rr].w[t + 2] = v.z; x[rr].w[t + 3] = v.w;
+        ck.x[rr].w[t] = v.x; ck.x[rr].w[t + 1] = v.y; ck.x[rr].w[t + 2] = v.z; ck.x[rr].w[t + 3] = v.w;
       }
     }
-    int dist[kChunks];
+  }
+  // Key of this lane's candidate of the chunk (kInfKey past cnt): lane
+  // (g, gl) ends with round gl of group g, candidate c0 + 8 gl + g.
+  __device__ __forceinline__ uint64_t chunk_key(const PageGeom &geom, const uint32_t *cand, uint32_t c0,
+                                                uint32_t cnt, const Chunk &ck) const {
+    const int l = lane_id();
+    const int g = l >> 3;
+    const int gl = l & 7;
+    int part[8];
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      dist[c] = 0;
-      if (c0 + c * kWave >= cnt) break;
-      int part[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) part[j] = c0 + (c * 8 + j) * 8 < cnt ? partial_u8(q, x[c * 8 + j]) : 0;
-      dist[c] = transpose_sum8(part) + qq;
-    }
-    // lane (g, gl) of chunk c holds round 8c + gl of group g: candidate
-    // c0 + (8c + gl) * 8 + g, stored at c0 + g * kRounds + 8c + gl
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      const uint32_t rr = (uint32_t)(c * 8 + gl);
-      const bool ok = c0 + rr * 8 + g < cnt;
-      const uint32_t v = ok ? slot_of_locator(geom, cand[c0 + g * kRounds + rr]) : 0u;
-      key[c] = ok ? (((uint64_t)(uint32_t)dist[c] << 32) | ((uint64_t)v << 1)) : kInfKey;
-    }
+    for (int j = 0; j < 8; ++j) part[j] = partial_u8(q, ck.x[j]);
+    const int dist = transpose_sum8(part) + qq;
+    const bool ok = c0 + (uint32_t)gl * 8 + (uint32_t)g < cnt;
+    const uint32_t pos = (c0 & ~127u) + g * kRounds + ((c0 >> 6) & 1u) * 8u + gl;
+    const uint32_t v = ok ? slot_of_locator(geom, cand[pos]) : 0u;
+    return ok ? (((uint64_t)(uint32_t)dist << 32) | ((uint64_t)v << 1)) : kInfKey;
   }
 
   // Paged: keys of the candidates whose pages are ready (rdy, slot per lane;

@@ -445,31 +445,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
           uint64_t key = m.paged_keys([&](uint32_t si, uint32_t v) { return cached_vec<N2S>(p, si, v); }, crs,
                                       S.cand, t * kWave, rdy[t], rslot[t], mr);
           ctr.eval += cnt;
-          const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
-          const bool pass = key < thr;
-          uint64_t pm = ballot(pass);
-          if (!pass) key = kInfKey;
-          if (pm != 0) {
-            if ((uint32_t)__popcll(pm) <= kInsertMax) {
-              while (pm) {
-                const int lane = __builtin_ctzll(pm);
-                pm &= pm - 1;
-                insert_key<KPL>(F, readlane64(key, lane));
-              }
-            } else {
-              uint64_t cc[1] = {key};
-              bitonic_sort<1, true>(cc);
-              if (!S.forgot) {
-                F[KPL - 1] = min64(F[KPL - 1], cc[0]);
-                bitonic_merge_up<KPL>(F);
-              } else {
-                merge_dedupe<KPL>(F, cc[0]);
-              }
-            }
-#pragma unroll
-            for (int r = 0; r < KPL; ++r)
-              if ((uint32_t)(r * kWave + l) >= p.L) F[r] = kInfKey;
-          }
+          merge_keys<KPL>(F, key, S.forgot != 0, p.L);
           if (rdy[t]) {
             unpin(p.cache, rslot[t]);
             S.cstate[t * kWave + l] = kDone;

@@ -41,6 +41,27 @@ struct ResidentParams {
   unsigned long long *next_query;  // zero at launch: queries handed out past the first grid
 };
 
+// Evaluates NCH chunks of 64 compacted candidates (locator metrics) and
+// merges their keys into F, with two chunks in flight.
+template <int NCH, int KPL, class M>
+__device__ __forceinline__ void eval_chunks(const M &m, const ResidentParams &p, const uint32_t *cand, uint32_t cnt,
+                                            uint64_t (&F)[KPL], bool forgot) {
+  const __amdgpu_buffer_rsrc_t rs = units16_rsrc(p.pages, p.geom);
+  typename M::Chunk A, B;
+  m.chunk_issue(rs, cand, 0, A);
+  if constexpr (NCH > 1) m.chunk_issue(rs, cand, kWave, B);
+  uint64_t key = m.chunk_key(p.geom, cand, 0, cnt, A);
+  if constexpr (NCH > 2) m.chunk_issue(rs, cand, 2 * kWave, A);
+  merge_keys<KPL>(F, key, forgot, p.L);
+  if constexpr (NCH > 1) {
+    key = m.chunk_key(p.geom, cand, kWave, cnt, B);
+    if constexpr (NCH > 3) m.chunk_issue(rs, cand, 3 * kWave, B);
+    merge_keys<KPL>(F, key, forgot, p.L);
+  }
+  if constexpr (NCH > 2) merge_keys<KPL>(F, m.chunk_key(p.geom, cand, 2 * kWave, cnt, A), forgot, p.L);
+  if constexpr (NCH > 3) merge_keys<KPL>(F, m.chunk_key(p.geom, cand, 3 * kWave, cnt, B), forgot, p.L);
+}
+
 // Several waves per SIMD (M::kWavesPerSimd: 4 for uint8 rows up to 128 bytes,
 // with an 8 KB visited table; 2 otherwise): one wave's gathers overlap the
 // others' filtering and merging.  The grid is as large as the chip holds at
@@ -159,50 +180,27 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
         __syncthreads();
         n_eval += cnt;
 
-        // ---- evaluate: gather a batch of vectors in one round trip -------------
-        for (uint32_t c0 = 0; c0 < cnt; c0 += kBatch) {
-          uint64_t key[kChunks];
-          m.template resident_keys<N2S>(p.pages, p.geom, cand, c0, cnt, p.entry, key);
-          const uint64_t thr = frontier_at<KPL>(F, p.L - 1);
-          uint64_t pass_mask[kChunks];
-          uint32_t survivors = 0;
-#pragma unroll
-          for (int c = 0; c < kChunks; ++c) {
-            const bool pass = key[c] < thr;
-            pass_mask[c] = ballot(pass);
-            if (!pass) key[c] = kInfKey;
-            survivors += (uint32_t)__popcll(pass_mask[c]);
+        // ---- evaluate and merge -----------------------------------------------
+        if constexpr (M::kLocators) {
+          // chunks of 64 vectors, two in flight: the next chunk's gathers are
+          // outstanding while this one is reduced and merged (a fixed schedule
+          // per chunk count keeps every wait exact)
+          static_assert(kCandCap == 4 * kWave, "at most four chunks");
+          switch ((cnt + kWave - 1) / kWave) {
+            case 1: eval_chunks<1, KPL>(m, p, cand, cnt, F, forgot); break;
+            case 2: eval_chunks<2, KPL>(m, p, cand, cnt, F, forgot); break;
+            case 3: eval_chunks<3, KPL>(m, p, cand, cnt, F, forgot); break;
+            case 4: eval_chunks<4, KPL>(m, p, cand, cnt, F, forgot); break;
+            default: break;
           }
-          if (survivors == 0) continue;
-          // ---- merge into the frontier ----------------------------------------
-          if (survivors <= kInsertMax) {
+        } else {
+          // batches of kBatch vectors, one round trip each
+          for (uint32_t c0 = 0; c0 < cnt; c0 += kBatch) {
+            uint64_t key[kChunks];
+            m.template resident_keys<N2S>(p.pages, p.geom, cand, c0, cnt, p.entry, key);
 #pragma unroll
-            for (int c = 0; c < kChunks; ++c) {
-              uint64_t pm = pass_mask[c];
-              while (pm) {
-                const int lane = __builtin_ctzll(pm);
-                pm &= pm - 1;
-                insert_key<KPL>(F, readlane64(key[c], lane));
-              }
-            }
-          } else {
-#pragma unroll
-            for (int c = 0; c < kChunks; ++c) {
-              if (pass_mask[c] == 0) continue;
-              uint64_t cc[1] = {key[c]};
-              bitonic_sort<1, true>(cc);
-              if (!forgot) {
-                // no node can repeat: the P smallest of F and C are min(F, C reversed)
-                F[KPL - 1] = min64(F[KPL - 1], cc[0]);
-                bitonic_merge_up<KPL>(F);
-              } else {
-                merge_dedupe<KPL>(F, cc[0]);
-              }
-            }
+            for (int c = 0; c < kChunks; ++c) merge_keys<KPL>(F, key[c], forgot, p.L);
           }
-#pragma unroll
-          for (int r = 0; r < KPL; ++r)
-            if ((uint32_t)(r * kWave + l) >= p.L) F[r] = kInfKey;
         }
         __syncthreads();
       }
