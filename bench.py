@@ -17,6 +17,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 from pathlib import Path
@@ -104,6 +105,25 @@ def recall_at_k(x: np.ndarray, q: np.ndarray, ids: np.ndarray, k: int, sample: i
     return {"value": round(hits / (len(qs) * k), 4), "k": k, "queries": len(qs)}
 
 
+def gather_ceiling(n: int, rpp: int, page_bytes: int, vec_stride: int):
+    """Random 128-byte vector reads from the same page geometry with no search
+    around them (paper_2607_04415_amd/microbench/gather_ceiling.hip): the
+    practical ceiling of the resident kernel's dominant traffic."""
+    from paper_2607_04415_amd import _build
+    exe = _build.GATHER_CEILING
+    if not exe.exists():
+        return None
+    r = subprocess.run([str(exe), str(n), str(rpp), str(page_bytes), str(vec_stride)],
+                       capture_output=True, text=True, timeout=120)
+    if r.returncode != 0:
+        log(f"[bench] gather ceiling probe failed: {r.stderr.strip()}")
+        return None
+    d = json.loads(r.stdout.strip().splitlines()[-1])
+    best = max(d[k]["gbs"] for k in d if k.startswith("rounds_"))
+    return {"gbs": best, "vectors": d["vectors"], "waves": d["waves"],
+            "depths_gbs": {k: d[k]["gbs"] for k in d if k.startswith("rounds_")}}
+
+
 def host_link_peak_gbs(torch) -> float:
     """Pinned host -> HBM copy bandwidth (256 MiB, best of 5), the host-link ceiling."""
     src = torch.empty(1 << 28, dtype=torch.uint8).pin_memory()
@@ -166,6 +186,8 @@ def main():
     ap.add_argument("--recall-sample", type=int, default=100,
                     help="queries whose recall@k against exact top-k is reported (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gather-ceiling", action="store_true",
+                    help="skip the random-gather ceiling probe (microbench/gather_ceiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
     ap.add_argument("--paged-sample", type=int, default=2000,
@@ -279,6 +301,14 @@ def main():
                 "algorithmic_counts": counts_source,
                 "expansions_match_oracle": (None if counts_source != "oracle"
                                             else ocounts["expansions"] == st["expansions"])}
+
+    if not args.no_gather_ceiling and args.layout == "vectors-first" and w.index.dtype == "u8":
+        gc = gather_ceiling(w.index.n, info["records_per_page"], info["page_bytes"], 128)
+        if gc is not None:
+            roofline["gather_ceiling_gbs"] = gc["gbs"]
+            roofline["frac_of_gather_ceiling"] = round(achieved / gc["gbs"], 4)
+            log(f"[bench] random 128-B gather ceiling: {gc['gbs']:,.0f} GB/s "
+                f"({gc['vectors']:,} vectors, {gc['waves']} waves); achieved {achieved:,.0f} GB/s")
 
     recall = None
     if args.recall_sample > 0:

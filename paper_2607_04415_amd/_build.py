@@ -54,7 +54,24 @@ def build(verbose: bool = False, extra: list[str] | None = None, jobs: int | Non
         for o in objs:
             o.unlink(missing_ok=True)
     os.replace(tmp, LIB)
+    build_microbench(verbose)
     return LIB
+
+
+MICROBENCH = PKG / "microbench"
+GATHER_CEILING = MICROBENCH / "gather_ceiling"
+
+
+def build_microbench(verbose: bool = False) -> Path:
+    """The random-gather ceiling probe (a standalone HIP program bench.py runs)."""
+    src = MICROBENCH / "gather_ceiling.hip"
+    tmp = GATHER_CEILING.with_name(GATHER_CEILING.name + f".{os.getpid()}.tmp")
+    cmd = [HIPCC, *FLAGS, "-o", str(tmp), str(src)]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, GATHER_CEILING)
+    return GATHER_CEILING
 
 
 if __name__ == "__main__":
