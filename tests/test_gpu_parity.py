@@ -178,6 +178,43 @@ def test_visited_filter_overflow_still_exact(orc, torch_dev):
     assert st["reevaluations"] > 0, "the test did not exercise the overflow path"
 
 
+def _home_bucket_u8(ids, log2=12):
+    """Home bucket of each id in the resident uint8 kernel's 16-bit visited
+    table with 2^log2 half-words: the top log2 - 3 bits of
+    h = (id * 0x3779B1) mod 2^(log2 + 11) (the hash's 24-bit multiplier)."""
+    h = (ids.astype(np.uint64) * 0x3779B1) % (1 << (log2 + 11))
+    return (h >> 14).astype(np.int64)
+
+
+@pytest.mark.parametrize("vectors_first", [False, True])
+def test_visited_filter_bucket_collisions(orc, torch_dev, vectors_first):
+    """Adjacency lists built to collide in the visited table: 64 neighbours
+    that share one home bucket (seven slots fill, the rest take the next
+    bucket or go unrecorded), lists of a few ids repeated many times (lanes
+    holding the same id), and beams whose lists overlap."""
+    rng = np.random.default_rng(77)
+    n, D, R = 50000, 128, 64
+    x = rng.integers(0, 256, (n, D), dtype=np.uint8)
+    graph = rng.integers(0, n, (n, R), dtype=np.uint32)
+    graph[:, 0] = (np.arange(n, dtype=np.uint32) + 1) % n
+    home = _home_bucket_u8(np.arange(n))
+    buckets = np.bincount(home, minlength=512)
+    b = int(np.argmax(buckets))
+    same = np.flatnonzero(home == b)
+    nxt = np.flatnonzero(home == (b + 1) % 512)
+    assert len(same) >= 64 and len(nxt) >= 64
+    graph[0] = rng.permutation(same)[:64]                       # one bucket, 64 ids
+    for j, v in enumerate(graph[0][:8]):                        # their lists: more of it
+        graph[v] = np.concatenate([rng.permutation(same)[:32], rng.permutation(nxt)[:32]])
+    for v in graph[0][8:16]:                                    # few ids, many copies
+        graph[v] = np.repeat(rng.permutation(same)[:8], 8)
+    for v in graph[0][16:24]:                                   # overlapping lists
+        graph[v] = graph[graph[0][0]]
+    q = rng.integers(0, 256, (96, D), dtype=np.uint8)
+    _, st = check_parity(orc, torch_dev, x, graph, q, 10, 64, 4, entry=0,
+                         layout=dict(vectors_first=vectors_first))
+
+
 def test_more_than_2_24_nodes_uses_the_32bit_table(orc, torch_dev):
     """Above 2^24 nodes the resident kernel's 16-bit visited table cannot hold
     every id; the 32-bit table takes over and results stay exact."""
