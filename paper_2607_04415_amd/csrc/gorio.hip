@@ -319,13 +319,6 @@ extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, ui
 // ---------------------------------------------------------------------------
 namespace {
 
-
-
-
-}  // namespace
-
-namespace {
-
 // Paged search: reset the per-search rings and counters, arm the proxy,
 // launch the persistent kernel and wait for it under a watchdog.
 gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s, bool &timed_out) {
