@@ -140,13 +140,17 @@ def host_link_peak_gbs(torch) -> float:
 
 
 def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: bool = False,
-              vectors_first: bool = False, repeats: int = 5):
+              vectors_first: bool = False, repeats: int = 5, clusters=None):
     """Cold-cache paged searches over the first nq_sample queries of workload w:
     `repeats` timed runs, each after set_cache has emptied the cache; the
-    figures are the median run's."""
+    figures are the median run's.  clusters = (node_to_slot, centroids): pages
+    placed cluster by cluster and queries admitted cluster by cluster."""
     from workload import query_array
     q = query_array(w.index, w.queries)[:nq_sample]
-    ix = g.Index(a["x"], a["graph"], vectors_first=vectors_first)
+    ix = g.Index(a["x"], a["graph"], vectors_first=vectors_first,
+                 node_to_slot=None if clusters is None else clusters[0])
+    if clusters is not None:
+        ix.set_query_order(clusters[1])
     qd = torch.from_numpy(q).cuda()
     ids = torch.empty((len(q), w.k), dtype=torch.int32, device="cuda")
     dists = torch.empty((len(q), w.k), dtype=torch.int32 if q.dtype == np.uint8 else torch.float32,
@@ -166,6 +170,7 @@ def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: boo
     ms = st["kernel_ms"]
     acc = st["hits"] + st["misses"]
     out = {"workload": w.name, "queries": len(q), "blocking": blocking,
+           "placement": "identity" if clusters is None else f"clusters ({len(clusters[1])}, queries by cluster)",
            "cache_slots": ix.info["cache_slots"], "latency_us": w.latency_us,
            "oversub": 1 if blocking else w.oversub, "runs": len(runs),
            "qps": round(len(q) / wall, 1), "qps_runs": [round(len(q) / r[0], 1) for r in runs],
@@ -199,6 +204,8 @@ def main():
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
     ap.add_argument("--paged-sample", type=int, default=2000,
                     help="queries of each paged configuration to run (0 = skip the paged legs)")
+    ap.add_argument("--paged-clusters", type=int, default=256,
+                    help="paged legs: k-means clusters for page placement and query admission (0 = off)")
     ap.add_argument("--paged-repeats", type=int, default=5,
                     help="cold-cache runs per paged leg (the median is reported)")
     ap.add_argument("--f32-sample", type=int, default=0,
@@ -329,20 +336,30 @@ def main():
     if args.paged_sample > 0 and w.name == "u8-1m-hbm":
         link = host_link_peak_gbs(torch)
         legs = []
-        for name, blocking in (("u8-1m-cache10-lat0", False), ("u8-1m-cache10-lat0", True),
-                               ("u8-1m-cache10-lat20", False)):
+        clusters = None
+        if args.paged_clusters > 0:
+            t0 = time.perf_counter()
+            clusters = g.cluster_order(a["x"], args.paged_clusters)
+            log(f"[bench] cluster placement ({args.paged_clusters} clusters) in {time.perf_counter() - t0:.1f} s")
+        plan = [("u8-1m-cache10-lat0", False, clusters), ("u8-1m-cache10-lat0", True, clusters),
+                ("u8-1m-cache10-lat20", False, clusters)]
+        if clusters is not None:
+            plan.append(("u8-1m-cache10-lat20", False, None))   # identity placement, index order
+        for name, blocking, cl in plan:
             leg, pi, pd, pq = paged_leg(torch, g, a, WORKLOADS[name], args.paged_sample, qps, blocking,
                                         vectors_first=args.layout == "vectors-first",
-                                        repeats=args.paged_repeats)
+                                        repeats=args.paged_repeats, clusters=cl)
             # the paged results must equal the resident results on the same queries
             if WORKLOADS[name].queries == w.queries:
                 leg["equals_resident"] = bool(np.array_equal(pi, gi[:len(pq)]) and np.array_equal(pd, gd[:len(pq)]))
-            log(f"[bench] paged {name} blocking={blocking}: {leg['qps']:,.0f} q/s, hit rate "
+            log(f"[bench] paged {name} blocking={blocking} {leg['placement']}: {leg['qps']:,.0f} q/s, hit rate "
                 f"{leg['hit_rate']:.3f}, miss service {leg['miss_service_gbs']} GB/s")
             legs.append(leg)
         miss_gbs = legs[0]["miss_service_gbs"]
         paged = {"host_link_peak_gbs": round(link, 1), "legs": legs,
                  "split_phase_vs_blocking": round(legs[0]["qps"] / max(1e-9, legs[1]["qps"]), 3)}
+        if clusters is not None:
+            paged["clusters_vs_identity"] = round(legs[2]["qps"] / max(1e-9, legs[3]["qps"]), 3)
 
     if args.f32_sample > 0:
         wf = WORKLOADS["f32-10m-cache5-lat20"]
@@ -356,8 +373,14 @@ def main():
         ri, rd = ri.cpu().numpy().view(np.uint32), rd.cpu().numpy()
         rqps = len(qf) / (rst["kernel_ms"] * 1e-3)
         ixr.close()
+        fclusters = None
+        if args.paged_clusters > 0:
+            t0 = time.perf_counter()
+            fclusters = g.cluster_order(af["x"], args.paged_clusters)
+            log(f"[bench] {wf.name}: cluster placement ({args.paged_clusters} clusters) in "
+                f"{time.perf_counter() - t0:.1f} s")
         leg, pi, pd, _ = paged_leg(torch, g, af, wf, args.f32_sample, rqps,
-                                   vectors_first=args.layout == "vectors-first", repeats=1)
+                                   vectors_first=args.layout == "vectors-first", repeats=1, clusters=fclusters)
         leg["resident_kernel_qps"] = round(rqps, 1)
         leg["equals_resident"] = bool(np.array_equal(pi, ri) and np.array_equal(pd.view(np.uint32), rd.view(np.uint32)))
         log(f"[bench] paged {wf.name}: {leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, "

@@ -196,6 +196,46 @@ gorio_status gorio_copy_pages(const gorio_index *ix, uint64_t first, uint64_t co
 gorio_status gorio_locality_order(const uint32_t *graph, uint64_t n, uint32_t R, uint32_t entry,
                                   uint32_t records_per_page, uint32_t *node_to_slot);
 
+/*
+ * Cluster placement (host call; runs on the current HIP device): k-means on
+ * the vectors, then node_to_slot places the nodes cluster by cluster (id order
+ * inside a cluster), for use as gorio_page_layout.node_to_slot.  Graph pages
+ * are the unit of I/O (Sec. 3.1) and page layout and graph locality decide how
+ * much of a fetched page a search uses (Sec. 6, DiskANN and Starling); a paged
+ * cache holds a few clusters' pages at once, so placing nodes by cluster and
+ * admitting queries by cluster (gorio_set_query_order) lets queries in flight
+ * reuse each other's pages.
+ *   vectors:    host, n x D row-major, uint8 or float32 per dtype.
+ *   clusters:   K centroids, 1 <= K <= min(n, 65536).  Initial centroids are the
+ *               vectors of nodes floor(i n / K); then `iterations` (<= 64) Lloyd
+ *               steps (nearest centroid by squared L2 in float32 on the GPU, ties to
+ *               the smaller index; each centroid becomes the mean of its members,
+ *               an empty one stays).
+ *   node_to_slot: host out, n entries, a permutation of [0, n).
+ *   centroids:  host out, K x D float32 (the final centroids).
+ * Deterministic.  Results of a search never depend on the placement.
+ * Errors: GORIO_EINVAL for NULL pointers or n, D (1..1024), K, iterations out of
+ * range; GORIO_ENOMEM / GORIO_EDEVICE from the device.
+ */
+gorio_status gorio_cluster_order(gorio_dtype dtype, const void *vectors, uint64_t n, uint32_t D,
+                                 uint32_t clusters, uint32_t iterations, uint32_t *node_to_slot,
+                                 float *centroids);
+
+/*
+ * Admission order of paged searches (the persistent scheduler of Sec. 3.3
+ * decides which query a free slot takes next): with K > 0 centroids each paged
+ * search first assigns every query to its nearest centroid (squared L2 in
+ * float32, ties to the smaller index) and admits the queries cluster by
+ * cluster, in index order inside a cluster, so the queries in flight share
+ * pages (the cross-query reuse that Sec. 7.2 names as miss coalescing).  Each
+ * query's answer is unchanged and is written to its own row.  Resident
+ * searches ignore the order.
+ *   centroids: host, K x D float32 (e.g. from gorio_cluster_order); copied.
+ *   clusters:  K, 0 <= K <= 65536; 0 restores index order.
+ * Errors: GORIO_EINVAL for a NULL index, K > 65536, or NULL centroids with K > 0.
+ */
+gorio_status gorio_set_query_order(gorio_index *ix, const float *centroids, uint32_t clusters);
+
 /* Release everything the index owns.  NULL is a no-op. */
 void gorio_free_index(gorio_index *ix);
 

@@ -55,9 +55,9 @@ class IndexInfo(ctypes.Structure):
 
 
 # every symbol include/gorio.h declares
-EXPORTS = ("gorio_build_index", "gorio_set_cache", "gorio_set_backing", "gorio_search",
-           "gorio_index_info_get", "gorio_copy_pages", "gorio_locality_order", "gorio_free_index",
-           "gorio_last_error")
+EXPORTS = ("gorio_build_index", "gorio_set_cache", "gorio_set_backing", "gorio_set_query_order",
+           "gorio_search", "gorio_index_info_get", "gorio_copy_pages", "gorio_locality_order",
+           "gorio_cluster_order", "gorio_free_index", "gorio_last_error")
 
 _lib = None
 
@@ -86,6 +86,10 @@ def lib() -> ctypes.CDLL:
         L.gorio_copy_pages.argtypes = [v, u64, u64, v]
         L.gorio_locality_order.restype = i32
         L.gorio_locality_order.argtypes = [v, u64, u32, u32, u32, v]
+        L.gorio_cluster_order.restype = i32
+        L.gorio_cluster_order.argtypes = [i32, v, u64, u32, u32, u32, v, v]
+        L.gorio_set_query_order.restype = i32
+        L.gorio_set_query_order.argtypes = [v, v, u32]
         L.gorio_free_index.restype = None
         L.gorio_free_index.argtypes = [v]
         L.gorio_last_error.restype = ctypes.c_char_p
@@ -115,6 +119,21 @@ def locality_order(graph: np.ndarray, entry: int, records_per_page: int) -> np.n
     _check(lib().gorio_locality_order(graph.ctypes.data, graph.shape[0], graph.shape[1], int(entry),
                                       int(records_per_page), out.ctypes.data))
     return out
+
+
+def cluster_order(vectors: np.ndarray, clusters: int, iterations: int = 4):
+    """(node_to_slot, centroids): nodes placed cluster by cluster after
+    `iterations` Lloyd steps of k-means on the GPU (gorio_cluster_order)."""
+    vectors = np.ascontiguousarray(vectors)
+    dt = U8 if vectors.dtype == np.uint8 else F32
+    if dt == F32:
+        vectors = np.ascontiguousarray(vectors, dtype=np.float32)
+    n, D = vectors.shape
+    n2s = np.empty(n, np.uint32)
+    cent = np.empty((clusters, D), np.float32)
+    _check(lib().gorio_cluster_order(dt, vectors.ctypes.data, n, D, int(clusters), int(iterations),
+                                     n2s.ctypes.data, cent.ctypes.data))
+    return n2s, cent
 
 
 class Index:
@@ -169,6 +188,14 @@ class Index:
                     blocking: bool = False):
         _check(lib().gorio_set_backing(self._h, float(latency_us), int(max_outstanding),
                                        int(oversub), int(bool(blocking))))
+
+    def set_query_order(self, centroids: np.ndarray | None):
+        """Paged searches admit queries by nearest centroid (None: index order)."""
+        if centroids is None:
+            _check(lib().gorio_set_query_order(self._h, None, 0))
+            return
+        c = np.ascontiguousarray(centroids, dtype=np.float32)
+        _check(lib().gorio_set_query_order(self._h, c.ctypes.data, c.shape[0]))
 
     def pages(self, first: int = 0, count: int | None = None) -> np.ndarray:
         info = self.info

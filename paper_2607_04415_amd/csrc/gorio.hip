@@ -11,6 +11,7 @@
 
 #include "../../include/gorio.h"
 #include "build_kernels.hpp"
+#include "cluster.hpp"
 #include "index.hpp"
 #include "launch.hpp"
 
@@ -301,6 +302,26 @@ extern "C" gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes) {
   return ix->make_paged(bytes / ix->page_bytes);
 }
 
+extern "C" gorio_status gorio_set_query_order(gorio_index *ix, const float *centroids, uint32_t clusters) {
+  if (!ix) return fail(GORIO_EINVAL, "index is NULL");
+  if (clusters > kMaxClusters) return fail(GORIO_EINVAL, "clusters=%u above %u", clusters, kMaxClusters);
+  if (clusters > 0 && !centroids) return fail(GORIO_EINVAL, "centroids must be non-NULL");
+  DeviceGuard dg(ix->device);
+  if (ix->d_centroids) (void)hipFree(ix->d_centroids);
+  if (ix->d_centroid_norms) (void)hipFree(ix->d_centroid_norms);
+  ix->d_centroids = ix->d_centroid_norms = nullptr;
+  ix->order_clusters = 0;
+  if (clusters == 0) return GORIO_OK;
+  std::vector<float> cc(clusters);
+  centroid_norms(centroids, clusters, ix->D, cc.data());
+  HIP_OR_FAIL(hipMalloc(&ix->d_centroids, (size_t)clusters * ix->D * 4));
+  HIP_OR_FAIL(hipMalloc(&ix->d_centroid_norms, (size_t)clusters * 4));
+  HIP_OR_FAIL(hipMemcpy(ix->d_centroids, centroids, (size_t)clusters * ix->D * 4, hipMemcpyHostToDevice));
+  HIP_OR_FAIL(hipMemcpy(ix->d_centroid_norms, cc.data(), (size_t)clusters * 4, hipMemcpyHostToDevice));
+  ix->order_clusters = clusters;
+  return GORIO_OK;
+}
+
 extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, uint32_t max_outstanding,
                                           uint32_t oversub, int blocking) {
   if (!ix) return fail(GORIO_EINVAL, "index is NULL");
@@ -390,6 +411,21 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.L = rp.L;
   pp.W = rp.W;
   pp.next_query = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kNextQuery));
+  // admission order: cluster by cluster of the queries' nearest centroids
+  DevBuf d_key, d_order;
+  pp.order = nullptr;
+  if (ix->order_clusters > 0) {
+    HIP_OR_FAIL(d_key.alloc((size_t)rp.nq * 4));
+    HIP_OR_FAIL(d_order.alloc((size_t)rp.nq * 4));
+    HIP_OR_FAIL(launch_nearest_centroid(ix->dtype, rp.queries, rp.nq, ix->D, ix->d_centroids, ix->d_centroid_norms,
+                                        ix->order_clusters, d_key.as<uint32_t>(), s));
+    std::vector<uint32_t> key(rp.nq), order(rp.nq);
+    HIP_OR_FAIL(hipMemcpyAsync(key.data(), d_key.p, (size_t)rp.nq * 4, hipMemcpyDeviceToHost, s));
+    HIP_OR_FAIL(hipStreamSynchronize(s));
+    order_by_key(key.data(), rp.nq, ix->order_clusters, order.data());
+    HIP_OR_FAIL(hipMemcpyAsync(d_order.p, order.data(), (size_t)rp.nq * 4, hipMemcpyHostToDevice, s));
+    pp.order = d_order.as<uint32_t>();
+  }
   pp.done_queries = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kDoneQueries));
   pp.fill_waves = (uint32_t)fwaves;
   pp.out_ids = rp.out_ids;

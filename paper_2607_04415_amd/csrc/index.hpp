@@ -112,6 +112,11 @@ struct gorio_index {
   uint32_t oversub = 1;
   int blocking = 0;
 
+  // paged searches admit their queries cluster by cluster (gorio_set_query_order)
+  uint32_t order_clusters = 0;
+  float *d_centroids = nullptr;       // order_clusters x D float32
+  float *d_centroid_norms = nullptr;  // order_clusters
+
   hipStream_t stream = nullptr;  // library-internal work (build, mode switches)
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;
   unsigned long long *d_stats = nullptr;
@@ -171,6 +176,8 @@ struct gorio_index {
     if (h_backing) (void)hipHostFree(h_backing);
     if (d_node_to_slot) (void)hipFree(d_node_to_slot);
     if (d_stats) (void)hipFree(d_stats);
+    if (d_centroids) (void)hipFree(d_centroids);
+    if (d_centroid_norms) (void)hipFree(d_centroid_norms);
     if (ev_start) (void)hipEventDestroy(ev_start);
     if (ev_stop) (void)hipEventDestroy(ev_stop);
     if (stream) (void)hipStreamDestroy(stream);
@@ -178,6 +185,8 @@ struct gorio_index {
     h_backing = nullptr;
     d_node_to_slot = nullptr;
     d_stats = nullptr;
+    d_centroids = d_centroid_norms = nullptr;
+    order_clusters = 0;
     ev_start = ev_stop = nullptr;
     stream = nullptr;
   }

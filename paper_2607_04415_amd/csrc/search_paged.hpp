@@ -57,6 +57,7 @@ struct PagedParams {
   const void *queries;                    // nq x D elements
   uint32_t nq, k, L, W;
   unsigned int *next_query;
+  const uint32_t *order;                  // nullptr: queries in index order; else admission order
   unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
   uint32_t *out_ids;
   uint32_t *out_dists;                    // distance bits (int32 or float32)
@@ -542,6 +543,7 @@ __global__ __launch_bounds__(kWave) void search_paged(PagedParams p) {
           admitting = false;
           continue;
         }
+        if (p.order) qi = first_lane_value(p.order[qi]);
         VisitedHbm<kPagedHtLog2>::clear(ht);
         // V = {entry}: the entry is the first candidate to evaluate
         if (l == 0) {

@@ -82,3 +82,18 @@ def test_build_needs_out_pointer(lib):
     x = np.zeros((4, 4), np.uint8)
     gr = np.zeros((4, 2), np.uint32)
     assert lib.gorio_build_index(0, x.ctypes.data, 4, 4, gr.ctypes.data, 2, None, g.NO_EDGE, None) == g.EINVAL
+
+
+def test_cluster_order_rejects_bad_arguments(lib):
+    """Argument checks come before any device work (no GPU needed)."""
+    x = np.zeros((10, 4), np.uint8)
+    n2s = np.empty(10, np.uint32)
+    cent = np.empty((16, 4), np.float32)
+    p = (x.ctypes.data, n2s.ctypes.data, cent.ctypes.data)
+    for dt, n, D, K, it in ((0, 10, 4, 0, 2), (0, 10, 4, 11, 2), (0, 10, 4, 2, 65), (0, 0, 4, 1, 1),
+                            (0, 10, 0, 2, 1), (0, 10, 1025, 2, 1), (5, 10, 4, 2, 1)):
+        assert lib.gorio_cluster_order(dt, p[0], n, D, K, it, p[1], p[2]) == g.EINVAL
+        assert lib.gorio_last_error().decode()
+    assert lib.gorio_cluster_order(0, None, 10, 4, 2, 1, p[1], p[2]) == g.EINVAL
+    assert lib.gorio_cluster_order(0, p[0], 10, 4, 2, 1, None, p[2]) == g.EINVAL
+    assert lib.gorio_set_query_order(None, None, 0) == g.EINVAL

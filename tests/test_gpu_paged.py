@@ -347,3 +347,71 @@ def test_paged_random_configuration(orc, torch_dev, seed):
     gi, gd, st = search(torch_dev, ix, q, k, L, W)
     assert_same(gi, gd, oids, od)
     assert st["expansions"] == int(oc["expansions"].sum())
+
+
+# --------------------------------------------------------------------------- #
+# cluster placement and cluster-ordered admission
+# --------------------------------------------------------------------------- #
+def test_cluster_order_places_clusters_contiguously(torch_dev):
+    """gorio_cluster_order: a permutation that lists the nodes grouped by their
+    nearest returned centroid (checked in float64, near-ties excepted), with
+    centroids inside the data's range; deterministic."""
+    rng = np.random.default_rng(5)
+    K, per, D = 8, 1500, 32
+    centres = rng.uniform(30, 225, (K, D))
+    lab = np.repeat(np.arange(K), per)
+    rng.shuffle(lab)
+    x = np.clip(np.rint(centres[lab] + 4 * rng.standard_normal((K * per, D))), 0, 255).astype(np.uint8)
+    for clusters in (8, 32):
+        n2s, cent = g.cluster_order(x, clusters, iterations=6)
+        assert np.array_equal(np.sort(n2s), np.arange(len(x), dtype=np.uint32))
+        assert cent.shape == (clusters, D) and np.isfinite(cent).all()
+        assert (cent >= 0).all() and (cent <= 255).all()
+        d = ((x.astype(np.float64)[:, None, :] - cent.astype(np.float64)[None]) ** 2).sum(2)
+        srt = np.sort(d, axis=1)
+        clear = srt[:, 1] - srt[:, 0] > 1e-3 * np.maximum(srt[:, 0], 1.0)
+        key = np.argmin(d, axis=1)[np.argsort(n2s)]
+        ok = clear[np.argsort(n2s)]
+        kk = key[ok]
+        assert (np.diff(kk) >= 0).all(), "slots are not grouped by nearest centroid"
+        n2s2, cent2 = g.cluster_order(x, clusters, iterations=6)
+        assert np.array_equal(n2s, n2s2) and np.array_equal(cent, cent2)
+    # with more centroids than blobs, each cluster stays inside one blob
+    by_slot = lab[np.argsort(n2s)]
+    runs = 1 + int((by_slot[1:] != by_slot[:-1]).sum())
+    assert runs <= 32, runs
+
+
+@pytest.mark.parametrize("vfirst,blocking", [(True, False), (False, False), (True, True)])
+def test_paged_cluster_placement_and_query_order(orc, torch_dev, small, vfirst, blocking):
+    """Cluster placement plus cluster-ordered admission: answers equal the
+    oracle's (which packs with the same placement) and the plain search's."""
+    a, q, oids, od, oc = small
+    n2s, cent = g.cluster_order(a["x"], 16)
+    ix = g.Index(a["x"], a["graph"], node_to_slot=n2s, vectors_first=vfirst)
+    assert ix.info["entry"] == orc.medoid(a["x"])
+    ix.set_cache(int(0.15 * ix.info["index_bytes"]))
+    ix.set_backing(latency_us=2.0, oversub=1 if blocking else 4, blocking=blocking)
+    ix.set_query_order(cent)
+    gi, gd, st = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    assert st["misses"] > 0
+    ix.set_query_order(None)                       # index order again
+    gi, gd, _ = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    ix.close()
+
+
+def test_query_order_resident_and_empty_batch(orc, torch_dev, small):
+    """The order is ignored by resident searches; nq = 0 is a no-op."""
+    a, q, oids, od, oc = small
+    _, cent = g.cluster_order(a["x"], 4, iterations=1)
+    ix = g.Index(a["x"], a["graph"])
+    ix.set_query_order(cent)
+    gi, gd, _ = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    ix.set_cache(int(0.2 * ix.info["index_bytes"]))
+    ix.set_backing(oversub=2)
+    gi, gd, _ = search(torch_dev, ix, q[:0], 10, 32, 4)
+    assert gi.shape == (0, 10)
+    ix.close()
