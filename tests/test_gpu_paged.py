@@ -415,3 +415,19 @@ def test_query_order_resident_and_empty_batch(orc, torch_dev, small):
     gi, gd, _ = search(torch_dev, ix, q[:0], 10, 32, 4)
     assert gi.shape == (0, 10)
     ix.close()
+
+
+def test_paged_f32_cluster_placement_and_query_order(orc, torch_dev, small_f32):
+    """float32 vectors through k-means, cluster placement and ordered admission:
+    answers equal the oracle's bit for bit."""
+    a, q, oids, od, oc = small_f32
+    n2s, cent = g.cluster_order(a["x"], 12, iterations=3)
+    assert np.array_equal(np.sort(n2s), np.arange(len(a["x"]), dtype=np.uint32))
+    ix = g.Index(a["x"], a["graph"], node_to_slot=n2s)
+    ix.set_cache(int(0.08 * ix.info["index_bytes"]))
+    ix.set_backing(latency_us=5.0, oversub=4)
+    ix.set_query_order(cent)
+    gi, gd, st = search(torch_dev, ix, q, 10, 128, 8)
+    assert_same(gi, gd, oids, od)
+    assert st["misses"] > 0
+    ix.close()
