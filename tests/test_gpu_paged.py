@@ -332,7 +332,16 @@ def test_paged_random_configuration(orc, torch_dev, seed):
     layout = dict(page_bytes=int(rng.choice([4096, 4096, 8192])), vectors_first=bool(rng.random() < 0.5))
     if rng.random() < 0.3:
         layout["node_to_slot"] = rng.permutation(n).astype(np.uint32)
+    # cluster placement and ordered admission (their own stream of draws, so
+    # the other parameters of each seed stay as they were)
+    crng = np.random.default_rng(5000 + seed)
+    cent = None
+    if "node_to_slot" not in layout and crng.random() < 0.4:
+        layout["node_to_slot"], cent = g.cluster_order(a["x"], int(crng.integers(1, 40)),
+                                                       iterations=int(crng.integers(0, 5)))
     ix = g.Index(a["x"], a["graph"], **layout)
+    if cent is not None and crng.random() < 0.75:
+        ix.set_query_order(cent)
     e = ix.info["entry"]
     oids, od, oc, _ = orc.pack(a["x"], a["graph"], **layout).search(q, k, L, W, e, threads=8)
     pb = ix.info["page_bytes"]
@@ -341,8 +350,8 @@ def test_paged_random_configuration(orc, torch_dev, seed):
     ix.set_backing(latency_us=float(rng.choice([0.0, 3.0, 20.0])), oversub=int(rng.choice([1, 2, 4, 8])),
                    blocking=blocking)
     print(f"[random {seed}] {dtype} n={n} D={D} R={R} k={k} L={L} W={W} {layout.get('page_bytes')} "
-          f"vfirst={layout['vectors_first']} perm={'node_to_slot' in layout} slots={ix.info['cache_slots']} "
-          f"blocking={blocking}", flush=True)
+          f"vfirst={layout['vectors_first']} perm={'node_to_slot' in layout} clusters={cent is not None} "
+          f"slots={ix.info['cache_slots']} blocking={blocking}", flush=True)
     gi, gd, st = search(torch_dev, ix, q, k, L, W)
     assert_same(gi, gd, oids, od)
     assert st["expansions"] == int(oc["expansions"].sum())
