@@ -14,6 +14,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <thread>
 #include <vector>
 
 #include "../../include/gorio.h"
@@ -23,39 +24,69 @@ namespace gorio {
 gorio_status fail(gorio_status st, const char *fmt, ...);
 
 // Nearest centroid of each vector: argmin_k (|c_k|^2 - 2 x . c_k), float32
-// arithmetic, ties to the smaller k.  One thread per vector; every lane of a
-// wave reads the same centroid element (a broadcast).
-template <typename T>
-__global__ void nearest_centroid(const T *v, uint64_t count, uint32_t D, const float *c, const float *cc,
-                                 uint32_t K, uint32_t *out) {
+// arithmetic, d in order, ties to the smaller k.  One thread per vector;
+// every lane of a wave reads the same centroid element (a broadcast).  With
+// the dimension known at compile time (DC > 0) the vector is held in
+// registers and each centroid is read once per wave through scalar loads.
+template <typename T, int DC>
+__global__ __launch_bounds__(256) void nearest_centroid(const T *v, uint64_t count, uint32_t D, const float *c,
+                                                        const float *cc, uint32_t K, uint32_t *out) {
   const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= count) return;
   const T *x = v + i * D;
   float best = 0.0f;
   uint32_t arg = 0;
-  for (uint32_t k = 0; k < K; ++k) {
-    const float *ck = c + (uint64_t)k * D;
-    float dot = 0.0f;
-    for (uint32_t d = 0; d < D; ++d) dot += (float)x[d] * ck[d];
-    const float s = cc[k] - 2.0f * dot;
-    if (k == 0 || s < best) {
-      best = s;
-      arg = k;
+  if constexpr (DC > 0) {
+    float xr[DC];
+#pragma unroll
+    for (int d = 0; d < DC; ++d) xr[d] = (float)x[d];
+    for (uint32_t k = 0; k < K; ++k) {
+      const float *ck = c + (uint64_t)k * DC;
+      float dot = 0.0f;
+#pragma unroll
+      for (int d = 0; d < DC; ++d) dot += xr[d] * ck[d];
+      const float s = cc[k] - 2.0f * dot;
+      if (k == 0 || s < best) {
+        best = s;
+        arg = k;
+      }
+    }
+  } else {
+    for (uint32_t k = 0; k < K; ++k) {
+      const float *ck = c + (uint64_t)k * D;
+      float dot = 0.0f;
+      for (uint32_t d = 0; d < D; ++d) dot += (float)x[d] * ck[d];
+      const float s = cc[k] - 2.0f * dot;
+      if (k == 0 || s < best) {
+        best = s;
+        arg = k;
+      }
     }
   }
   out[i] = arg;
 }
 
+template <typename T>
+hipError_t launch_nearest_centroid_t(const T *v, uint64_t count, uint32_t D, const float *c, const float *cc,
+                                     uint32_t K, uint32_t *out, hipStream_t s) {
+  const int block = 256;
+  const unsigned grid = (unsigned)((count + block - 1) / block);
+  switch (D) {
+    case 32: nearest_centroid<T, 32><<<grid, block, 0, s>>>(v, count, D, c, cc, K, out); break;
+    case 64: nearest_centroid<T, 64><<<grid, block, 0, s>>>(v, count, D, c, cc, K, out); break;
+    case 96: nearest_centroid<T, 96><<<grid, block, 0, s>>>(v, count, D, c, cc, K, out); break;
+    case 128: nearest_centroid<T, 128><<<grid, block, 0, s>>>(v, count, D, c, cc, K, out); break;
+    default: nearest_centroid<T, 0><<<grid, block, 0, s>>>(v, count, D, c, cc, K, out); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_nearest_centroid(gorio_dtype dt, const void *v, uint64_t count, uint32_t D, const float *c,
                                    const float *cc, uint32_t K, uint32_t *out, hipStream_t s) {
   if (count == 0) return hipSuccess;
-  const int block = 256;
-  const uint64_t grid = (count + block - 1) / block;
   if (dt == GORIO_U8)
-    nearest_centroid<uint8_t><<<(unsigned)grid, block, 0, s>>>(static_cast<const uint8_t *>(v), count, D, c, cc, K, out);
-  else
-    nearest_centroid<float><<<(unsigned)grid, block, 0, s>>>(static_cast<const float *>(v), count, D, c, cc, K, out);
-  return hipGetLastError();
+    return launch_nearest_centroid_t(static_cast<const uint8_t *>(v), count, D, c, cc, K, out, s);
+  return launch_nearest_centroid_t(static_cast<const float *>(v), count, D, c, cc, K, out, s);
 }
 
 void centroid_norms(const float *c, uint32_t K, uint32_t D, float *cc) {
@@ -129,8 +160,31 @@ extern "C" gorio_status gorio_cluster_order(gorio_dtype dtype, const void *vecto
     for (uint32_t d = 0; d < D; ++d) c[(size_t)k * D + d] = (float)elem(i, d);
   }
   std::vector<uint32_t> key(n);
-  std::vector<double> sum((size_t)K * D);
-  std::vector<uint64_t> cnt(K);
+  // Lloyd updates on the host: 16 threads sum fixed node ranges in float64,
+  // then the partial sums are added in range order (the same result on any
+  // machine)
+  const uint32_t nt = 16;
+  std::vector<std::vector<double>> sums(nt, std::vector<double>((size_t)K * D));
+  std::vector<std::vector<uint64_t>> cnts(nt, std::vector<uint64_t>(K));
+  auto accumulate = [&](uint32_t t) {
+    std::vector<double> &sum = sums[t];
+    std::vector<uint64_t> &cnt = cnts[t];
+    std::fill(sum.begin(), sum.end(), 0.0);
+    std::fill(cnt.begin(), cnt.end(), 0);
+    const uint64_t i0 = n * t / nt, i1 = n * (t + 1) / nt;
+    for (uint64_t i = i0; i < i1; ++i) {
+      const uint32_t k = key[i];
+      ++cnt[k];
+      double *sk = sum.data() + (size_t)k * D;
+      if (dtype == GORIO_U8) {
+        const uint8_t *x = static_cast<const uint8_t *>(vectors) + i * D;
+        for (uint32_t d = 0; d < D; ++d) sk[d] += x[d];
+      } else {
+        const float *x = static_cast<const float *>(vectors) + i * D;
+        for (uint32_t d = 0; d < D; ++d) sk[d] += x[d];
+      }
+    }
+  };
   for (uint32_t it = 0;; ++it) {
     centroid_norms(c.data(), K, D, cc.data());
     HIP_OR_FAIL(hipMemcpyAsync(d_c.p, c.data(), c.size() * 4, hipMemcpyHostToDevice, sg.s));
@@ -140,19 +194,22 @@ extern "C" gorio_status gorio_cluster_order(gorio_dtype dtype, const void *vecto
     HIP_OR_FAIL(hipMemcpyAsync(key.data(), d_key.p, n * 4, hipMemcpyDeviceToHost, sg.s));
     HIP_OR_FAIL(hipStreamSynchronize(sg.s));
     if (it == iterations) break;
-    // Lloyd update: each centroid becomes the mean of its members (an empty
-    // cluster keeps its centroid)
-    std::fill(sum.begin(), sum.end(), 0.0);
-    std::fill(cnt.begin(), cnt.end(), 0);
-    for (uint64_t i = 0; i < n; ++i) {
-      const uint32_t k = key[i];
-      ++cnt[k];
-      double *s = sum.data() + (size_t)k * D;
-      for (uint32_t d = 0; d < D; ++d) s[d] += elem(i, d);
+    // each centroid becomes the mean of its members (an empty cluster keeps
+    // its centroid)
+    std::vector<std::thread> pool;
+    for (uint32_t t = 1; t < nt; ++t) pool.emplace_back(accumulate, t);
+    accumulate(0);
+    for (auto &th : pool) th.join();
+    for (uint32_t k = 0; k < K; ++k) {
+      uint64_t cnt = 0;
+      for (uint32_t t = 0; t < nt; ++t) cnt += cnts[t][k];
+      if (!cnt) continue;
+      for (uint32_t d = 0; d < D; ++d) {
+        double sd = 0.0;
+        for (uint32_t t = 0; t < nt; ++t) sd += sums[t][(size_t)k * D + d];
+        c[(size_t)k * D + d] = (float)(sd / (double)cnt);
+      }
     }
-    for (uint32_t k = 0; k < K; ++k)
-      if (cnt[k])
-        for (uint32_t d = 0; d < D; ++d) c[(size_t)k * D + d] = (float)(sum[(size_t)k * D + d] / (double)cnt[k]);
   }
   // cluster by cluster, id order inside a cluster
   std::vector<uint32_t> order(n);
