@@ -202,12 +202,14 @@ def main():
                     help="skip the random-gather ceiling probe (microbench/gather_ceiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
-    ap.add_argument("--paged-sample", type=int, default=2000,
-                    help="queries of each paged configuration to run (0 = skip the paged legs)")
+    ap.add_argument("--paged-sample", type=int, default=-1,
+                    help="queries of each paged configuration to run (-1 = its full query count, "
+                         "0 = skip the paged legs)")
     ap.add_argument("--paged-clusters", type=int, default=256,
                     help="paged legs: k-means clusters for page placement and query admission (0 = off)")
-    ap.add_argument("--paged-repeats", type=int, default=5,
-                    help="cold-cache runs per paged leg (the median is reported)")
+    ap.add_argument("--paged-repeats", type=int, default=3,
+                    help="cold-cache runs per paged leg of up to 20k queries (the median is reported); "
+                         "larger legs run once")
     ap.add_argument("--f32-sample", type=int, default=0,
                     help="queries of the 10M x 96-d float32 paged configuration to run (0 = skip; "
                          "generating that index takes minutes the first time)")
@@ -333,7 +335,7 @@ def main():
 
     paged = None
     miss_gbs = None
-    if args.paged_sample > 0 and w.name == "u8-1m-hbm":
+    if args.paged_sample != 0 and w.name == "u8-1m-hbm":
         link = host_link_peak_gbs(torch)
         legs = []
         clusters = None
@@ -341,25 +343,30 @@ def main():
             t0 = time.perf_counter()
             clusters = g.cluster_order(a["x"], args.paged_clusters)
             log(f"[bench] cluster placement ({args.paged_clusters} clusters) in {time.perf_counter() - t0:.1f} s")
-        plan = [("u8-1m-cache10-lat0", False, clusters), ("u8-1m-cache10-lat0", True, clusters),
-                ("u8-1m-cache10-lat20", False, clusters)]
+        # C3 (10k queries, 0 us): split-phase and blocking; the identity
+        # placement beside them; C4 (100k queries, 20 us): split-phase, one run
+        plan = [("u8-1m-cache10-lat0", False, clusters), ("u8-1m-cache10-lat0", True, clusters)]
         if clusters is not None:
-            plan.append(("u8-1m-cache10-lat20", False, None))   # identity placement, index order
+            plan.append(("u8-1m-cache10-lat0", False, None))   # identity placement, index order
+        plan.append(("u8-1m-cache10-lat20", False, clusters))
         for name, blocking, cl in plan:
-            leg, pi, pd, pq = paged_leg(torch, g, a, WORKLOADS[name], args.paged_sample, qps, blocking,
+            wl = WORKLOADS[name]
+            nq_leg = wl.queries.nq if args.paged_sample < 0 else min(args.paged_sample, wl.queries.nq)
+            reps = args.paged_repeats if nq_leg <= 20000 else 1
+            leg, pi, pd, pq = paged_leg(torch, g, a, wl, nq_leg, qps, blocking,
                                         vectors_first=args.layout == "vectors-first",
-                                        repeats=args.paged_repeats, clusters=cl)
+                                        repeats=reps, clusters=cl)
             # the paged results must equal the resident results on the same queries
-            if WORKLOADS[name].queries == w.queries:
+            if wl.queries == w.queries:
                 leg["equals_resident"] = bool(np.array_equal(pi, gi[:len(pq)]) and np.array_equal(pd, gd[:len(pq)]))
-            log(f"[bench] paged {name} blocking={blocking} {leg['placement']}: {leg['qps']:,.0f} q/s, hit rate "
-                f"{leg['hit_rate']:.3f}, miss service {leg['miss_service_gbs']} GB/s")
+            log(f"[bench] paged {name} ({len(pq)} queries) blocking={blocking} {leg['placement']}: "
+                f"{leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, miss service {leg['miss_service_gbs']} GB/s")
             legs.append(leg)
         miss_gbs = legs[0]["miss_service_gbs"]
         paged = {"host_link_peak_gbs": round(link, 1), "legs": legs,
                  "split_phase_vs_blocking": round(legs[0]["qps"] / max(1e-9, legs[1]["qps"]), 3)}
         if clusters is not None:
-            paged["clusters_vs_identity"] = round(legs[2]["qps"] / max(1e-9, legs[3]["qps"]), 3)
+            paged["clusters_vs_identity"] = round(legs[0]["qps"] / max(1e-9, legs[2]["qps"]), 3)
 
     if args.f32_sample > 0:
         wf = WORKLOADS["f32-10m-cache5-lat20"]
