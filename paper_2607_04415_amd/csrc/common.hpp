@@ -264,7 +264,11 @@ struct VisitedLds16 {
   static constexpr uint32_t kSlots = 7;                  // id slots per bucket
   static constexpr uint32_t kLimit = kBuckets * kSlots;  // records at most this many ids
   static constexpr int kHomeBits = LOG2 - 3;
-  static constexpr uint32_t kMaxId = 1u << (kHomeBits + 14);  // ids must be below this
+  // The hash h = id * odd constant mod 2^kHashBits is one-to-one, and
+  // (home bucket, entry) = (h >> 14, 1 + (h & 0x3FFF)) names the id.  The
+  // multiply reads the low 24 bits of the id, so ids must also be below 2^24.
+  static constexpr int kHashBits = kHomeBits + 14;
+  static constexpr uint32_t kMaxId = 1u << (kHashBits < 24 ? kHashBits : 24);  // ids must be below this
 
   __device__ __forceinline__ static void clear(uint32_t *t) {
     uint4 *t4 = reinterpret_cast<uint4 *>(t);
@@ -311,7 +315,7 @@ struct VisitedLds16 {
     for (int i = 0; i < N; ++i) {
       // v_mul_u32_u24 reads the low 24 bits of each operand: exact for ids
       // below 2^24; an invalid lane's id only picks some bucket to read
-      const uint32_t h = mul_u24(ids[i], 0x9E3779B1u & 0xFFFFFFu) & (kMaxId - 1);
+      const uint32_t h = mul_u24(ids[i], 0x9E3779B1u & 0xFFFFFFu) & ((1u << kHashBits) - 1);
       bk[i] = h >> 14;
       e[i] = 1u + (h & 0x3FFFu);
       v0[i] = t4[bk[i]];

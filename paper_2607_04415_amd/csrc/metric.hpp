@@ -8,8 +8,9 @@
 //
 //   MetricU8  - exact int32 distance: q.q + sum (x.x - 2 q.x) with
 //               v_dot4_u32_u8 on coalesced reads, 8 lanes per vector.
-//   MetricF32 - one lane per candidate; t = q_d - x_d, acc = acc + t*t for
-//               d = 0 .. D-1 in order, every operation rounded to nearest
+//   MetricF32 - one lane per candidate (resident 96-d rows are gathered 8
+//               lanes per vector and transposed in registers); t = q_d - x_d,
+//               acc = acc + t*t for d = 0 .. D-1 in order, every operation rounded to nearest
 //               even with no fused multiply-add, so the result is the same
 //               float as a plain sequential loop.
 #pragma once
@@ -247,9 +248,13 @@ struct MetricF32 {
   static constexpr int kChunks = 1;
   static constexpr int kQueryWords = 4 * NV4;
   static constexpr uint32_t kPadDist = 0x7F800000u;  // +inf
-  // resident kernel: the whole-vector registers of a lane allow two waves per SIMD
-  static constexpr int kWavesPerSimd = 2;
-  static constexpr int kHtLog2 = 13;
+  // resident kernel: 96-d rows (gathered by lines and transposed) hold a
+  // whole vector per lane plus the transpose's temporaries, which fits one
+  // wave per SIMD and leaves LDS for a 32 KB visited table; other widths run
+  // two waves per SIMD with a 16 KB table
+  static constexpr bool kGathered = EXACT && NV4 % 8 == 0;
+  static constexpr int kWavesPerSimd = kGathered ? 1 : 2;
+  static constexpr int kHtLog2 = kGathered ? 14 : 13;
   static constexpr int kStep = 16;                   // dwords per round trip (generic path)
 
   const float *qs;  // the query in LDS (wave-uniform reads)
@@ -333,8 +338,99 @@ struct MetricF32 {
                                                 uint64_t (&key)[kChunks]) const {
     const uint32_t idx = c0 + lane_id();
     const uint32_t node = idx < cnt ? cand[idx] : fallback;
-    const float d = dist_global(pages + vec_offset(geom, slot_ct<N2S>(geom, node)));
-    key[0] = idx < cnt ? (((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)node << 1)) : kInfKey;
+    const uint64_t off = vec_offset(geom, slot_ct<N2S>(geom, node));
+    if constexpr (kGathered) {
+      const uint32_t c = transposed_candidate();
+      const float d = dist_gathered(pages, off);
+      const uint32_t cn = (uint32_t)__shfl((int)node, (int)c);
+      key[0] = c0 + c < cnt ? (((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)cn << 1)) : kInfKey;
+    } else {
+      const float d = dist_global(pages + off);
+      key[0] = idx < cnt ? (((uint64_t)__float_as_uint(d) << 32) | ((uint64_t)node << 1)) : kInfKey;
+    }
+  }
+
+  // Resident gather of 64 vectors, lane i's vector at byte offset `off` of
+  // lane i.  One lane reading a whole vector would make every 16-byte load
+  // instruction touch 64 different cache lines; instead the 8 lanes of a
+  // group read 8 vectors, one at a time, each lane 16 bytes of every 128
+  // (so each load instruction covers whole lines), and an 8 x 8 transpose of
+  // the 16-byte blocks inside the group (three butterfly exchanges over
+  // lane distances 1, 2, 4) then leaves each lane holding one 128-byte line
+  // of one vector for the sequential sum.  Lane g * 8 + s ends with the
+  // vector of lane s * 8 + g (transposed_candidate).
+  __device__ __forceinline__ static uint32_t transposed_candidate() {
+    const uint32_t l = lane_id();
+    return ((l & 7u) << 3) | (l >> 3);
+  }
+
+  // One butterfly stage of the 8 x 8 block transpose inside each group of 8
+  // lanes (x[r][c]: component c of block r).  Lanes with bit M of their
+  // group position set give away block r and receive into it; the others
+  // do so with block r + M (value selects only, so that the blocks stay in
+  // registers).  After the stages for M = 1, 2, 4, block r of lane t holds
+  // what block t of lane r held.
+  template <int M>
+  __device__ __forceinline__ static void transpose_stage(uint32_t (&x)[8][4], uint32_t gl) {
+    const bool hi = (gl & M) != 0;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int r = ((p & ~(M - 1)) << 1) | (p & (M - 1));  // the blocks with bit M clear
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t a = x[r][c], b = x[r + M][c];
+        const uint32_t got = xor_lanes<M>(hi ? a : b);
+        x[r][c] = hi ? got : a;
+        x[r + M][c] = hi ? b : got;
+      }
+    }
+  }
+
+  // Line j of the vectors of the group's 8 candidates: x[r][c] = float
+  // 32 j + 4 gl + c of the vector of lane r * 8 + g.
+  __device__ __forceinline__ static void load_line(const uint8_t *pages, uint64_t off, int j, uint32_t (&x)[8][4]) {
+    const uint32_t l = lane_id(), g = l >> 3, gl = l & 7u;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const uint64_t o = __shfl(off, r * 8 + (int)g);
+      const uint32_t *w = reinterpret_cast<const uint32_t *>(pages + o) + 32 * j + 4 * gl;
+      uint4 u;
+      __builtin_memcpy(&u, __builtin_assume_aligned(w, 4), 16);
+      x[r][0] = u.x;
+      x[r][1] = u.y;
+      x[r][2] = u.z;
+      x[r][3] = u.w;
+    }
+  }
+
+  // acc over line j of this lane's vector: after the transpose x[s][c] is
+  // float 32 j + 4 s + c, so s then c visits d in increasing order.
+  __device__ __forceinline__ float sum_line(float acc, uint32_t (&x)[8][4], int j) const {
+    const uint32_t gl = lane_id() & 7u;
+    transpose_stage<1>(x, gl);
+    transpose_stage<2>(x, gl);
+    transpose_stage<4>(x, gl);
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const float4 qv = *reinterpret_cast<const float4 *>(qs + 32 * j + 4 * s);
+      acc = step(acc, qv.x, __uint_as_float(x[s][0]));
+      acc = step(acc, qv.y, __uint_as_float(x[s][1]));
+      acc = step(acc, qv.z, __uint_as_float(x[s][2]));
+      acc = step(acc, qv.w, __uint_as_float(x[s][3]));
+    }
+    return acc;
+  }
+
+  __device__ __forceinline__ float dist_gathered(const uint8_t *pages, uint64_t off) const {
+    static_assert(EXACT && NV4 % 8 == 0, "whole 128-byte lines per vector");
+    constexpr int J = NV4 / 8;  // lines per vector, all in flight at once
+    uint32_t x[J][8][4];
+#pragma unroll
+    for (int j = 0; j < J; ++j) load_line(pages, off, j, x[j]);
+    float acc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) acc = sum_line(acc, x[j], j);
+    return acc;
   }
 
   template <class OffOf>
