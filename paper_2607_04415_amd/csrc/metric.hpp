@@ -44,6 +44,7 @@ struct MetricU8 {
   static constexpr uint32_t kPadDist = 0x7FFFFFFFu;  // INT32_MAX
   static_assert(!LOC16 || (EXACT && VDW % 4 == 0), "locators address whole 16-byte units");
   static constexpr bool kLocators = LOC16;
+  static constexpr bool kGathered = false;  // float32 line gather only
 
   // Where the kernel's compaction puts the i-th new candidate, and the word
   // it stores for node v (its id, or with LOC16 its vector's locator).
@@ -419,6 +420,33 @@ struct MetricF32 {
       acc = step(acc, qv.w, __uint_as_float(x[s][3]));
     }
     return acc;
+  }
+
+  // One batch of 64 candidates' vectors in flight (resident kernel, line
+  // gather): the loads are issued by gather_issue and consumed by gather_key,
+  // so that another batch's loads can be outstanding in between.
+  struct Gathered {
+    uint32_t x[NV4 / 8][8][4];
+    uint32_t node;
+  };
+
+  template <bool N2S>
+  __device__ __forceinline__ static void gather_issue(const uint8_t *pages, const PageGeom &geom, const uint32_t *cand,
+                                                      uint32_t c0, uint32_t cnt, uint32_t fallback, Gathered &b) {
+    const uint32_t idx = c0 + lane_id();
+    b.node = idx < cnt ? cand[idx] : fallback;
+    const uint64_t off = vec_offset(geom, slot_ct<N2S>(geom, b.node));
+#pragma unroll
+    for (int j = 0; j < NV4 / 8; ++j) load_line(pages, off, j, b.x[j]);
+  }
+
+  __device__ __forceinline__ uint64_t gather_key(Gathered &b, uint32_t c0, uint32_t cnt) const {
+    float acc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV4 / 8; ++j) acc = sum_line(acc, b.x[j], j);
+    const uint32_t c = transposed_candidate();
+    const uint32_t cn = (uint32_t)__shfl((int)b.node, (int)c);
+    return c0 + c < cnt ? (((uint64_t)__float_as_uint(acc) << 32) | ((uint64_t)cn << 1)) : kInfKey;
   }
 
   __device__ __forceinline__ float dist_gathered(const uint8_t *pages, uint64_t off) const {

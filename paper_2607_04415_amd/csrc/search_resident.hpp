@@ -62,6 +62,27 @@ __device__ __forceinline__ void eval_chunks(const M &m, const ResidentParams &p,
   if constexpr (NCH > 3) merge_keys<KPL>(F, m.chunk_key(p.geom, cand, 3 * kWave, cnt, B), forgot, p.L);
 }
 
+// Evaluates NCH batches of 64 compacted candidates with the float32 line
+// gather and merges their keys into F, two batches in flight (the same
+// fixed schedule as eval_chunks).
+template <int NCH, int KPL, bool N2S, class M>
+__device__ __forceinline__ void eval_gathered(const M &m, const ResidentParams &p, const uint32_t *cand, uint32_t cnt,
+                                              uint64_t (&F)[KPL], bool forgot) {
+  typename M::Gathered A, B;
+  M::template gather_issue<N2S>(p.pages, p.geom, cand, 0, cnt, p.entry, A);
+  if constexpr (NCH > 1) M::template gather_issue<N2S>(p.pages, p.geom, cand, kWave, cnt, p.entry, B);
+  uint64_t key = m.gather_key(A, 0, cnt);
+  if constexpr (NCH > 2) M::template gather_issue<N2S>(p.pages, p.geom, cand, 2 * kWave, cnt, p.entry, A);
+  merge_keys<KPL>(F, key, forgot, p.L);
+  if constexpr (NCH > 1) {
+    key = m.gather_key(B, kWave, cnt);
+    if constexpr (NCH > 3) M::template gather_issue<N2S>(p.pages, p.geom, cand, 3 * kWave, cnt, p.entry, B);
+    merge_keys<KPL>(F, key, forgot, p.L);
+  }
+  if constexpr (NCH > 2) merge_keys<KPL>(F, m.gather_key(A, 2 * kWave, cnt), forgot, p.L);
+  if constexpr (NCH > 3) merge_keys<KPL>(F, m.gather_key(B, 3 * kWave, cnt), forgot, p.L);
+}
+
 // Several waves per SIMD (M::kWavesPerSimd: 4 for uint8 rows up to 128 bytes,
 // with an 8 KB visited table; 2 otherwise): one wave's gathers overlap the
 // others' filtering and merging.  The grid is as large as the chip holds at
@@ -191,6 +212,17 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
             case 2: eval_chunks<2, KPL>(m, p, cand, cnt, F, forgot); break;
             case 3: eval_chunks<3, KPL>(m, p, cand, cnt, F, forgot); break;
             case 4: eval_chunks<4, KPL>(m, p, cand, cnt, F, forgot); break;
+            default: break;
+          }
+        } else if constexpr (M::kGathered && !N2S) {
+          // float32 line gather, two batches of 64 in flight (with a
+          // placement permutation the next batch's slot loads would wait on
+          // the older batch's loads, so that case takes the plain loop)
+          switch ((cnt + kWave - 1) / kWave) {
+            case 1: eval_gathered<1, KPL, N2S>(m, p, cand, cnt, F, forgot); break;
+            case 2: eval_gathered<2, KPL, N2S>(m, p, cand, cnt, F, forgot); break;
+            case 3: eval_gathered<3, KPL, N2S>(m, p, cand, cnt, F, forgot); break;
+            case 4: eval_gathered<4, KPL, N2S>(m, p, cand, cnt, F, forgot); break;
             default: break;
           }
         } else {
