@@ -14,7 +14,8 @@
 //   evaluate- one round trip gathers a batch of candidate vectors; the
 //             distance policy (metric.hpp) turns them into keys: uint8 with
 //             8 lanes per 128-B vector and v_dot4_u32_u8, float32 with one
-//             lane per vector and the sequential rounded sum;
+//             lane per vector (96-d rows read 8 lanes per vector by lines,
+//             then transposed in registers) and the sequential rounded sum;
 //   merge   - only keys below F's L-th key can enter: a few are inserted by
 //             rank (ballot + DPP shift), many are bitonic-sorted per 64-lane
 //             chunk and bitonic-merged into F.
@@ -83,9 +84,10 @@ __device__ __forceinline__ void eval_gathered(const M &m, const ResidentParams &
   if constexpr (NCH > 3) merge_keys<KPL>(F, m.gather_key(B, 3 * kWave, cnt), forgot, p.L);
 }
 
-// Several waves per SIMD (M::kWavesPerSimd: 4 for uint8 rows up to 128 bytes,
-// with an 8 KB visited table; 2 otherwise): one wave's gathers overlap the
-// others' filtering and merging.  The grid is as large as the chip holds at
+// Waves per SIMD from the distance policy (M::kWavesPerSimd: 4 for uint8
+// rows up to 128 bytes, with an 8 KB visited table; 1 for gathered 96-d
+// float32 rows, which keep two batches of whole vectors in registers; 2
+// otherwise): one wave's gathers overlap the others' filtering and merging.  The grid is as large as the chip holds at
 // once; workgroup b starts with query b and then takes the next unclaimed
 // query from a global counter, so the XCDs and CUs that finish early take
 // more queries and the batch ends when the last queries end, wherever they
