@@ -27,19 +27,21 @@ using ResidentHtLarge = VisitedLds<13>;
 
 namespace detail {
 
-// One workgroup per wave slot the device holds at once (queries beyond the
-// grid are taken from the kernel's counter), at most `grid`.
-template <auto Kernel>
+// One workgroup per wave slot the device holds at once, but at most
+// `grid_waves_per_simd` per SIMD (queries beyond the grid are taken from the
+// kernel's counter), and at most `grid`.
+template <auto Kernel, int grid_waves_per_simd>
 hipError_t launch_resident_grid(const ResidentParams &p, int grid, hipStream_t s) {
   static int slots = 0;  // per kernel
   if (slots == 0) {
+    constexpr int kSimdsPerCu = 4;
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(Kernel), kWave, 0);
     if (e != hipSuccess) return e;
-    slots = std::max(1, cus * per_cu);
+    slots = std::max(1, cus * std::min(per_cu, kSimdsPerCu * grid_waves_per_simd));
   }
   Kernel<<<std::min(grid, slots), kWave, 0, s>>>(p);
   return hipGetLastError();
@@ -48,8 +50,9 @@ hipError_t launch_resident_grid(const ResidentParams &p, int grid, hipStream_t s
 template <int KPL, class M, bool N2S>
 hipError_t resident_t(const ResidentParams &p, int grid, hipStream_t s) {
   using Small = VisitedLds16<M::kHtLog2>;
-  if (p.n <= Small::kMaxId) return launch_resident_grid<search_resident<KPL, M, Small, N2S>>(p, grid, s);
-  return launch_resident_grid<search_resident<KPL, M, ResidentHtLarge, N2S>>(p, grid, s);
+  constexpr int kGrid = M::kGridWavesPerSimd;
+  if (p.n <= Small::kMaxId) return launch_resident_grid<search_resident<KPL, M, Small, N2S>, kGrid>(p, grid, s);
+  return launch_resident_grid<search_resident<KPL, M, ResidentHtLarge, N2S>, kGrid>(p, grid, s);
 }
 
 // frontier slots per lane (L <= 64 KPL) and node_to_slot presence
