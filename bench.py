@@ -124,6 +124,17 @@ def gather_ceiling(n: int, rpp: int, page_bytes: int, vec_stride: int):
             "depths_gbs": {k: d[k]["gbs"] for k in d if k.startswith("rounds_")}}
 
 
+def cluster_count(arg: int, nq: int) -> int:
+    """k-means clusters for a paged leg: `arg` if positive, none if 0, else by
+    the leg's query count.  Queries are admitted cluster by cluster, so a
+    larger batch can use smaller clusters before too few of its queries share
+    each one (1M uint8 index, 10% cache: 256 clusters best at 10k queries,
+    512 at 100k)."""
+    if arg >= 0:
+        return arg
+    return 256 if nq <= 20000 else 512
+
+
 def host_link_peak_gbs(torch) -> float:
     """Pinned host -> HBM copy bandwidth (256 MiB, best of 5), the host-link ceiling."""
     src = torch.empty(1 << 28, dtype=torch.uint8).pin_memory()
@@ -205,8 +216,9 @@ def main():
     ap.add_argument("--paged-sample", type=int, default=-1,
                     help="queries of each paged configuration to run (-1 = its full query count, "
                          "0 = skip the paged legs)")
-    ap.add_argument("--paged-clusters", type=int, default=256,
-                    help="paged legs: k-means clusters for page placement and query admission (0 = off)")
+    ap.add_argument("--paged-clusters", type=int, default=-1,
+                    help="paged legs: k-means clusters for page placement and query admission (0 = off, "
+                         "-1 = by the leg's query count: 256 up to 20k queries, 512 above)")
     ap.add_argument("--paged-repeats", type=int, default=3,
                     help="cold-cache runs per paged leg of up to 20k queries (the median is reported); "
                          "larger legs run once")
@@ -348,20 +360,27 @@ def main():
     if args.paged_sample != 0 and w.name == "u8-1m-hbm":
         link = host_link_peak_gbs(torch)
         legs = []
-        clusters = None
-        if args.paged_clusters > 0:
-            t0 = time.perf_counter()
-            clusters = g.cluster_order(a["x"], args.paged_clusters)
-            log(f"[bench] cluster placement ({args.paged_clusters} clusters) in {time.perf_counter() - t0:.1f} s")
+        placements = {}
+
+        def placement(nq_leg):
+            k = cluster_count(args.paged_clusters, nq_leg)
+            if k and k not in placements:
+                t0 = time.perf_counter()
+                placements[k] = g.cluster_order(a["x"], k)
+                log(f"[bench] cluster placement ({k} clusters) in {time.perf_counter() - t0:.1f} s")
+            return placements.get(k)
+
         # C3 (10k queries, 0 us): split-phase and blocking; the identity
         # placement beside them; C4 (100k queries, 20 us): split-phase, one run
-        plan = [("u8-1m-cache10-lat0", False, clusters), ("u8-1m-cache10-lat0", True, clusters)]
-        if clusters is not None:
-            plan.append(("u8-1m-cache10-lat0", False, None))   # identity placement, index order
-        plan.append(("u8-1m-cache10-lat20", False, clusters))
-        for name, blocking, cl in plan:
+        clustered = args.paged_clusters != 0
+        plan = [("u8-1m-cache10-lat0", False, clustered), ("u8-1m-cache10-lat0", True, clustered)]
+        if clustered:
+            plan.append(("u8-1m-cache10-lat0", False, False))   # identity placement, index order
+        plan.append(("u8-1m-cache10-lat20", False, clustered))
+        for name, blocking, use_clusters in plan:
             wl = WORKLOADS[name]
             nq_leg = wl.queries.nq if args.paged_sample < 0 else min(args.paged_sample, wl.queries.nq)
+            cl = placement(nq_leg) if use_clusters else None
             reps = args.paged_repeats if nq_leg <= 20000 else 1
             leg, pi, pd, pq = paged_leg(torch, g, a, wl, nq_leg, qps, blocking,
                                         vectors_first=args.layout == "vectors-first",
@@ -375,7 +394,7 @@ def main():
         miss_gbs = legs[0]["miss_service_gbs"]
         paged = {"host_link_peak_gbs": round(link, 1), "legs": legs,
                  "split_phase_vs_blocking": round(legs[0]["qps"] / max(1e-9, legs[1]["qps"]), 3)}
-        if clusters is not None:
+        if clustered:
             paged["clusters_vs_identity"] = round(legs[0]["qps"] / max(1e-9, legs[2]["qps"]), 3)
 
     if args.f32_sample > 0:
@@ -391,10 +410,11 @@ def main():
         rqps = len(qf) / (rst["kernel_ms"] * 1e-3)
         ixr.close()
         fclusters = None
-        if args.paged_clusters > 0:
+        fk = cluster_count(args.paged_clusters, len(qf))
+        if fk:
             t0 = time.perf_counter()
-            fclusters = g.cluster_order(af["x"], args.paged_clusters)
-            log(f"[bench] {wf.name}: cluster placement ({args.paged_clusters} clusters) in "
+            fclusters = g.cluster_order(af["x"], fk)
+            log(f"[bench] {wf.name}: cluster placement ({fk} clusters) in "
                 f"{time.perf_counter() - t0:.1f} s")
         leg, pi, pd, _ = paged_leg(torch, g, af, wf, args.f32_sample, rqps,
                                    vectors_first=args.layout == "vectors-first", repeats=1, clusters=fclusters)
