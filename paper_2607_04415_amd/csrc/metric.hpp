@@ -9,10 +9,11 @@
 //   MetricU8  - exact int32 distance: q.q + sum (x.x - 2 q.x) with
 //               v_dot4_u32_u8 on coalesced reads, 8 lanes per vector.
 //   MetricF32 - one lane per candidate (resident 96-d rows are gathered 8
-//               lanes per vector and transposed in registers); t = q_d - x_d,
-//               acc = acc + t*t for d = 0 .. D-1 in order, every operation rounded to nearest
-//               even with no fused multiply-add, so the result is the same
-//               float as a plain sequential loop.
+//               lanes per vector and transposed in registers);
+//               t = q_d - x_d, acc = acc + t*t for d = 0 .. D-1 in order,
+//               every operation rounded to nearest even with no fused
+//               multiply-add, so the result is the same float as a plain
+//               sequential loop.
 #pragma once
 
 #include "frontier.hpp"
