@@ -3,15 +3,18 @@
  *
  * The library implements the GPU side of GORIO ("GPU-Centered Remote I/O for
  * Graph ANNS over NVMe-oF"): batched DiskANN-style beam search whose node
- * records live in 4 KB pages.  The GPU owns query evolution, page-miss
- * generation, pending-query state and resume decisions (Sec. 3.1, Fig. 1); a
- * host proxy thread only services page reads and publishes completions to
- * GPU-visible memory (Sec. 3.3, Sec. 4 "CPU transport proxy").  On one GPU the
- * remote NVMe-oF namespace of Sec. 4 ("Remote storage") is stood in for by a
- * pinned host-memory backing store with an injected per-request latency.
+ * records live in 4 KB pages.  Every search-side decision is taken on the GPU:
+ * how each query advances, which pages it is missing, where a query waiting
+ * for pages is kept and when it continues (Sec. 3.1, Fig. 1).  A host proxy
+ * thread does nothing but read pages from the backing store and post their
+ * completions where the GPU can see them (Sec. 3.3, Sec. 4 "CPU transport
+ * proxy").  On one GPU a pinned host-memory backing store with an injected
+ * per-request latency takes the place of the remote NVMe-oF namespace of
+ * Sec. 4 ("Remote storage").
  *
- * Search semantics (the loop of Sec. 1 and Sec. 2.2: expand nodes, compute
- * distances, update the candidate frontier, discover the next pages):
+ * Search semantics (Sec. 1 and Sec. 2.2 describe the search only as a loop
+ * that grows a candidate frontier by visiting graph nodes and scoring their
+ * neighbours, which in turn names the pages to read next):
  *   key(v) = (squared L2 distance(q, v), v)       -- ties broken by node id
  *   V = {entry};  X = {}
  *   repeat: F = the min(L, |V|) smallest keys of V;
@@ -41,8 +44,12 @@
  *   - Status codes, never exceptions; gorio_last_error() returns a
  *     thread-local message for the last failing call on this thread.
  *   - The caller owns every array it passes; the library copies what it keeps.
- *   - One search per index at a time; no call on an index may overlap a search
- *     on it.  Different indexes may be used from different threads.
+ *   - One thread at a time per index; no call on an index may overlap a
+ *     search on it from another thread.  Searches of one index issued on
+ *     different streams run one after another: each search's work waits on
+ *     the GPU for the previous search of the index (an event the index
+ *     records), because they share the index's counters.  Different indexes
+ *     may be used from different threads.
  *   - The device is the HIP device current when gorio_build_index is called;
  *     later calls switch to it and restore the caller's device.
  */
@@ -114,7 +121,11 @@ typedef struct {
 } gorio_index_info;
 
 /*
- * Build an index: pack records into pages and choose the entry node.
+ * Build an index: pack records into pages and choose the entry node.  The
+ * index is a DiskANN-style graph (Sec. 5.1) stored as fixed-size graph pages
+ * that are the unit of every read (Sec. 3.1, Fig. 1: graph pages on the remote
+ * namespace; Sec. 4 "Remote storage": the page-cache path fetches whole
+ * pages).  Record and page layout as described at the top of this file.
  *   vectors: host, n x D row-major (uint8 or float32 per dtype).
  *   graph:   host, n x R row-major uint32; UINT32_MAX = no edge; any other id must be < n.
  *   layout:  NULL = all defaults.
@@ -146,13 +157,43 @@ gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes);
  *   latency_us:      injected delay from a page request's publication to its completion (>= 0).
  *   max_outstanding: cap on requests the proxy holds in flight (0 = default 4096).
  *   oversub:         query slots per resident wavefront of the persistent kernel (1..16).
- *   blocking:        0 = split-phase (park the query, run other ready queries);
- *                    1 = wait in place for each missing page (the blocking
- *                    demand-paging baseline the paper compares against, Sec. 5.1).
+ *   blocking:        scheduling mode.
+ *                    0 = split-phase: the persistent GPU scheduler parks a query
+ *                        on a missing page and runs other ready queries (Sec. 3.3);
+ *                    1 = wait in place for each missing page, one query per wave
+ *                        (the blocking demand-paging path the paper compares
+ *                        against, Sec. 5.1, Table 2);
+ *                    2 = host-scheduled rounds: a host thread (the caller's)
+ *                        keeps the query lanes and launches one round kernel at a
+ *                        time over the lanes whose pages have been filled, using
+ *                        the same page cache, descriptors and proxy (the
+ *                        GustANN-style scheduler over GORIO's backend that the
+ *                        paper compares against, Sec. 5.1, Table 2).  oversub is
+ *                        ignored; the lanes are min(query_waves or 8 per compute
+ *                        unit, slots / (2 * max_pending), nq, 8192).
+ *                    Results are the same in every mode.
  * Takes effect at the next search.  Ignored in resident mode.
+ * Errors: GORIO_EINVAL for a NULL index or an argument out of range.
  */
 gorio_status gorio_set_backing(gorio_index *ix, double latency_us, uint32_t max_outstanding,
                                uint32_t oversub, int blocking);
+
+/*
+ * Shape of the paged scheduler (Sec. 3.3: the persistent scheduler runs many
+ * queries per wave and caps the page requests in flight).
+ *   query_waves: most waves that run queries (0 = 8 per compute unit).
+ *   max_pending: page requests one query keeps outstanding (1..256; 0 = 32).
+ * A search runs min(query_waves * oversub, slots / (2 * max_pending), nq)
+ * queries at once, in ceil(that / oversub) waves (one query per wave when
+ * blocking): every query may pin max_pending slots, and half of the cache is
+ * kept free for the clock to evict.  With equal query_waves, the blocking
+ * mode therefore holds oversub times fewer queries than the split-phase mode,
+ * which is the comparison of Sec. 5.2 (waits in place vs. yields and runs
+ * other queries).  Takes effect at the next search; ignored in resident mode.
+ * Errors: GORIO_EINVAL for a NULL index, query_waves > 65536 or
+ * max_pending > 256.
+ */
+gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_waves, uint32_t max_pending);
 
 /*
  * Batched search (GORIO Sec. 3.3: persistent scheduler; each query is finished
@@ -236,10 +277,21 @@ gorio_status gorio_cluster_order(gorio_dtype dtype, const void *vectors, uint64_
  */
 gorio_status gorio_set_query_order(gorio_index *ix, const float *centroids, uint32_t clusters);
 
-/* Release everything the index owns.  NULL is a no-op. */
+/*
+ * Release everything the index owns: its HBM pages or cache, the ready-table
+ * words and rings of Sec. 3.2, the pinned backing store and the proxy thread
+ * of Sec. 3.3 / Sec. 4 ("CPU transport proxy"), which is stopped first.  Must
+ * not overlap a search on the index.  NULL is a no-op.
+ */
 void gorio_free_index(gorio_index *ix);
 
-/* Message for the last failing call on this thread ("" if none). */
+/*
+ * Message for the last failing call on this thread ("" if none).  Errors are
+ * returned as status codes so that no failure of the transport path (Sec. 4)
+ * or of a search crosses the ABI as an exception; the text says which check
+ * or which HIP call failed.  The pointer stays valid until the next failing
+ * call on the same thread.
+ */
 const char *gorio_last_error(void);
 
 #ifdef __cplusplus

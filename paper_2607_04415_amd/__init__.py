@@ -57,7 +57,7 @@ class IndexInfo(ctypes.Structure):
 # every symbol include/gorio.h declares
 EXPORTS = ("gorio_build_index", "gorio_set_cache", "gorio_set_backing", "gorio_set_query_order",
            "gorio_search", "gorio_index_info_get", "gorio_copy_pages", "gorio_locality_order",
-           "gorio_cluster_order", "gorio_free_index", "gorio_last_error")
+           "gorio_cluster_order", "gorio_set_scheduler", "gorio_free_index", "gorio_last_error")
 
 _lib = None
 
@@ -78,6 +78,8 @@ def lib() -> ctypes.CDLL:
         L.gorio_set_cache.argtypes = [v, u64]
         L.gorio_set_backing.restype = i32
         L.gorio_set_backing.argtypes = [v, ctypes.c_double, u32, u32, i32]
+        L.gorio_set_scheduler.restype = i32
+        L.gorio_set_scheduler.argtypes = [v, u32, u32]
         L.gorio_search.restype = i32
         L.gorio_search.argtypes = [v, v, u64, u32, u32, u32, v, v, ctypes.POINTER(Stats), v]
         L.gorio_index_info_get.restype = i32
@@ -185,9 +187,15 @@ class Index:
         _check(lib().gorio_set_cache(self._h, int(nbytes)))
 
     def set_backing(self, latency_us: float = 0.0, max_outstanding: int = 0, oversub: int = 1,
-                    blocking: bool = False):
+                    blocking: bool = False, mode: int | None = None):
+        """mode: 0 split-phase, 1 blocking, 2 host-scheduled rounds (default: from `blocking`)."""
+        m = int(bool(blocking)) if mode is None else int(mode)
         _check(lib().gorio_set_backing(self._h, float(latency_us), int(max_outstanding),
-                                       int(oversub), int(bool(blocking))))
+                                       int(oversub), m))
+
+    def set_scheduler(self, query_waves: int = 0, max_pending: int = 0):
+        """Paged scheduler shape: most query waves and page requests per query (0 = default)."""
+        _check(lib().gorio_set_scheduler(self._h, int(query_waves), int(max_pending)))
 
     def set_query_order(self, centroids: np.ndarray | None):
         """Paged searches admit queries by nearest centroid (None: index order)."""

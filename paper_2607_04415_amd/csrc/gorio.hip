@@ -15,6 +15,13 @@
 #include "index.hpp"
 #include "launch.hpp"
 
+#if defined(__x86_64__)
+#include <immintrin.h>
+#define GORIO_CPU_PAUSE() _mm_pause()
+#else
+#define GORIO_CPU_PAUSE() std::this_thread::yield()
+#endif
+
 using namespace gorio;
 
 // ---------------------------------------------------------------------------
@@ -140,6 +147,7 @@ extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors
   HIP_OR_FAIL(hipStreamCreateWithFlags(&ix->stream, hipStreamNonBlocking));
   HIP_OR_FAIL(hipEventCreate(&ix->ev_start));
   HIP_OR_FAIL(hipEventCreate(&ix->ev_stop));
+  HIP_OR_FAIL(hipEventCreateWithFlags(&ix->ev_done, hipEventDisableTiming));
   HIP_OR_FAIL(hipMalloc(&ix->d_stats, sizeof(unsigned long long) * kStatWords));
   hipStream_t s = ix->stream;
 
@@ -327,11 +335,20 @@ extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, ui
   if (!ix) return fail(GORIO_EINVAL, "index is NULL");
   if (!(latency_us >= 0.0) || latency_us > 1e7) return fail(GORIO_EINVAL, "latency_us=%g out of range", latency_us);
   if (oversub < 1 || oversub > 16) return fail(GORIO_EINVAL, "oversub=%u outside [1, 16]", oversub);
-  if (blocking != 0 && blocking != 1) return fail(GORIO_EINVAL, "blocking must be 0 or 1");
+  if (blocking < 0 || blocking > 2) return fail(GORIO_EINVAL, "mode (blocking) must be 0, 1 or 2");
   ix->latency_us = latency_us;
   ix->max_outstanding = max_outstanding ? max_outstanding : 4096;
   ix->oversub = oversub;
   ix->blocking = blocking;
+  return GORIO_OK;
+}
+
+extern "C" gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_waves, uint32_t max_pending) {
+  if (!ix) return fail(GORIO_EINVAL, "index is NULL");
+  if (query_waves > 65536) return fail(GORIO_EINVAL, "query_waves=%u above 65536", query_waves);
+  if (max_pending > 256) return fail(GORIO_EINVAL, "max_pending=%u above 256", max_pending);
+  ix->query_waves = query_waves;
+  ix->max_pending = max_pending;
   return GORIO_OK;
 }
 
@@ -340,26 +357,227 @@ extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, ui
 // ---------------------------------------------------------------------------
 namespace {
 
-// Paged search: reset the per-search rings and counters, arm the proxy,
-// launch the persistent kernel and wait for it under a watchdog.
+// Host-scheduled rounds (the GustANN-style comparison point of Sec. 5.1, over
+// the same page cache, miss descriptors and proxy): the calling thread owns
+// the query schedule.  It keeps `lanes` query lanes, starts queries in free
+// lanes in admission order, and launches one round kernel at a time over the
+// lanes it deems runnable.  A lane is runnable when one of the cache slots it
+// reported waiting for has been filled -- the fill waves publish, per
+// completion ring, how many completions they have copied, and the host reads
+// the filled {page, slot} entries back from the ring -- or, for a lane that
+// could not issue all of its requests, when any page has been filled.  A lane
+// not woken within a few milliseconds is run anyway, so a missed wake costs
+// time, never progress.
+gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, const std::vector<uint32_t> &order,
+                             hipStream_t s, double limit_s, bool &timed_out) {
+  using Clock = std::chrono::steady_clock;
+  PagedState &P = *ix->paged;
+  const uint32_t words = lane_state_words(pp.L);
+  if ((uint64_t)lanes * words > P.lane_state_words) {
+    if (P.d_lane_state) (void)hipFree(P.d_lane_state);
+    P.d_lane_state = nullptr;
+    P.lane_state_words = 0;
+    HIP_OR_FAIL(hipMalloc(&P.d_lane_state, (uint64_t)lanes * words * 4));
+    P.lane_state_words = (uint64_t)lanes * words;
+  }
+  if (lanes > P.round_cap) {
+    if (P.h_round) (void)hipHostFree(P.h_round);
+    if (P.h_lane_out) (void)hipHostFree(P.h_lane_out);
+    P.h_round = P.d_round = nullptr;
+    P.h_lane_out = P.d_lane_out = nullptr;
+    P.round_cap = 0;
+    HIP_OR_FAIL(host_ring(&P.h_round, &P.d_round, 2 * (size_t)lanes));
+    HIP_OR_FAIL(host_ring(&P.h_lane_out, &P.d_lane_out, lanes));
+    P.round_cap = lanes;
+  }
+  if (!P.h_fill_head)
+    HIP_OR_FAIL(host_ring(&P.h_fill_head, &P.d_fill_head, (size_t)PagedState::kMaxRings * PagedState::kTailStride));
+  if (!P.fill_stream) HIP_OR_FAIL(hipStreamCreateWithFlags(&P.fill_stream, hipStreamNonBlocking));
+  if (!P.ev_round) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_round, hipEventDisableTiming));
+  if (!P.ev_fill) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_fill, hipEventDisableTiming));
+  const uint32_t rings = std::max(1u, pp.fill_waves);
+  for (uint32_t r = 0; r < rings; ++r)
+    __atomic_store_n(P.h_fill_head + (size_t)r * PagedState::kTailStride, 0ull, __ATOMIC_RELEASE);
+  pp.fill_head = P.d_fill_head;
+  RoundParams rp;
+  rp.lanes = P.d_round;
+  rp.admit = P.d_round + lanes;
+  rp.state = P.d_lane_state;
+  rp.state_words = words;
+  rp.out = P.d_lane_out;
+  uint32_t *h_lanes = P.h_round, *h_admit = P.h_round + lanes;
+
+  // fill waves in a kernel of their own, after the control words were reset on s
+  HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+  HIP_OR_FAIL(hipStreamWaitEvent(P.fill_stream, ix->ev_start, 0));
+  {
+    const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, (int)pp.fill_waves, P.fill_stream)
+                                                 : launch_paged_u8(pp, (int)pp.fill_waves, P.fill_stream);
+    if (le != hipSuccess) return fail(GORIO_EDEVICE, "fill kernel launch failed: %s", hipGetErrorString(le));
+  }
+
+  enum : uint8_t { kFree = 0, kRunnable = 1, kWaiting = 2, kRunning = 3 };
+  const uint64_t nq = pp.nq;
+  std::vector<uint8_t> lstate(lanes, kFree);
+  std::vector<uint32_t> epoch(lanes, 0);
+  std::vector<Clock::time_point> since(lanes);
+  std::vector<uint32_t> runq, freeq;
+  runq.reserve(lanes);
+  freeq.reserve(lanes);
+  for (uint32_t l = lanes; l-- > 0;) freeq.push_back(l);
+  using Waiter = std::pair<uint32_t, uint32_t>;  // lane, its park epoch
+  std::vector<std::vector<Waiter>> waiters(P.slots);
+  std::vector<Waiter> any_fill;
+  std::vector<uint64_t> ring_head(rings, 0);
+  const uint64_t cq_cap = P.cq_cap;
+  auto wake = [&](uint32_t lane, uint32_t ep) {
+    if (lstate[lane] == kWaiting && epoch[lane] == ep) {
+      lstate[lane] = kRunnable;
+      runq.push_back(lane);
+    }
+  };
+  auto poll_fills = [&]() {
+    bool progress = false;
+    for (uint32_t r = 0; r < rings; ++r) {
+      const uint64_t fh = __atomic_load_n(P.h_fill_head + (size_t)r * PagedState::kTailStride, __ATOMIC_ACQUIRE);
+      uint64_t &h = ring_head[r];
+      if (fh <= h) continue;
+      if (fh - h > cq_cap) h = fh - cq_cap;  // entries already reused by the proxy: the fallback wakes them
+      const unsigned long long *ring = P.h_cq + (size_t)r * cq_cap;
+      for (; h < fh; ++h) {
+        const uint32_t slot = (uint32_t)__atomic_load_n(&ring[h & (cq_cap - 1)], __ATOMIC_RELAXED);
+        if (slot >= P.slots) continue;
+        for (const Waiter &w : waiters[slot]) wake(w.first, w.second);
+        waiters[slot].clear();
+      }
+      progress = true;
+    }
+    if (progress && !any_fill.empty()) {
+      for (const Waiter &w : any_fill) wake(w.first, w.second);
+      any_fill.clear();
+    }
+    return progress;
+  };
+
+  const auto t0 = Clock::now();
+  auto last_sweep = t0;
+  const auto stale = std::chrono::milliseconds(4);
+  uint64_t admitted = 0, finished = 0;
+  gorio_status st = GORIO_OK;
+  while (finished < nq) {
+    const auto now = Clock::now();
+    if (std::chrono::duration<double>(now - t0).count() > limit_s) {
+      timed_out = true;
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      break;
+    }
+    if (now - last_sweep > std::chrono::milliseconds(1)) {  // lanes no fill has woken
+      last_sweep = now;
+      for (uint32_t l = 0; l < lanes; ++l)
+        if (lstate[l] == kWaiting && now - since[l] > stale) wake(l, epoch[l]);
+    }
+    uint32_t nlist = 0;
+    for (uint32_t lane : runq) {
+      h_lanes[nlist] = lane;
+      h_admit[nlist] = kNone;
+      lstate[lane] = kRunning;
+      ++nlist;
+    }
+    runq.clear();
+    while (!freeq.empty() && admitted < nq) {
+      const uint32_t lane = freeq.back();
+      freeq.pop_back();
+      h_lanes[nlist] = lane;
+      h_admit[nlist] = order.empty() ? (uint32_t)admitted : order[admitted];
+      lstate[lane] = kRunning;
+      ++admitted;
+      ++nlist;
+    }
+    if (nlist == 0) {
+      if (!poll_fills()) {
+        for (int i = 0; i < 32; ++i) GORIO_CPU_PAUSE();
+      }
+      continue;
+    }
+    const hipError_t le = ix->dtype == GORIO_F32 ? launch_rounds_f32(pp, rp, (int)nlist, s)
+                                                 : launch_rounds_u8(pp, rp, (int)nlist, s);
+    if (le != hipSuccess) {
+      st = fail(GORIO_EDEVICE, "round launch failed: %s", hipGetErrorString(le));
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      break;
+    }
+    HIP_OR_FAIL(hipEventRecord(P.ev_round, s));
+    hipError_t q;
+    while ((q = hipEventQuery(P.ev_round)) == hipErrorNotReady) GORIO_CPU_PAUSE();
+    if (q != hipSuccess) {
+      st = fail(GORIO_EDEVICE, "round failed: %s", hipGetErrorString(q));
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      break;
+    }
+    const auto done_at = Clock::now();
+    for (uint32_t i = 0; i < nlist; ++i) {
+      const uint32_t lane = h_lanes[i];
+      const LaneOut &o = P.h_lane_out[lane];
+      if (o.code == kLaneDone) {
+        ++finished;
+        lstate[lane] = kFree;
+        freeq.push_back(lane);
+        continue;
+      }
+      const uint32_t ep = ++epoch[lane];
+      lstate[lane] = kWaiting;
+      since[lane] = done_at;
+      const uint32_t nw = std::min(o.nwait, kLaneWaitCap);
+      for (uint32_t j = 0; j < nw; ++j)
+        if (o.wait[j] < P.slots) waiters[o.wait[j]].push_back({lane, ep});
+      if (o.retry || nw == 0) any_fill.push_back({lane, ep});
+    }
+    poll_fills();
+  }
+  // the fill waves leave once every query is done (or on abort)
+  HIP_OR_FAIL(hipEventRecord(P.ev_fill, P.fill_stream));
+  for (;;) {
+    const hipError_t q = hipEventQuery(P.ev_fill);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) return fail(GORIO_EDEVICE, "fill kernel failed: %s", hipGetErrorString(q));
+    if (!timed_out && std::chrono::duration<double>(Clock::now() - t0).count() > limit_s) {
+      timed_out = true;
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+    }
+    std::this_thread::sleep_for(std::chrono::microseconds(50));
+  }
+  HIP_OR_FAIL(hipStreamWaitEvent(s, P.ev_fill, 0));
+  HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+  return st;
+}
+
+// Paged search: reset the per-search rings and counters, fill in the kernel
+// parameters, arm the proxy, then run either the persistent kernel (GPU
+// scheduler, split-phase or blocking) or host-scheduled rounds, under a
+// watchdog.
 gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s, bool &timed_out) {
   PagedState &P = *ix->paged;
-  const uint32_t oversub = ix->blocking ? 1u : ix->oversub;
+  const bool host_rounds = ix->blocking == 2;
+  const bool blocking = ix->blocking == 1;
+  const uint32_t oversub = (blocking || host_rounds) ? 1u : ix->oversub;
   int dev = 0, cus = 0;
   HIP_OR_FAIL(hipGetDevice(&dev));
   HIP_OR_FAIL(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-  // concurrent queries: each may hold kMaxPendingPerQuery pins, kept within
-  // half the cache so the clock always finds victims for the rest
-  const uint32_t max_pending = (uint32_t)std::max(1, std::min(256, env_int("GORIO_MAX_PENDING", (int)kMaxPendingPerQuery)));
+  // concurrent queries: each may hold max_pending pins, kept within half the
+  // cache so the clock always finds victims for the rest
+  const uint32_t pend_dflt = ix->max_pending ? ix->max_pending : kMaxPendingPerQuery;
+  const uint32_t max_pending = (uint32_t)std::max(1, std::min(256, env_int("GORIO_MAX_PENDING", (int)pend_dflt)));
   const uint64_t q_cache = std::max<uint64_t>(1, P.slots / (2ull * max_pending));
-  const uint64_t q_live = std::min<uint64_t>({(uint64_t)cus * 8 * oversub, q_cache, rp.nq});
+  const uint64_t wave_cap = ix->query_waves ? ix->query_waves : (uint64_t)cus * 8;
+  const uint64_t q_live = std::min<uint64_t>({wave_cap * oversub, q_cache, rp.nq, host_rounds ? 8192ull : ~0ull});
+  // persistent kernel: query waves; host rounds: lanes
   const int qwaves = (int)std::max<uint64_t>(1, (q_live + oversub - 1) / oversub);
   // waves that only copy arriving pages, each from a completion ring of its
   // own, so the fill rate does not depend on how many queries run at once
-  // and no two waves contend for completions
-  const int fwaves = std::max(0, std::min((int)PagedState::kMaxRings, env_int("GORIO_FILL_WAVES", 32)));
+  // and no two waves contend for completions (host rounds need them)
+  int fwaves = std::max(0, std::min((int)PagedState::kMaxRings, env_int("GORIO_FILL_WAVES", 32)));
+  if (host_rounds) fwaves = std::max(fwaves, 1);
   const uint32_t rings = (uint32_t)std::max(1, fwaves);
-  const int grid = qwaves + fwaves;
   const uint64_t ht_entries = (uint64_t)qwaves * oversub << kPagedHtLog2;
   if (ht_entries > P.ht_pool_entries) {
     if (P.d_ht_pool) (void)hipFree(P.d_ht_pool);
@@ -413,13 +631,15 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.next_query = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kNextQuery));
   // admission order: cluster by cluster of the queries' nearest centroids
   DevBuf d_key, d_order;
+  std::vector<uint32_t> order;
   pp.order = nullptr;
   if (ix->order_clusters > 0) {
     HIP_OR_FAIL(d_key.alloc((size_t)rp.nq * 4));
     HIP_OR_FAIL(d_order.alloc((size_t)rp.nq * 4));
     HIP_OR_FAIL(launch_nearest_centroid(ix->dtype, rp.queries, rp.nq, ix->D, ix->d_centroids, ix->d_centroid_norms,
                                         ix->order_clusters, d_key.as<uint32_t>(), s));
-    std::vector<uint32_t> key(rp.nq), order(rp.nq);
+    std::vector<uint32_t> key(rp.nq);
+    order.resize(rp.nq);
     HIP_OR_FAIL(hipMemcpyAsync(key.data(), d_key.p, (size_t)rp.nq * 4, hipMemcpyDeviceToHost, s));
     HIP_OR_FAIL(hipStreamSynchronize(s));
     order_by_key(key.data(), rp.nq, ix->order_clusters, order.data());
@@ -427,13 +647,14 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
     pp.order = d_order.as<uint32_t>();
   }
   pp.done_queries = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kDoneQueries));
+  pp.fill_head = nullptr;
   pp.fill_waves = (uint32_t)fwaves;
   pp.out_ids = rp.out_ids;
   pp.out_dists = rp.out_dists;
   pp.ht_pool = P.d_ht_pool;
   pp.oversub = oversub;
   pp.max_pending = max_pending;
-  pp.blocking = ix->blocking;
+  pp.blocking = blocking ? 1 : 0;
   pp.stats = rp.stats;
 
   // test hooks: random extra delay per request (completions leave out of
@@ -441,31 +662,38 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   const char *jit = getenv("GORIO_PROXY_JITTER_US");
   P.proxy.begin(ix->latency_us, ix->max_outstanding, rings, jit ? atof(jit) : 0.0,
                 env_int("GORIO_PROXY_HOLD", 0) != 0);
-  HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
-  const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, grid, s) : launch_paged_u8(pp, grid, s);
-  if (le != hipSuccess) {
-    P.proxy.end();
-    return fail(GORIO_EDEVICE, "paged search launch failed: %s", hipGetErrorString(le));
-  }
-  HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
-  // watchdog: the kernel polls the abort flag (through its device mirror)
   const double limit_s = env_int("GORIO_WATCHDOG_S", 120);
-  const auto t0 = std::chrono::steady_clock::now();
-  for (;;) {
-    hipError_t q = hipEventQuery(ix->ev_stop);
-    if (q == hipSuccess) break;
-    if (q != hipErrorNotReady) {
+  gorio_status st = GORIO_OK;
+  if (host_rounds) {
+    st = run_host_rounds(ix, pp, (uint32_t)q_live, order, s, limit_s, timed_out);
+  } else {
+    const int grid = qwaves + fwaves;
+    HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+    const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, grid, s) : launch_paged_u8(pp, grid, s);
+    if (le != hipSuccess) {
       P.proxy.end();
-      return fail(GORIO_EDEVICE, "paged search failed: %s", hipGetErrorString(q));
+      return fail(GORIO_EDEVICE, "paged search launch failed: %s", hipGetErrorString(le));
     }
-    const double el = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-    if (!timed_out && el > limit_s) {
-      timed_out = true;
-      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+    HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+    // watchdog: the kernel polls the abort flag (through its device mirror)
+    const auto t0 = std::chrono::steady_clock::now();
+    for (;;) {
+      hipError_t q = hipEventQuery(ix->ev_stop);
+      if (q == hipSuccess) break;
+      if (q != hipErrorNotReady) {
+        P.proxy.end();
+        return fail(GORIO_EDEVICE, "paged search failed: %s", hipGetErrorString(q));
+      }
+      const double el = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+      if (!timed_out && el > limit_s) {
+        timed_out = true;
+        __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      }
+      std::this_thread::sleep_for(std::chrono::microseconds(200));
     }
-    std::this_thread::sleep_for(std::chrono::microseconds(200));
   }
   P.proxy.end();
+  if (st != GORIO_OK) return st;
   if (timed_out) {
     gorio_status rs = ix->reset_cache();  // pins and LOADING slots of aborted queries
     if (rs != GORIO_OK) return rs;
@@ -510,6 +738,9 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   if (!i_dev) { HIP_OR_FAIL(ibuf.alloc(obytes)); d_ids = ibuf.as<uint32_t>(); }
   if (!d_dev) { HIP_OR_FAIL(dbuf.alloc(obytes)); d_dists = dbuf.p; }
 
+  // the previous search of this index, on whatever stream it ran, finishes
+  // before this one clears the counters it shares
+  if (ix->ev_done_recorded) HIP_OR_FAIL(hipStreamWaitEvent(s, ix->ev_done, 0));
   fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(ix->d_stats), 2 * kStatWords, 0u);
 
   ResidentParams p;
@@ -546,6 +777,8 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   if (!d_dev) HIP_OR_FAIL(hipMemcpyAsync(dists, d_dists, obytes, hipMemcpyDeviceToHost, s));
   unsigned long long h_stats[kStatWords] = {};
   if (stats) HIP_OR_FAIL(hipMemcpyAsync(h_stats, ix->d_stats, sizeof h_stats, hipMemcpyDeviceToHost, s));
+  HIP_OR_FAIL(hipEventRecord(ix->ev_done, s));
+  ix->ev_done_recorded = true;
   if (stats || !i_dev || !d_dev || !q_dev) HIP_OR_FAIL(hipStreamSynchronize(s));
   if (stats) {
     float ms = 0.f;

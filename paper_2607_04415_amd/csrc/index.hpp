@@ -15,6 +15,8 @@ namespace gorio {
 
 gorio_status fail(gorio_status st, const char *fmt, ...);
 
+struct LaneOut;  // search_paged.hpp: a host-scheduled lane's report
+
 enum StatWord : int {
   kStatEval = 0,
   kStatReeval,
@@ -52,6 +54,17 @@ struct PagedState {
   static constexpr uint32_t kTailStride = 16;  // u64 words
   uint32_t *d_ht_pool = nullptr;
   uint64_t ht_pool_entries = 0;
+  // host-scheduled rounds: lane states (HBM), the round's lane list and the
+  // lanes' reports (host memory the kernels read and write), and how far each
+  // completion ring has been filled (written by the fill waves)
+  hipStream_t fill_stream = nullptr;
+  hipEvent_t ev_round = nullptr, ev_fill = nullptr;
+  uint32_t *d_lane_state = nullptr;
+  uint64_t lane_state_words = 0;
+  uint32_t *h_round = nullptr, *d_round = nullptr;   // 2 x round_cap: lanes, then admissions
+  uint32_t round_cap = 0;
+  LaneOut *h_lane_out = nullptr, *d_lane_out = nullptr;
+  unsigned long long *h_fill_head = nullptr, *d_fill_head = nullptr;
   Proxy proxy;
 
   enum Ctrl { kClock = 0, kMqTail, kCqHead, kTailSeen, kPollLock, kAbortSeen, kNextQuery, kDoneQueries, kCtrlWords = 8 };
@@ -68,6 +81,13 @@ struct PagedState {
     if (d_page_slot) (void)hipFree(d_page_slot);
     if (d_ctrl) (void)hipFree(d_ctrl);
     if (d_ht_pool) (void)hipFree(d_ht_pool);
+    if (d_lane_state) (void)hipFree(d_lane_state);
+    if (h_round) (void)hipHostFree(h_round);
+    if (h_lane_out) (void)hipHostFree(h_lane_out);
+    if (h_fill_head) (void)hipHostFree(h_fill_head);
+    if (fill_stream) (void)hipStreamDestroy(fill_stream);
+    if (ev_round) (void)hipEventDestroy(ev_round);
+    if (ev_fill) (void)hipEventDestroy(ev_fill);
     if (h_mq) (void)hipHostFree(h_mq);
     if (h_cq) (void)hipHostFree(h_cq);
     if (h_cq_tail) (void)hipHostFree(h_cq_tail);
@@ -77,6 +97,14 @@ struct PagedState {
     d_page_slot = nullptr;
     d_ctrl = nullptr;
     d_ht_pool = nullptr;
+    d_lane_state = nullptr;
+    lane_state_words = 0;
+    h_round = d_round = nullptr;
+    round_cap = 0;
+    h_lane_out = d_lane_out = nullptr;
+    h_fill_head = d_fill_head = nullptr;
+    fill_stream = nullptr;
+    ev_round = ev_fill = nullptr;
     h_mq = d_mq = h_cq = d_cq = h_cq_tail = d_cq_tail = nullptr;
     h_abort = d_abort = nullptr;
     slots = 0;
@@ -111,6 +139,9 @@ struct gorio_index {
   uint32_t max_outstanding = 4096;
   uint32_t oversub = 1;
   int blocking = 0;
+  // paged scheduler shape (gorio_set_scheduler); 0 = the library's choice
+  uint32_t query_waves = 0;   // waves that run queries
+  uint32_t max_pending = 0;   // page requests one query keeps outstanding
 
   // paged searches admit their queries cluster by cluster (gorio_set_query_order)
   uint32_t order_clusters = 0;
@@ -119,6 +150,11 @@ struct gorio_index {
 
   hipStream_t stream = nullptr;  // library-internal work (build, mode switches)
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+  // Recorded after the last operation of every search on the stream it used.
+  // The next search makes its own stream wait for it, so searches of one index
+  // issued on different streams never share the counters below at once.
+  hipEvent_t ev_done = nullptr;
+  bool ev_done_recorded = false;
   unsigned long long *d_stats = nullptr;
 
   uint64_t index_bytes() const { return num_pages * (uint64_t)page_bytes; }
@@ -180,6 +216,7 @@ struct gorio_index {
     if (d_centroid_norms) (void)hipFree(d_centroid_norms);
     if (ev_start) (void)hipEventDestroy(ev_start);
     if (ev_stop) (void)hipEventDestroy(ev_stop);
+    if (ev_done) (void)hipEventDestroy(ev_done);
     if (stream) (void)hipStreamDestroy(stream);
     d_pages = nullptr;
     h_backing = nullptr;
@@ -187,7 +224,8 @@ struct gorio_index {
     d_stats = nullptr;
     d_centroids = d_centroid_norms = nullptr;
     order_clusters = 0;
-    ev_start = ev_stop = nullptr;
+    ev_start = ev_stop = ev_done = nullptr;
+    ev_done_recorded = false;
     stream = nullptr;
   }
 };

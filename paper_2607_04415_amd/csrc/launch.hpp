@@ -17,9 +17,20 @@ namespace gorio {
 hipError_t launch_resident_u8(const ResidentParams &p, int grid, hipStream_t s);
 hipError_t launch_resident_f32(const ResidentParams &p, int grid, hipStream_t s);
 
-// Paged search: the persistent kernel (fill waves + query waves).
+// Paged search: the persistent kernel (fill waves + query waves).  With
+// grid == pp.fill_waves it runs only the fill waves.
 hipError_t launch_paged_u8(const PagedParams &pp, int grid, hipStream_t s);
 hipError_t launch_paged_f32(const PagedParams &pp, int grid, hipStream_t s);
+
+// Host-scheduled rounds: one workgroup per listed lane.
+hipError_t launch_rounds_u8(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s);
+hipError_t launch_rounds_f32(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s);
+
+// 32-bit words of one lane's saved state for a search with frontier size L.
+inline uint32_t lane_state_words(uint32_t L) {
+  const size_t b = L <= 64 ? sizeof(QSlot<1>) : L <= 128 ? sizeof(QSlot<2>) : sizeof(QSlot<4>);
+  return (uint32_t)((b + 3) / 4);
+}
 
 // Visited tables of the resident kernel: 16-bit entries (2^M::kHtLog2 of
 // them) when every id fits that table's domain, else 8192 32-bit entries.
@@ -89,6 +100,20 @@ hipError_t paged(const PagedParams &pp, int grid, hipStream_t s) {
   if (pp.L <= 64) return n2s ? paged_t<1, M, true>(pp, grid, s) : paged_t<1, M, false>(pp, grid, s);
   if (pp.L <= 128) return n2s ? paged_t<2, M, true>(pp, grid, s) : paged_t<2, M, false>(pp, grid, s);
   return n2s ? paged_t<4, M, true>(pp, grid, s) : paged_t<4, M, false>(pp, grid, s);
+}
+
+template <int KPL, class M, bool N2S>
+hipError_t rounds_t(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s) {
+  paged_round<KPL, M, N2S><<<grid, kWave, sizeof(QSlot<KPL>), s>>>(pp, rp);
+  return hipGetLastError();
+}
+
+template <class M>
+hipError_t rounds(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s) {
+  const bool n2s = pp.geom.node_to_slot != nullptr;
+  if (pp.L <= 64) return n2s ? rounds_t<1, M, true>(pp, rp, grid, s) : rounds_t<1, M, false>(pp, rp, grid, s);
+  if (pp.L <= 128) return n2s ? rounds_t<2, M, true>(pp, rp, grid, s) : rounds_t<2, M, false>(pp, rp, grid, s);
+  return n2s ? rounds_t<4, M, true>(pp, rp, grid, s) : rounds_t<4, M, false>(pp, rp, grid, s);
 }
 
 }  // namespace detail

@@ -8,4 +8,9 @@ hipError_t launch_paged_f32(const PagedParams &pp, int grid, hipStream_t s) {
   return detail::paged<MetricF32<64, false>>(pp, grid, s);
 }
 
+hipError_t launch_rounds_f32(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s) {
+  if (pp.D == 96) return detail::rounds<MetricF32<24, true>>(pp, rp, grid, s);
+  return detail::rounds<MetricF32<64, false>>(pp, rp, grid, s);
+}
+
 }  // namespace gorio

@@ -11,4 +11,12 @@ hipError_t launch_paged_u8(const PagedParams &pp, int grid, hipStream_t s) {
   return detail::paged<MetricU8<16, false>>(pp, grid, s);
 }
 
+hipError_t launch_rounds_u8(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s) {
+  if (pp.D == 128) return detail::rounds<MetricU8<4, true>>(pp, rp, grid, s);
+  const uint32_t vdw = (pp.D / 4 + 7) / 8;
+  if (vdw <= 1) return detail::rounds<MetricU8<1, false>>(pp, rp, grid, s);
+  if (vdw <= 4) return detail::rounds<MetricU8<4, false>>(pp, rp, grid, s);
+  return detail::rounds<MetricU8<16, false>>(pp, rp, grid, s);
+}
+
 }  // namespace gorio

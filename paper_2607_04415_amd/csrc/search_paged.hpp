@@ -59,6 +59,8 @@ struct PagedParams {
   unsigned int *next_query;
   const uint32_t *order;                  // nullptr: queries in index order; else admission order
   unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
+  unsigned long long *fill_head;          // host memory or nullptr: completions of ring k filled so far,
+                                          // at fill_head[k * tail_stride] (host-scheduled rounds)
   uint32_t *out_ids;
   uint32_t *out_dists;                    // distance bits (int32 or float32)
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
@@ -267,6 +269,36 @@ __device__ __forceinline__ bool query_runnable(const PagedParams &p, const QSlot
   ntodo = todo;
   if (p.blocking) return nwait == 0;
   return ntodo > 0 && nwait < p.max_pending;
+}
+
+// Start query qi in slot S: V = {entry}, and the entry is the first
+// candidate to evaluate (the frontier is empty until it is).
+template <int KPL>
+__device__ __forceinline__ void admit_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uint32_t qi) {
+  const int l = lane_id();
+  VisitedHbm<kPagedHtLog2>::clear(ht);
+  if (l == 0) {
+    S.qi = qi;
+    S.active = 1;
+    S.parked = 0;
+    S.phase = kPhEval;
+    S.nbeam = 0;
+    S.b0 = 0;
+    S.ncand = 1;
+    S.cand[0] = p.entry;
+    S.cstate[0] = kTodo;
+    S.ht_used = 1;
+    S.forgot = 0;
+  }
+#pragma unroll
+  for (int r = 0; r < KPL; ++r) S.F[r * kWave + l] = kInfKey;
+  __syncthreads();
+  {
+    uint32_t e1[1] = {p.entry};
+    bool v1[1] = {l == 0}, n1[1], r1[1];
+    VisitedHbm<kPagedHtLog2>::test_and_set_n<1>(ht, e1, v1, true, n1, r1);
+  }
+  __syncthreads();
 }
 
 // Runs one query until it finishes (returns true) or parks (false).
@@ -482,6 +514,7 @@ __device__ void fill_loop(const PagedParams &p, uint32_t k) {
   const unsigned long long *tail = p.cq_tail + (uint64_t)k * p.tail_stride;
   unsigned long long head = 0, served = 0;
   uint32_t idle = 0;
+  unsigned long long *filled = p.fill_head ? p.fill_head + (uint64_t)k * p.tail_stride : nullptr;
   for (;;) {
     if (k == 0 && l == 0) refresh_abort(p);
     if (aborted(p)) break;
@@ -502,6 +535,8 @@ __device__ void fill_loop(const PagedParams &p, uint32_t k) {
       served += good;
       head += good < n ? good + 1 : n;  // step over a malformed entry
     }
+    // host-scheduled rounds: entries [0, head) of this ring are now READY
+    if (filled && l == 0) __hip_atomic_store(filled, head, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (l == 0) atomicAdd(&p.stats[6], served);
 }
@@ -544,30 +579,7 @@ __global__ __launch_bounds__(kWave) void search_paged(PagedParams p) {
           continue;
         }
         if (p.order) qi = first_lane_value(p.order[qi]);
-        VisitedHbm<kPagedHtLog2>::clear(ht);
-        // V = {entry}: the entry is the first candidate to evaluate
-        if (l == 0) {
-          S.qi = qi;
-          S.active = 1;
-          S.parked = 0;
-          S.phase = kPhEval;
-          S.nbeam = 0;
-          S.b0 = 0;
-          S.ncand = 1;
-          S.cand[0] = p.entry;
-          S.cstate[0] = kTodo;
-          S.ht_used = 1;
-          S.forgot = 0;
-        }
-#pragma unroll
-        for (int r = 0; r < KPL; ++r) S.F[r * kWave + l] = kInfKey;
-        __syncthreads();
-        {
-          uint32_t e1[1] = {p.entry};
-          bool v1[1] = {l == 0}, n1[1], r1[1];
-          VisitedHbm<kPagedHtLog2>::test_and_set_n<1>(ht, e1, v1, true, n1, r1);
-        }
-        __syncthreads();
+        admit_query(p, S, ht, qi);
       } else if (S.parked) {
         any_active = true;
         if (!query_runnable(p, S)) continue;
@@ -609,6 +621,127 @@ __global__ __launch_bounds__(kWave) void search_paged(PagedParams p) {
     atomicAdd(&p.stats[6], ctr.served);
     atomicAdd(&p.stats[7], ctr.park);
     atomicAdd(&p.stats[8], ctr.resume);
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// Host-scheduled rounds (the host-scheduled comparison point of Sec. 5.1: a
+// query scheduler on the host coordinates many query lanes, over the same GPU
+// page cache, miss descriptors and proxy).  The host keeps the lanes' states
+// in HBM and chooses which lanes run in each launch; a launch runs every
+// chosen lane once, until its query finishes or parks, and reports what the
+// lane now waits for.  Fill waves run in a kernel of their own beside the
+// rounds and publish how far each completion ring has been filled, which is
+// the completion state the host schedules from.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kLaneWaitCap = 60;
+enum : uint32_t { kLaneIdle = 0, kLaneParked = 1, kLaneDone = 2 };
+
+// What a lane reported at the end of its turn (host memory, one per lane).
+struct LaneOut {
+  uint32_t code;                 // kLaneIdle (not runnable, not run), kLaneParked, kLaneDone
+  uint32_t nwait;                // entries of wait[]
+  uint32_t retry;                // 1: can proceed without one of wait[] arriving (requests it could
+                                 // not issue for want of a free slot, or more waits than wait[] holds)
+  uint32_t qi;                   // the lane's query
+  uint32_t wait[kLaneWaitCap];   // cache slots of the pages the lane waits for
+};
+
+struct RoundParams {
+  const uint32_t *lanes;   // this launch's lanes, one per workgroup (host memory)
+  const uint32_t *admit;   // per entry: query to start in the lane, or kNone to resume it
+  uint32_t *state;         // per lane: its QSlot, state_words 32-bit words (HBM)
+  uint32_t state_words;
+  LaneOut *out;            // per lane (host memory)
+};
+
+// Record which cache slots a parked lane waits for.
+template <int KPL>
+__device__ __forceinline__ void report_waits(const PagedParams &p, const QSlot<KPL> &S, LaneOut &o, uint32_t code) {
+  const int l = lane_id();
+  const uint32_t *items = S.cstate;
+  uint32_t n = 0;
+  if (S.phase == kPhExpand) {
+    items = S.bstate + S.b0;
+    n = min(S.nbeam - S.b0, min(kCandCap / p.R, (uint32_t)kPagedMaxW));
+  } else if (S.phase == kPhEval) {
+    n = S.ncand;
+  }
+  uint32_t cnt = 0, todo = 0;
+  for (uint32_t base = 0; base < n; base += kWave) {
+    const uint32_t c = base + l;
+    const uint32_t st = c < n ? items[c] : kDone;
+    const bool w = st < kDone;
+    const uint64_t mw = ballot(w);
+    const uint32_t pos = cnt + lanes_below(mw);
+    if (w && pos < kLaneWaitCap) o.wait[pos] = st;
+    cnt += (uint32_t)__popcll(mw);
+    todo += (uint32_t)__popcll(ballot(st == kTodo));
+  }
+  if (l == 0) {
+    o.nwait = min(cnt, kLaneWaitCap);
+    o.retry = (cnt > kLaneWaitCap || (todo > 0 && cnt < p.max_pending)) ? 1u : 0u;
+    o.qi = S.qi;
+    o.code = code;
+  }
+}
+
+template <int KPL, class M, bool N2S>
+__global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams r) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
+  QSlot<KPL> &S = *reinterpret_cast<QSlot<KPL> *>(lds);
+  uint32_t *sw = reinterpret_cast<uint32_t *>(lds);
+  const int l = lane_id();
+  const uint32_t lane = r.lanes[blockIdx.x];
+  const uint32_t qa = r.admit[blockIdx.x];
+  uint32_t *ht = p.ht_pool + ((uint64_t)lane << kPagedHtLog2);
+  uint32_t *st = r.state + (uint64_t)lane * r.state_words;
+  LaneOut &o = r.out[lane];
+  if (aborted(p)) {
+    if (l == 0) {
+      o.code = kLaneIdle;
+      o.nwait = 0;
+      o.retry = 1;
+    }
+    return;
+  }
+  PagedCounters ctr;
+  if (qa != kNone) {
+    admit_query(p, S, ht, qa);
+  } else {
+    for (uint32_t i = l; i < r.state_words; i += kWave) sw[i] = st[i];
+    __syncthreads();
+    if (!query_runnable(p, S)) {
+      report_waits(p, S, o, kLaneIdle);
+      return;
+    }
+    ++ctr.resume;
+  }
+  const bool done = run_query<KPL, M, N2S>(p, S, ht, qbuf, ctr);
+  if (done) {
+    if (l == 0) {
+      atomicAdd(p.done_queries, 1u);
+      o.nwait = 0;
+      o.retry = 0;
+      o.qi = S.qi;
+      o.code = kLaneDone;
+    }
+  } else {
+    ++ctr.park;
+    for (uint32_t i = l; i < r.state_words; i += kWave) st[i] = sw[i];
+    report_waits(p, S, o, kLaneParked);
+  }
+  if (l == 0) {
+    if (ctr.eval) atomicAdd(&p.stats[0], ctr.eval);
+    if (ctr.reeval) atomicAdd(&p.stats[1], ctr.reeval);
+    if (ctr.exp) atomicAdd(&p.stats[2], ctr.exp);
+    if (ctr.iter) atomicAdd(&p.stats[3], ctr.iter);
+    if (ctr.hit) atomicAdd(&p.stats[4], ctr.hit);
+    if (ctr.miss) atomicAdd(&p.stats[5], ctr.miss);
+    if (ctr.park) atomicAdd(&p.stats[7], ctr.park);
+    if (ctr.resume) atomicAdd(&p.stats[8], ctr.resume);
   }
 }
 

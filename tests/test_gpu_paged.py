@@ -8,7 +8,6 @@ import numpy as np
 import pytest
 
 import paper_2607_04415_amd as g
-import os
 
 from workload import IndexSpec, QuerySpec, WORKLOADS, index_arrays, query_array
 
@@ -300,37 +299,6 @@ def test_paged_f32_generic_dims(orc, torch_dev):
     ix.set_backing(latency_us=0.0, oversub=4)
     gi, gd, _ = search(torch_dev, ix, q, 10, 64, 4)
     assert_same(gi, gd, oids, od)
-
-
-F32_10M = WORKLOADS["f32-10m-cache5-lat20"]
-
-
-@pytest.mark.skipif(os.environ.get("GORIO_SKIP_BIG") == "1",
-                    reason="GORIO_SKIP_BIG=1: the 10M float32 index takes about a minute to generate")
-def test_workload_f32_10m_paged(orc, torch_dev):
-    """The 10M x 96-d float32 index at full size: 5% cache, 20 us latency, 4 query
-    slots per wave, on the first 1,000 queries; the paged answers equal the
-    resident kernel's, and both equal the oracle's on the first 100."""
-    w = F32_10M
-    a = index_arrays(w.index)
-    q = query_array(w.index, w.queries)[:1000]
-    ix = g.Index(a["x"], a["graph"])
-    e = ix.info["entry"]
-    assert e == orc.medoid(a["x"])
-    ri, rd, rst = search(torch_dev, ix, q, w.k, w.L, w.W)
-    ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))
-    assert ix.info["cache_slots"] == int(w.cache_frac * ix.info["index_bytes"]) // 4096
-    ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
-    gi, gd, st = search(torch_dev, ix, q, w.k, w.L, w.W)
-    assert_same(gi, gd, ri, rd)
-    assert st["expansions"] == rst["expansions"]
-    print(f"[f32 10m] resident {rst['kernel_ms']:.1f} ms, paged {st['kernel_ms']:.1f} ms for {len(q)} queries, "
-          f"hit rate {st['hits'] / max(1, st['hits'] + st['misses']):.3f}, "
-          f"{st['bytes_served'] / st['kernel_ms'] / 1e6:.2f} GB/s", flush=True)
-    ix.close()
-    packed = orc.pack(a["x"], a["graph"])
-    oids, od, oc, _ = packed.search(q[:100], w.k, w.L, w.W, e, threads=16)
-    assert_same(gi[:100], gd[:100], oids, od)
 
 
 RANDOM_CONFIGS = 10
