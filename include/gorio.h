@@ -211,6 +211,26 @@ gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq,
                           uint32_t k, uint32_t L, uint32_t W,
                           uint32_t *ids, void *dists, gorio_stats *stats, void *stream);
 
+/*
+ * gorio_search for callers that cannot allocate memory: code running under
+ * HIP graph capture, serving loops and harnesses that forbid hipMalloc.  It
+ * allocates nothing and stages nothing; the caller passes device buffers.
+ * Resident indexes only (a paged index -> GORIO_EUNSUPPORTED).
+ *   queries, ids, dists: device pointers, as for gorio_search (host pointers
+ *            -> GORIO_EINVAL).  k, L, W and nq: as for gorio_search.
+ *   stats:   NULL, or filled with kernel_ms, evaluations, reevaluations,
+ *            expansions and iterations (the call then waits for the search).
+ *   stream:  hipStream_t (NULL = the null stream).
+ * Scratch: the search's counters live in a fixed 128-byte device array of
+ * the library, one per GPU, kept until the process ends; no batch size needs
+ * more.  Each call clears it first.  Calls that overlap on one GPU (different
+ * indexes, streams or threads) share that array and race; serialise them.
+ * Results are the same as gorio_search's.
+ */
+gorio_status gorio_search_noalloc(gorio_index *ix, const void *queries, uint64_t nq,
+                                  uint32_t k, uint32_t L, uint32_t W,
+                                  uint32_t *ids, void *dists, gorio_stats *stats, void *stream);
+
 /* Facts about the index (entry node, page counts, mode). */
 gorio_status gorio_index_info_get(const gorio_index *ix, gorio_index_info *info);
 

@@ -56,7 +56,7 @@ class IndexInfo(ctypes.Structure):
 
 # every symbol include/gorio.h declares
 EXPORTS = ("gorio_build_index", "gorio_set_cache", "gorio_set_backing", "gorio_set_query_order",
-           "gorio_search", "gorio_index_info_get", "gorio_copy_pages", "gorio_locality_order",
+           "gorio_search", "gorio_search_noalloc", "gorio_index_info_get", "gorio_copy_pages", "gorio_locality_order",
            "gorio_cluster_order", "gorio_set_scheduler", "gorio_free_index", "gorio_last_error")
 
 _lib = None
@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.gorio_set_scheduler.argtypes = [v, u32, u32]
         L.gorio_search.restype = i32
         L.gorio_search.argtypes = [v, v, u64, u32, u32, u32, v, v, ctypes.POINTER(Stats), v]
+        L.gorio_search_noalloc.restype = i32
+        L.gorio_search_noalloc.argtypes = [v, v, u64, u32, u32, u32, v, v, ctypes.POINTER(Stats), v]
         L.gorio_index_info_get.restype = i32
         L.gorio_index_info_get.argtypes = [v, ctypes.POINTER(IndexInfo)]
         L.gorio_copy_pages.restype = i32
