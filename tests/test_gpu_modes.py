@@ -197,6 +197,7 @@ def test_workload_f32_10m_full(orc, torch_dev):
     e = ix.info["entry"]
     ri, rd, rst = search(torch_dev, ix, q, w.k, w.L, w.W)
     ix.close()
+    print(f"[f32 10m full] resident search done ({rst['kernel_ms']:.1f} ms)", flush=True)
     n2s, cent = g.cluster_order(a["x"], 512)
     px = g.Index(a["x"], a["graph"], vectors_first=True, node_to_slot=n2s)
     px.set_cache(int(w.cache_frac * px.info["index_bytes"]))
@@ -207,7 +208,14 @@ def test_workload_f32_10m_full(orc, torch_dev):
     print(f"[f32 10m full] resident {rst['kernel_ms']:.1f} ms, paged {st['kernel_ms']:.0f} ms, "
           f"hit rate {st['hits'] / max(1, st['hits'] + st['misses']):.3f}", flush=True)
     assert e == orc.medoid(a["x"])
-    oids, od, oc, _ = orc.pack(a["x"], a["graph"]).search(q, w.k, w.L, w.W, e, threads=16)
+    packed = orc.pack(a["x"], a["graph"])
+    print("[f32 10m full] oracle pages packed", flush=True)
+    oids, od, oc = [], [], []
+    for lo in range(0, len(q), 10_000):     # in slices, so progress shows
+        i_, d_, c_, _ = packed.search(q[lo:lo + 10_000], w.k, w.L, w.W, e, threads=16)
+        oids.append(i_), od.append(d_), oc.append(c_)
+        print(f"[f32 10m full] oracle {lo + len(i_):,} queries", flush=True)
+    oids, od, oc = np.concatenate(oids), np.concatenate(od), np.concatenate(oc)
     print("[f32 10m full] oracle done", flush=True)
     from test_gpu_parity import f32_acceptance
     for name, (xi, xd, xs) in (("resident", (ri, rd, rst)), ("paged", (gi, gd, st))):
