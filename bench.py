@@ -9,7 +9,13 @@ Prints one JSON line.  `value` is queries per second over the timed steps
 (inputs already resident in HBM).  `roofline` prices the search kernel's
 algorithmic bytes (expansions x (4 + 4R) + first-time evaluations x vector
 bytes) against its average duration, measured with HIP events on the launch
-stream.  `cpu_baseline` times the CPU oracle on a bounded sample.
+stream; `achieved_hbm_gbs` is the HBM traffic rocprofv3 counted for the same
+kernel (committed counter summary) over that duration.  `cpu_baseline` times
+the CPU oracle.  The same line carries the other configurations: the small
+uint8 index and the 10M x 96-d float32 index resident in HBM
+(`resident_legs`), and the paged legs (`paged`: cold 10% / 5% caches behind
+the host proxy, the blocking and host-scheduled modes, an equal-wave
+split-phase vs blocking comparison over injected latencies).
 """
 from __future__ import annotations
 
@@ -35,10 +41,12 @@ PROFILES = ROOT / "profiles"
 KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp", "paper_2607_04415_amd/csrc/frontier.hpp",
                   "paper_2607_04415_amd/csrc/metric.hpp", "paper_2607_04415_amd/csrc/launch.hpp",
                   "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
+MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
+T_START = time.perf_counter()
 
 
 def log(msg):
-    print(msg, file=sys.stderr, flush=True)
+    print(f"[bench {time.perf_counter() - T_START:6.1f}s] {msg}", file=sys.stderr, flush=True)
 
 
 def kernel_source_hash() -> str:
@@ -63,25 +71,49 @@ def measured_traffic(workload: str, layout: str):
     return t.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(a, q, w, gpu_ids, gpu_dists, sample_nq: int, threads: int):
-    """Time the CPU oracle on the first `sample_nq` queries with `threads` threads
-    on disjoint shards; also check the GPU answers on that sample."""
+def oracle_threads() -> tuple[int, int]:
+    """(T, nproc): threads for the CPU oracle and the CPUs this process may run
+    on.  T is nproc, capped at the host's per-GPU CPU share (OMP_NUM_THREADS,
+    else 16)."""
+    nproc = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    share = int(os.environ.get("OMP_NUM_THREADS", "16") or 16)
+    return max(1, min(nproc, share)), nproc
+
+
+def cpu_baseline(a, q, w, gpu_ids, gpu_dists, sample_nq: int, one_thread_nq: int, packed=None):
+    """Time the CPU oracle on the first `sample_nq` queries with T threads on
+    disjoint shards, and with one thread on the first `one_thread_nq`; also
+    check the GPU answers on the T-thread sample."""
     from oracle import load
     orc = load()
-    packed = orc.pack(a["x"], a["graph"])
+    t0 = time.perf_counter()
+    if packed is None:
+        packed = orc.pack(a["x"], a["graph"])
     entry = orc.medoid(a["x"])
+    prep = time.perf_counter() - t0
+    threads, nproc = oracle_threads()
     qs = q[:sample_nq]
     t0 = time.perf_counter()
     oids, od, oc, _ = packed.search(qs, w.k, w.L, w.W, entry, threads=threads)
     dt = time.perf_counter() - t0
-    exact = bool(np.array_equal(oids, gpu_ids[:sample_nq]) and np.array_equal(od, gpu_dists[:sample_nq]))
+    exact = bool(np.array_equal(oids, gpu_ids[:sample_nq])
+                 and np.array_equal(od.view(np.uint32), gpu_dists[:sample_nq].view(np.uint32)))
+    one = None
+    if one_thread_nq > 0:
+        t0 = time.perf_counter()
+        packed.search(q[:one_thread_nq], w.k, w.L, w.W, entry, threads=1)
+        dt1 = time.perf_counter() - t0
+        one = {"value": round(one_thread_nq / dt1, 1), "unit": "queries/s",
+               "sample": f"first {one_thread_nq} queries, 1 thread, {dt1:.2f} s"}
     counts = {"queries": len(qs), "evaluations": int(oc["evaluations"].sum()),
-              "expansions": int(oc["expansions"].sum())}
-    return {
+              "expansions": int(oc["expansions"].sum()), "iterations": int(oc["iterations"].sum())}
+    base = {
         "value": round(sample_nq / dt, 1), "unit": "queries/s", "cores": threads, "kind": "oracle",
-        "sample": f"first {sample_nq} of {len(q)} queries of the same workload, "
-                  f"{threads} threads on disjoint query shards, {dt:.2f} s wall",
-    }, exact, entry, counts
+        "sample": f"first {sample_nq} of {len(q)} queries of the same workload, {threads} threads on "
+                  f"disjoint query shards, {dt:.2f} s wall (page packing and medoid {prep:.1f} s, not timed)",
+        "nproc": nproc, "one_thread": one,
+    }
+    return base, exact, entry, counts, (oids, od), packed
 
 
 def recall_at_k(x: np.ndarray, q: np.ndarray, ids: np.ndarray, k: int, sample: int) -> dict:
@@ -116,7 +148,7 @@ def gather_ceiling(n: int, rpp: int, page_bytes: int, vec_stride: int):
     r = subprocess.run([str(exe), str(n), str(rpp), str(page_bytes), str(vec_stride)],
                        capture_output=True, text=True, timeout=120)
     if r.returncode != 0:
-        log(f"[bench] gather ceiling probe failed: {r.stderr.strip()}")
+        log(f"gather ceiling probe failed: {r.stderr.strip()}")
         return None
     d = json.loads(r.stdout.strip().splitlines()[-1])
     best = max(d[k]["gbs"] for k in d if k.startswith("rounds_"))
@@ -150,14 +182,83 @@ def host_link_peak_gbs(torch) -> float:
     return best
 
 
-def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: bool = False,
-              vectors_first: bool = False, repeats: int = 5, clusters=None):
+def algorithmic_bytes(st: dict, R: int, vec_bytes: int, oracle_evals=None):
+    """(bytes, source): expansions x (4 + 4R) + first-time evaluations x vector
+    bytes.  First-time evaluations are the oracle's |V| when it ran on the whole
+    batch; otherwise the GPU's evaluations minus those its visited filter could
+    not record (a lower bound: an unrecorded evaluation may still be a first)."""
+    if oracle_evals is not None:
+        return st["expansions"] * (4 + 4 * R) + oracle_evals * vec_bytes, "oracle"
+    return st["expansions"] * (4 + 4 * R) + (st["evaluations"] - st["reevaluations"]) * vec_bytes, \
+        "gpu lower bound (evaluations minus unrecorded ones)"
+
+
+def resident_leg(torch, g, a, q, w, layout: str, steps: int, warmup: int):
+    """Build the index in `layout`, run the warm-up and the timed steps.
+
+    Timed steps are issued back to back on the stream, as a serving loop would:
+    no host round trip per batch (the call returns once the search is queued).
+    HIP events recorded on the same stream around each call give every launch's
+    duration; the counters come from one more call after the timed region."""
+    ix = g.Index(a["x"], a["graph"], vectors_first=layout == "vectors-first")
+    info = ix.info
+    nq = len(q)
+    qd = torch.from_numpy(q).cuda()
+    ids = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
+    dists = torch.empty((nq, w.k), dtype=torch.int32 if q.dtype == np.uint8 else torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    for _ in range(warmup):
+        ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
+    cur = torch.cuda.current_stream()
+    events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream, stats=False)
+        e1.record(cur)
+        events.append((e0, e1))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernel_ms = [x.elapsed_time(y) for x, y in events]
+    st = ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
+    ix.close()
+    del qd
+    log(f"{w.name} {layout}: {steps} steps: {elapsed * 1e3 / steps:.3f} ms/step, {nq * steps / elapsed:,.0f} queries/s")
+    return {"info": info, "elapsed": elapsed, "kernel_ms": kernel_ms, "stats": st,
+            "ids": ids.cpu().numpy().view(np.uint32), "dists": dists.cpu().numpy()}
+
+
+def roofline_of(res: dict, w, R: int, oracle_evals, traffic, kernel: str) -> dict:
+    st = res["stats"]
+    alg, src = algorithmic_bytes(st, R, w.index.vec_bytes, oracle_evals)
+    kms = float(np.mean(res["kernel_ms"]))
+    achieved = alg / (kms * 1e-3) / 1e9
+    r = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+         "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": kernel,
+         "kernel_ms_avg": round(kms, 4), "algorithmic_bytes_per_launch": int(alg), "algorithmic_counts": src}
+    if src != "oracle":   # the range the unrecorded evaluations leave open
+        hi = st["expansions"] * (4 + 4 * R) + st["evaluations"] * w.index.vec_bytes
+        r["algorithmic_upper_gbs"] = round(hi / (kms * 1e-3) / 1e9, 1)
+    if traffic:
+        r["traffic_gbs"] = round(traffic / (kms * 1e-3) / 1e9, 1)
+        r["traffic_frac"] = round(traffic / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    return r
+
+
+def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, mode: int = 0,
+              vectors_first: bool = True, repeats: int = 5, clusters=None, warmup_nq: int = 2000,
+              query_waves: int = 0, max_pending: int = 0, latency_us=None, oversub=None, label=None):
     """Cold-cache paged searches over the first nq_sample queries of workload w:
-    `repeats` timed runs, each after set_cache has emptied the cache; the
-    figures are the median run's.  clusters = (node_to_slot, centroids): pages
-    placed cluster by cluster and queries admitted cluster by cluster."""
+    one untimed warm-up search on the first warmup_nq queries, then `repeats`
+    timed runs, each from a cache that set_cache has just emptied; the figures
+    are the median run's.  clusters = (node_to_slot, centroids): pages placed
+    cluster by cluster and queries admitted cluster by cluster."""
     from workload import query_array
     q = query_array(w.index, w.queries)[:nq_sample]
+    lat = w.latency_us if latency_us is None else latency_us
+    ovs = (w.oversub if oversub is None else oversub) if mode == 0 else 1
     ix = g.Index(a["x"], a["graph"], vectors_first=vectors_first,
                  node_to_slot=None if clusters is None else clusters[0])
     if clusters is not None:
@@ -166,30 +267,40 @@ def paged_leg(torch, g, a, w, nq_sample: int, resident_qps: float, blocking: boo
     ids = torch.empty((len(q), w.k), dtype=torch.int32, device="cuda")
     dists = torch.empty((len(q), w.k), dtype=torch.int32 if q.dtype == np.uint8 else torch.float32,
                         device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def configure():
+        ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))      # empty cache
+        ix.set_backing(latency_us=lat, oversub=ovs, mode=mode)
+        ix.set_scheduler(query_waves=query_waves, max_pending=max_pending)
+
+    configure()
+    wn = min(warmup_nq, len(q))
+    ix.search_into(qd[:wn], wn, w.k, w.L, w.W, ids[:wn], dists[:wn], stream=stream)
     runs = []
     for _ in range(max(1, repeats)):
-        ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))      # empty cache
-        ix.set_backing(latency_us=w.latency_us, oversub=1 if blocking else w.oversub, blocking=blocking)
+        configure()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        st = ix.search_into(qd, len(q), w.k, w.L, w.W, ids, dists,
-                            stream=torch.cuda.current_stream().cuda_stream)
+        st = ix.search_into(qd, len(q), w.k, w.L, w.W, ids, dists, stream=stream)
         torch.cuda.synchronize()
         runs.append((time.perf_counter() - t0, st))
-    runs.sort(key=lambda r: r[0])
-    wall, st = runs[len(runs) // 2]
+    order = sorted(range(len(runs)), key=lambda i: runs[i][0])
+    wall, st = runs[order[len(runs) // 2]]
     ms = st["kernel_ms"]
     acc = st["hits"] + st["misses"]
-    out = {"workload": w.name, "queries": len(q), "blocking": blocking,
+    out = {"workload": w.name, "queries": len(q), "mode": MODES[mode], "label": label or MODES[mode],
            "placement": "identity" if clusters is None else f"clusters ({len(clusters[1])}, queries by cluster)",
-           "cache_slots": ix.info["cache_slots"], "latency_us": w.latency_us,
-           "oversub": 1 if blocking else w.oversub, "runs": len(runs),
+           "cache_slots": ix.info["cache_slots"], "latency_us": lat, "oversub": ovs,
+           "query_waves": query_waves or "default", "max_pending": max_pending or 32,
+           "warmup_queries": wn, "runs": len(runs),
            "qps": round(len(q) / wall, 1), "qps_runs": [round(len(q) / r[0], 1) for r in runs],
            "kernel_ms": round(ms, 2),
            "hit_rate": round(st["hits"] / max(1, acc), 4),
            "pages_served": st["pages_served"],
+           "link_mb_per_query": round(st["bytes_served"] / len(q) / 1e6, 3),
            "miss_service_gbs": round(st["bytes_served"] / (ms * 1e-3) / 1e9, 2),
-           "parks": st["parks"], "resumes": st["resumes"],
+           "parks": st["parks"], "resumes": st["resumes"], "proxy_peak": st["proxy_peak"],
            "vs_resident_qps": round(len(q) / wall / resident_qps, 5) if resident_qps else None}
     ix.close()
     return out, ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), q
@@ -203,9 +314,10 @@ def main():
     ap.add_argument("--workload", default="u8-1m-hbm")
     ap.add_argument("--layout", choices=LAYOUTS, default="vectors-first",
                     help="page layout of the timed index (the other one is timed too and reported)")
-    ap.add_argument("--no-other-layout", action="store_true",
-                    help="do not time the other page layout")
+    ap.add_argument("--no-other-layout", action="store_true", help="do not time the other page layout")
     ap.add_argument("--cpu-sample", type=int, default=10000)
+    ap.add_argument("--one-thread-sample", type=int, default=2000,
+                    help="queries the 1-thread oracle baseline runs (0 = skip)")
     ap.add_argument("--recall-sample", type=int, default=100,
                     help="queries whose recall@k against exact top-k is reported (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -213,18 +325,29 @@ def main():
                     help="skip the random-gather ceiling probe (microbench/gather_ceiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration)")
+    ap.add_argument("--no-small", action="store_true", help="skip the 10k-vector uint8 leg")
     ap.add_argument("--paged-sample", type=int, default=-1,
-                    help="queries of each paged configuration to run (-1 = its full query count, "
+                    help="queries of each 1M paged configuration to run (-1 = its full query count, "
                          "0 = skip the paged legs)")
     ap.add_argument("--paged-clusters", type=int, default=-1,
                     help="paged legs: k-means clusters for page placement and query admission (0 = off, "
                          "-1 = by the leg's query count: 256 up to 20k queries, 512 above)")
-    ap.add_argument("--paged-repeats", type=int, default=3,
-                    help="cold-cache runs per paged leg of up to 20k queries (the median is reported); "
-                         "larger legs run once")
-    ap.add_argument("--f32-sample", type=int, default=0,
-                    help="queries of the 10M x 96-d float32 paged configuration to run (0 = skip; "
-                         "generating that index takes minutes the first time)")
+    ap.add_argument("--paged-repeats", type=int, default=5,
+                    help="cold-cache runs per paged leg of up to 20k queries (the median is reported)")
+    ap.add_argument("--large-repeats", type=int, default=3,
+                    help="cold-cache runs per paged leg of more than 20k queries")
+    ap.add_argument("--ablation-sample", type=int, default=5000,
+                    help="queries of the equal-wave split-phase vs blocking comparison (0 = skip)")
+    ap.add_argument("--ablation-latencies", default="0,20,200",
+                    help="injected latencies (us) of that comparison")
+    ap.add_argument("--f32-sample", type=int, default=-1,
+                    help="queries of the 10M x 96-d float32 legs (-1 = all 100,000; 0 = skip)")
+    ap.add_argument("--no-f32-paged", action="store_true", help="run the float32 resident leg only")
+    ap.add_argument("--f32-clusters", type=int, default=512)
+    ap.add_argument("--f32-cpu-sample", type=int, default=2000,
+                    help="float32 queries the oracle runs (baseline and the GPU answers' check)")
+    ap.add_argument("--budget-s", type=float, default=500.0,
+                    help="legs that would end past this many seconds are skipped and listed")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: runs on one GPU only (asked for {args.gpus}); "
@@ -234,7 +357,7 @@ def main():
 
     import torch
     import paper_2607_04415_amd as g
-    from workload import WORKLOADS, index_arrays, query_array
+    from workload import WORKLOADS, index_arrays, index_cached, query_array
 
     if not g.LIB_PATH.exists():
         raise SystemExit("libgorio.so is not built: run python __graft_entry__.py build")
@@ -248,189 +371,255 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "launches": 5}), flush=True)
         return
+    skipped = []
+
+    def fits(name: str, est_s: float) -> bool:
+        if time.perf_counter() - T_START + est_s <= args.budget_s:
+            return True
+        skipped.append({"leg": name, "estimated_s": est_s,
+                        "at_s": round(time.perf_counter() - T_START, 1)})
+        log(f"skipping {name}: {est_s:.0f} s would pass the {args.budget_s:.0f} s budget")
+        return False
+
+    # ------------------------------------------------------------------ main
     w = WORKLOADS[args.workload]
-    log(f"[bench] workload {w.name}: {w.description}")
-    t0 = time.perf_counter()
+    log(f"workload {w.name}: {w.description}")
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
-    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f} s")
-    qd = torch.from_numpy(q).cuda()
+    log("inputs ready")
     nq = len(q)
-
-    def timed(layout: str):
-        """Build the index in `layout`, run the warm-up and the timed steps."""
-        ix = g.Index(a["x"], a["graph"], vectors_first=layout == "vectors-first")
-        info = ix.info
-        if w.cache_frac < 1.0:
-            ix.set_cache(int(w.cache_frac * info["index_bytes"]))
-            ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
-        ids = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
-        dists = torch.empty((nq, w.k), dtype=torch.int32, device="cuda")
-        stream = torch.cuda.current_stream().cuda_stream
-        for _ in range(args.warmup):
-            ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)
-        # Timed steps are issued back to back on the stream, as a serving loop
-        # would: no host round trip per batch (the call returns once the search
-        # is queued).  HIP events recorded on the same stream around each call
-        # give every launch's duration; the counters come from one more call
-        # after the timed region.
-        cur = torch.cuda.current_stream()
-        events = []
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(cur)
-            ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream, stats=False)
-            e1.record(cur)
-            events.append((e0, e1))
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t0
-        kernel_ms = [a.elapsed_time(b) for a, b in events]
-        stats = [ix.search_into(qd, nq, w.k, w.L, w.W, ids, dists, stream=stream)]
-        ix.close()
-        log(f"[bench] {layout}: {args.steps} steps: {elapsed * 1e3 / args.steps:.3f} ms/step, "
-            f"{nq * args.steps / elapsed:,.0f} queries/s")
-        return info, elapsed, kernel_ms, stats, ids, dists
-
-    info, elapsed, kernel_ms, stats, ids, dists = timed(args.layout)
-    ms_per_step = elapsed * 1e3 / args.steps
-    qps = nq * args.steps / elapsed
+    main_res = resident_leg(torch, g, a, q, w, args.layout, args.steps, args.warmup)
+    info, st = main_res["info"], main_res["stats"]
+    qps = nq * args.steps / main_res["elapsed"]
+    ms_per_step = main_res["elapsed"] * 1e3 / args.steps
+    gi, gd = main_res["ids"], main_res["dists"]
     other = None
     if not args.no_other_layout:
         o_layout = [x for x in LAYOUTS if x != args.layout][0]
-        _, o_el, o_kms, _, o_ids, o_d = timed(o_layout)
-        other = {"layout": o_layout, "value": round(nq * args.steps / o_el, 1),
-                 "ms_per_step": round(o_el * 1e3 / args.steps, 4),
-                 "kernel_ms_avg": round(float(np.mean(o_kms)), 4),
-                 "same_answers": bool(torch.equal(o_ids, ids) and torch.equal(o_d, dists))}
+        o = resident_leg(torch, g, a, q, w, o_layout, args.steps, args.warmup)
+        other = {"layout": o_layout, "value": round(nq * args.steps / o["elapsed"], 1),
+                 "ms_per_step": round(o["elapsed"] * 1e3 / args.steps, 4),
+                 "kernel_ms_avg": round(float(np.mean(o["kernel_ms"])), 4),
+                 "same_answers": bool(np.array_equal(o["ids"], gi) and np.array_equal(o["dists"], gd))}
 
-    gi = ids.cpu().numpy().view(np.uint32)
-    gd = dists.cpu().numpy()
-    cpu = None
-    exact = None
-    ocounts = None
+    cpu = exact = ocounts = packed_main = None
     if not args.no_cpu_baseline:
-        threads = min(os.cpu_count() or 1, 16)
-        cpu, exact, entry, ocounts = cpu_baseline(a, q, w, gi, gd, min(args.cpu_sample, nq), threads)
+        cpu, exact, entry, ocounts, _, packed_main = cpu_baseline(a, q, w, gi, gd, min(args.cpu_sample, nq),
+                                                                  min(args.one_thread_sample, nq))
         assert entry == info["entry"], "entry node differs from the oracle's"
-        log(f"[bench] oracle on CPU: {cpu['value']:,.0f} queries/s with {threads} threads; "
+        log(f"oracle on CPU: {cpu['value']:,.0f} queries/s with {cpu['cores']} threads (nproc {cpu['nproc']}); "
             f"GPU answers oracle-exact on the sample: {exact}")
-
-    # Algorithmic bytes: every expansion reads 4 + 4R bytes, every node of V
-    # (first-time evaluations) its vector.  |V| is exact from the oracle's
-    # counts when it ran on the whole batch; otherwise the GPU's evaluations
-    # minus those it could not record in its visited filter (a lower bound:
-    # an unrecorded evaluation may still be the node's first).
-    st = stats[-1]
     R = info["R"]
-    vec_bytes = w.index.vec_bytes
-    if ocounts is not None and ocounts["queries"] == nq:
-        first_evals, counts_source = ocounts["evaluations"], "oracle"
-    else:
-        first_evals, counts_source = st["evaluations"] - st["reevaluations"], "gpu lower bound"
-    alg_bytes = st["expansions"] * (4 + 4 * R) + first_evals * vec_bytes
-    avg_kernel_ms = float(np.mean(kernel_ms))
-    achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
+    full_counts = ocounts["evaluations"] if ocounts is not None and ocounts["queries"] == nq else None
     traffic = measured_traffic(w.name, args.layout)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic,
-                "kernel": "search_resident<MetricU8>", "kernel_ms_avg": round(avg_kernel_ms, 4),
-                "algorithmic_bytes_per_launch": int(alg_bytes),
-                "algorithmic_counts": counts_source,
-                "expansions_match_oracle": (None if counts_source != "oracle"
-                                            else ocounts["expansions"] == st["expansions"])}
-
+    kname = "search_resident<MetricU8>" if w.index.dtype == "u8" else "search_resident<MetricF32>"
+    roofline = roofline_of(main_res, w, R, full_counts, traffic, kname)
+    if full_counts is not None:
+        roofline["expansions_match_oracle"] = ocounts["expansions"] == st["expansions"]
     if not args.no_gather_ceiling and args.layout == "vectors-first" and w.index.dtype == "u8":
         gc = gather_ceiling(w.index.n, info["records_per_page"], info["page_bytes"], 128)
         if gc is not None:
             roofline["gather_ceiling_gbs"] = gc["gbs"]
-            roofline["frac_of_gather_ceiling"] = round(achieved / gc["gbs"], 4)
-            log(f"[bench] random 128-B gather ceiling: {gc['gbs']:,.0f} GB/s "
-                f"({gc['vectors']:,} vectors, {gc['waves']} waves); achieved {achieved:,.0f} GB/s")
-
+            roofline["frac_of_gather_ceiling"] = round(roofline["achieved"] / gc["gbs"], 4)
+            log(f"random 128-B gather ceiling: {gc['gbs']:,.0f} GB/s; achieved {roofline['achieved']:,.0f} GB/s")
     recall = None
     if args.recall_sample > 0:
         recall = recall_at_k(a["x"], q, gi, w.k, min(args.recall_sample, nq))
-        log(f"[bench] recall@{w.k} on {recall['queries']} queries: {recall['value']}")
+        log(f"recall@{w.k} on {recall['queries']} queries: {recall['value']}")
 
+    resident_legs = []
+    # ------------------------------------------------------------ small index
+    if not args.no_small and w.name != "u8-10k-hbm":
+        ws = WORKLOADS["u8-10k-hbm"]
+        a_s = index_arrays(ws.index)
+        q_s = query_array(ws.index, ws.queries)
+        r = resident_leg(torch, g, a_s, q_s, ws, "vectors-first", args.steps, args.warmup)
+        cb, ex, _, oc, _, _ = cpu_baseline(a_s, q_s, ws, r["ids"], r["dists"], len(q_s), len(q_s))
+        resident_legs.append({
+            "workload": ws.name, "queries": len(q_s),
+            "value": round(len(q_s) * args.steps / r["elapsed"], 1), "unit": "queries/s",
+            "ms_per_step": round(r["elapsed"] * 1e3 / args.steps, 4), "steps": args.steps,
+            "oracle_exact": ex, "roofline": roofline_of(r, ws, ws.index.R, oc["evaluations"], None,
+                                                        "search_resident<MetricU8>"),
+            "cpu_baseline": cb})
+        log(f"{ws.name}: oracle-exact {ex}")
+
+    # ------------------------------------------------------------------ paged
     paged = None
     miss_gbs = None
     if args.paged_sample != 0 and w.name == "u8-1m-hbm":
         link = host_link_peak_gbs(torch)
         legs = []
         placements = {}
+        vfirst = args.layout == "vectors-first"
 
         def placement(nq_leg):
             k = cluster_count(args.paged_clusters, nq_leg)
             if k and k not in placements:
                 t0 = time.perf_counter()
                 placements[k] = g.cluster_order(a["x"], k)
-                log(f"[bench] cluster placement ({k} clusters) in {time.perf_counter() - t0:.1f} s")
+                log(f"cluster placement ({k} clusters) in {time.perf_counter() - t0:.2f} s")
             return placements.get(k)
 
-        # C3 (10k queries, 0 us): split-phase and blocking; the identity
-        # placement beside them; C4 (100k queries, 20 us): split-phase, one run
-        clustered = args.paged_clusters != 0
-        plan = [("u8-1m-cache10-lat0", False, clustered), ("u8-1m-cache10-lat0", True, clustered)]
-        if clustered:
-            plan.append(("u8-1m-cache10-lat0", False, False))   # identity placement, index order
-        plan.append(("u8-1m-cache10-lat20", False, clustered))
-        for name, blocking, use_clusters in plan:
-            wl = WORKLOADS[name]
-            nq_leg = wl.queries.nq if args.paged_sample < 0 else min(args.paged_sample, wl.queries.nq)
-            cl = placement(nq_leg) if use_clusters else None
-            reps = args.paged_repeats if nq_leg <= 20000 else 1
-            leg, pi, pd, pq = paged_leg(torch, g, a, wl, nq_leg, qps, blocking,
-                                        vectors_first=args.layout == "vectors-first",
-                                        repeats=reps, clusters=cl)
-            # the paged results must equal the resident results on the same queries
+        def check(leg, pi, pd, pq, wl):
+            # every paged answer must equal the resident kernel's on the same queries
             if wl.queries == w.queries:
                 leg["equals_resident"] = bool(np.array_equal(pi, gi[:len(pq)]) and np.array_equal(pd, gd[:len(pq)]))
-            log(f"[bench] paged {name} ({len(pq)} queries) blocking={blocking} {leg['placement']}: "
-                f"{leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, miss service {leg['miss_service_gbs']} GB/s")
-            legs.append(leg)
-        miss_gbs = legs[0]["miss_service_gbs"]
-        paged = {"host_link_peak_gbs": round(link, 1), "legs": legs,
-                 "split_phase_vs_blocking": round(legs[0]["qps"] / max(1e-9, legs[1]["qps"]), 3)}
-        if clustered:
-            paged["clusters_vs_identity"] = round(legs[0]["qps"] / max(1e-9, legs[2]["qps"]), 3)
+            if exact is not None and wl.queries == w.queries and len(pq) <= args.cpu_sample:
+                leg["oracle_exact"] = bool(exact and leg.get("equals_resident"))
+            log(f"paged {wl.name} ({len(pq)} queries) {leg['label']} {leg['placement']}: {leg['qps']:,.0f} q/s, "
+                f"hit rate {leg['hit_rate']:.3f}, miss service {leg['miss_service_gbs']} GB/s")
 
-    if args.f32_sample > 0:
-        wf = WORKLOADS["f32-10m-cache5-lat20"]
-        log(f"[bench] {wf.name}: loading or generating the index")
-        af = index_arrays(wf.index)
-        qf = query_array(wf.index, wf.queries)[:args.f32_sample]
-        # the same queries on the HBM-resident index: the reference answers and rate
-        ixr = g.Index(af["x"], af["graph"], vectors_first=args.layout == "vectors-first")
-        ri, rd, rst = ixr.search(torch.from_numpy(qf).cuda(), wf.k, wf.L, wf.W)
-        torch.cuda.synchronize()
-        ri, rd = ri.cpu().numpy().view(np.uint32), rd.cpu().numpy()
-        rqps = len(qf) / (rst["kernel_ms"] * 1e-3)
-        ixr.close()
-        fclusters = None
-        fk = cluster_count(args.paged_clusters, len(qf))
-        if fk:
-            t0 = time.perf_counter()
-            fclusters = g.cluster_order(af["x"], fk)
-            log(f"[bench] {wf.name}: cluster placement ({fk} clusters) in "
-                f"{time.perf_counter() - t0:.1f} s")
-        leg, pi, pd, _ = paged_leg(torch, g, af, wf, args.f32_sample, rqps,
-                                   vectors_first=args.layout == "vectors-first", repeats=1, clusters=fclusters)
-        leg["resident_kernel_qps"] = round(rqps, 1)
-        leg["equals_resident"] = bool(np.array_equal(pi, ri) and np.array_equal(pd.view(np.uint32), rd.view(np.uint32)))
-        log(f"[bench] paged {wf.name}: {leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, "
-            f"miss service {leg['miss_service_gbs']} GB/s (resident {rqps:,.0f} q/s)")
-        if paged is None:
-            paged = {"host_link_peak_gbs": round(host_link_peak_gbs(torch), 1), "legs": []}
-        paged["legs"].append(leg)
-        del af
+        clustered = args.paged_clusters != 0
+        w3 = WORKLOADS["u8-1m-cache10-lat0"]
+        n3 = w3.queries.nq if args.paged_sample < 0 else min(args.paged_sample, w3.queries.nq)
+        # C3 legs: split-phase, blocking (one query per wave: equal live queries),
+        # identity placement, host-scheduled rounds
+        plan = [(0, clustered, "split-phase"), (1, clustered, "blocking"),
+                (0, False, "split-phase, identity placement"), (2, clustered, "host-scheduled")]
+        for mode, use_cl, label in plan:
+            if use_cl is False and not clustered and label.endswith("identity placement"):
+                continue
+            if not fits(f"{w3.name} {label}", 6 + 3.0 * args.paged_repeats):
+                continue
+            cl = placement(n3) if use_cl else None
+            leg, pi, pd, pq = paged_leg(torch, g, a, w3, n3, qps, mode, vfirst, args.paged_repeats, cl,
+                                        label=label)
+            check(leg, pi, pd, pq, w3)
+            legs.append(leg)
+        by_label = {l["label"]: l for l in legs}
+        if by_label:
+            miss_gbs = legs[0]["miss_service_gbs"]
+        paged = {"host_link_peak_gbs": round(link, 1), "legs": legs}
+        if "split-phase" in by_label and "blocking" in by_label:
+            paged["split_phase_vs_blocking"] = round(by_label["split-phase"]["qps"] / by_label["blocking"]["qps"], 3)
+        if "split-phase" in by_label and "split-phase, identity placement" in by_label:
+            paged["clusters_vs_identity"] = round(
+                by_label["split-phase"]["qps"] / by_label["split-phase, identity placement"]["qps"], 3)
+        if "split-phase" in by_label and "host-scheduled" in by_label:
+            paged["gpu_vs_host_scheduled"] = round(
+                by_label["split-phase"]["qps"] / by_label["host-scheduled"]["qps"], 3)
+
+        # equal-wave comparison: both modes get the split-phase default's query
+        # waves; split-phase then holds oversub times more queries in flight
+        if args.ablation_sample > 0:
+            lats = [float(x) for x in args.ablation_latencies.split(",") if x.strip()]
+            na = min(args.ablation_sample, w3.queries.nq)
+            slots = int(w3.cache_frac * int(np.ceil(w3.index.n / w3.index.records_per_page)))
+            waves = max(1, min(slots // (2 * 32), na) // w3.oversub)
+            rows = []
+            for lat in lats:
+                row = {"latency_us": lat, "query_waves": waves,
+                       "little_law_requests": round(link * 1e9 * lat * 1e-6 / 4096, 1)}
+                for mode in (0, 1):
+                    if not fits(f"equal-wave {MODES[mode]} at {lat} us", 4 + 2.5 * args.paged_repeats):
+                        continue
+                    cl = placement(na) if clustered else None
+                    leg, pi, pd, pq = paged_leg(torch, g, a, w3, na, qps, mode, vfirst, args.paged_repeats, cl,
+                                                warmup_nq=1000, query_waves=waves, latency_us=lat,
+                                                label=f"equal waves, {MODES[mode]}")
+                    check(leg, pi, pd, pq, w3)
+                    row[MODES[mode]] = {k: leg[k] for k in ("qps", "qps_runs", "kernel_ms", "hit_rate",
+                                                            "miss_service_gbs", "proxy_peak", "equals_resident")
+                                        if k in leg}
+                    row[MODES[mode]]["live_queries"] = waves * (w3.oversub if mode == 0 else 1)
+                if "split-phase" in row and "blocking" in row:
+                    row["split_phase_vs_blocking"] = round(row["split-phase"]["qps"] / row["blocking"]["qps"], 3)
+                rows.append(row)
+            paged["equal_wave_ablation"] = {
+                "queries": na, "runs_per_point": args.paged_repeats,
+                "blocking_outstanding_cap": waves * 32, "rows": rows}
+
+        # C4: 100k queries, 20 us
+        w4 = WORKLOADS["u8-1m-cache10-lat20"]
+        n4 = w4.queries.nq if args.paged_sample < 0 else min(args.paged_sample, w4.queries.nq)
+        if fits(w4.name, 8 + 15.0 * args.large_repeats * n4 / 100000):
+            cl = placement(n4) if clustered else None
+            leg, pi, pd, pq = paged_leg(torch, g, a, w4, n4, qps, 0, vfirst,
+                                        args.large_repeats if n4 > 20000 else args.paged_repeats, cl,
+                                        warmup_nq=10000)
+            check(leg, pi, pd, pq, w4)
+            if packed_main is not None:   # these queries differ from the resident batch: the oracle checks a slice
+                ns = min(args.f32_cpu_sample, len(pq))
+                oi, od4, _, _ = packed_main.search(pq[:ns], w4.k, w4.L, w4.W, info["entry"],
+                                                   threads=oracle_threads()[0])
+                leg["oracle_exact"] = bool(np.array_equal(pi[:ns], oi) and np.array_equal(pd[:ns], od4))
+                leg["oracle_checked_queries"] = ns
+            # what the host link allows at this hit rate, and what 2x of resident would need
+            bpq = leg["pages_served"] * 4096 / max(1, leg["queries"])
+            acc_pq = None
+            leg["link_bound_qps"] = round(link * 1e9 / bpq, 1)
+            if ocounts is not None and ocounts["queries"] > 0:
+                acc_pq = (ocounts["expansions"] + ocounts["evaluations"]) / ocounts["queries"]
+            if acc_pq:
+                target = qps / 2
+                allowed_misses = link * 1e9 / target / 4096
+                leg["target_qps_2x_of_resident"] = round(target, 1)
+                leg["record_accesses_per_query"] = round(acc_pq, 1)
+                leg["hit_rate_needed_for_target"] = round(max(0.0, 1 - allowed_misses / acc_pq), 5)
+            legs.append(leg)
+
+    # --------------------------------------------------- 10M float32 index
+    if args.f32_sample != 0:
+        wr, wp = WORKLOADS["f32-10m-hbm"], WORKLOADS["f32-10m-cache5-lat20"]
+        est_gen = 5 if index_cached(wr.index) else 90
+        if fits(wr.name, est_gen + 40):
+            log(f"{wr.name}: loading or generating the index")
+            af = index_arrays(wr.index)
+            qf = query_array(wr.index, wr.queries)
+            if args.f32_sample > 0:
+                qf = qf[:args.f32_sample]
+            r = resident_leg(torch, g, af, qf, wr, "vectors-first", max(3, args.steps // 4), 1)
+            rqps = len(qf) * max(3, args.steps // 4) / r["elapsed"]
+            ftraffic = measured_traffic(wr.name, "vectors-first")
+            fleg = {"workload": wr.name, "queries": len(qf),
+                    "value": round(rqps, 1), "unit": "queries/s",
+                    "ms_per_step": round(r["elapsed"] * 1e3 / max(3, args.steps // 4), 3),
+                    "steps": max(3, args.steps // 4),
+                    "roofline": roofline_of(r, wr, wr.index.R, None, ftraffic, "search_resident<MetricF32>"),
+                    "counters": {k: r["stats"][k] for k in ("evaluations", "reevaluations", "expansions",
+                                                            "iterations")}}
+            if ftraffic:
+                fleg["achieved_hbm_gbs"] = fleg["roofline"]["traffic_gbs"]
+            packed = None
+            if args.f32_cpu_sample > 0 and fits(f"{wr.name} oracle", 60):
+                from oracle import load
+                t0 = time.perf_counter()
+                packed = load().pack(af["x"], af["graph"])
+                log(f"{wr.name}: oracle pages packed in {time.perf_counter() - t0:.1f} s")
+                ns = min(args.f32_cpu_sample, len(qf))
+                cb, ex, entry, oc, (oids_f, od_f), _ = cpu_baseline(af, qf, wr, r["ids"], r["dists"], ns,
+                                                                    ns // 10, packed=packed)
+                fleg["cpu_baseline"] = cb
+                fleg["oracle_exact"] = ex
+                fleg["oracle_checked_queries"] = ns
+                log(f"{wr.name}: {rqps:,.0f} q/s resident; oracle-exact on {ns}: {ex}")
+            resident_legs.append(fleg)
+            if not args.no_f32_paged and fits(wp.name, 30 + 52.0 * (args.large_repeats + 0.1) * len(qf) / 100000):
+                t0 = time.perf_counter()
+                fcl = g.cluster_order(af["x"], args.f32_clusters) if args.f32_clusters else None
+                log(f"{wp.name}: cluster placement ({args.f32_clusters}) in {time.perf_counter() - t0:.2f} s")
+                leg, pi, pd, _ = paged_leg(torch, g, af, wp, len(qf), rqps, 0, True,
+                                           args.large_repeats if len(qf) > 20000 else args.paged_repeats,
+                                           fcl, warmup_nq=10000)
+                leg["equals_resident"] = bool(np.array_equal(pi, r["ids"]) and
+                                              np.array_equal(pd.view(np.uint32), r["dists"].view(np.uint32)))
+                if packed is not None:
+                    ns = fleg["oracle_checked_queries"]
+                    leg["oracle_exact"] = bool(np.array_equal(pi[:ns], oids_f) and
+                                               np.array_equal(pd[:ns].view(np.uint32), od_f.view(np.uint32)))
+                    leg["oracle_checked_queries"] = ns
+                log(f"paged {wp.name}: {leg['qps']:,.0f} q/s, hit rate {leg['hit_rate']:.3f}, "
+                    f"miss service {leg['miss_service_gbs']} GB/s (resident {rqps:,.0f} q/s)")
+                if paged is None:
+                    paged = {"host_link_peak_gbs": round(host_link_peak_gbs(torch), 1), "legs": []}
+                paged["legs"].append(leg)
+            del packed, af
 
     out = {
         "metric": METRIC, "value": round(qps, 1), "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.index.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.index.n, "D": w.index.D, "R": R, "nq": nq,
                    "k": w.k, "L": w.L, "W": w.W, "record_bytes": info["record_bytes"],
@@ -439,12 +628,17 @@ def main():
         "other_layout": other,
         "oracle_exact": exact,
         "recall": recall,
-        "achieved_hbm_gbs": roofline["achieved"],
+        "achieved_hbm_gbs": roofline.get("traffic_gbs"),
+        "achieved_hbm_frac": roofline.get("traffic_frac"),
+        "algorithmic_gbs": roofline["achieved"],
         "miss_service_gbs": miss_gbs,
         "counters": {k: st[k] for k in ("evaluations", "reevaluations", "expansions", "iterations")},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "resident_legs": resident_legs,
         "paged": paged,
+        "skipped": skipped,
+        "bench_s": round(time.perf_counter() - T_START, 1),
     }
     print(json.dumps(out), flush=True)
 

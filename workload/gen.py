@@ -108,6 +108,8 @@ WORKLOADS = {
                  cache_frac=0.10, latency_us=20.0, oversub=4,
                  description="1M uint8 index, 100k queries, 10% page cache, 20 us per "
                              "page request, 4x oversubscribed query slots"),
+        Workload("f32-10m-hbm", _F32_10M, QuerySpec(100_000, 2005), k=10, L=128, W=8,
+                 description="10M x 96-d float32, R=64, 100k queries, L=128 W=8, HBM-resident"),
         Workload("f32-10m-cache5-lat20", _F32_10M, QuerySpec(100_000, 2005), k=10, L=128, W=8,
                  cache_frac=0.05, latency_us=20.0, oversub=4,
                  description="10M x 96-d float32, R=64, 100k queries, L=128 W=8, 5% page "
