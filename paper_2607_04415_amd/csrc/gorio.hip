@@ -463,6 +463,9 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   auto last_sweep = t0;
   const auto stale = std::chrono::milliseconds(4);
   uint64_t admitted = 0, finished = 0;
+  // scheduler counters (printed to stderr with GORIO_ROUNDS_STATS=1)
+  uint64_t n_rounds = 0, n_lane_runs = 0, n_idle = 0, n_stale = 0;
+  double round_us = 0.0;
   gorio_status st = GORIO_OK;
   while (finished < nq) {
     const auto now = Clock::now();
@@ -474,7 +477,10 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     if (now - last_sweep > std::chrono::milliseconds(1)) {  // lanes no fill has woken
       last_sweep = now;
       for (uint32_t l = 0; l < lanes; ++l)
-        if (lstate[l] == kWaiting && now - since[l] > stale) wake(l, epoch[l]);
+        if (lstate[l] == kWaiting && now - since[l] > stale) {
+          wake(l, epoch[l]);
+          ++n_stale;
+        }
     }
     uint32_t nlist = 0;
     for (uint32_t lane : runq) {
@@ -515,9 +521,13 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
       break;
     }
     const auto done_at = Clock::now();
+    ++n_rounds;
+    n_lane_runs += nlist;
+    round_us += std::chrono::duration<double, std::micro>(done_at - now).count();
     for (uint32_t i = 0; i < nlist; ++i) {
       const uint32_t lane = h_lanes[i];
       const LaneOut &o = P.h_lane_out[lane];
+      if (o.code == kLaneIdle) ++n_idle;
       if (o.code == kLaneDone) {
         ++finished;
         lstate[lane] = kFree;
@@ -525,6 +535,11 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
         continue;
       }
       const uint32_t ep = ++epoch[lane];
+      if (o.code == kLaneYield) {  // its turn ended while it could still proceed: next round
+        lstate[lane] = kRunnable;
+        runq.push_back(lane);
+        continue;
+      }
       lstate[lane] = kWaiting;
       since[lane] = done_at;
       const uint32_t nw = std::min(o.nwait, kLaneWaitCap);
@@ -534,6 +549,13 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     }
     poll_fills();
   }
+  if (env_int("GORIO_ROUNDS_STATS", 0))
+    fprintf(stderr, "[gorio rounds] lanes %u, rounds %llu, lane runs %llu (%.1f per round, %llu not runnable), "
+            "stale wakes %llu, %.1f us per round (launch to done), %.3f s in all\n", lanes,
+            (unsigned long long)n_rounds, (unsigned long long)n_lane_runs,
+            n_rounds ? (double)n_lane_runs / n_rounds : 0.0, (unsigned long long)n_idle,
+            (unsigned long long)n_stale, n_rounds ? round_us / n_rounds : 0.0,
+            std::chrono::duration<double>(Clock::now() - t0).count());
   // the fill waves leave once every query is done (or on abort)
   HIP_OR_FAIL(hipEventRecord(P.ev_fill, P.fill_stream));
   for (;;) {
@@ -655,6 +677,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.oversub = oversub;
   pp.max_pending = max_pending;
   pp.blocking = blocking ? 1 : 0;
+  pp.turn_passes = host_rounds ? (uint32_t)std::max(0, env_int("GORIO_TURN_PASSES", 1)) : 0u;
   pp.stats = rp.stats;
 
   // test hooks: random extra delay per request (completions leave out of

@@ -9,7 +9,8 @@
 //   MetricU8  - exact int32 distance: q.q + sum (x.x - 2 q.x) with
 //               v_dot4_u32_u8 on coalesced reads, 8 lanes per vector.
 //   MetricF32 - one lane per candidate (resident 96-d rows are gathered 8
-//               lanes per vector and transposed in registers);
+//               lanes per vector by whole lines and handed to their lanes
+//               through LDS);
 //               t = q_d - x_d, acc = acc + t*t for d = 0 .. D-1 in order,
 //               every operation rounded to nearest even with no fused
 //               multiply-add, so the result is the same float as a plain
@@ -256,8 +257,8 @@ struct MetricF32 {
   static constexpr int kChunks = 1;
   static constexpr int kQueryWords = 4 * NV4;
   static constexpr uint32_t kPadDist = 0x7F800000u;  // +inf
-  // resident kernel: 96-d rows (gathered by lines and transposed) hold a
-  // whole vector per lane plus the transpose's temporaries, which fits one
+  // resident kernel: 96-d rows (gathered by lines, blocks staged through a
+  // 4 KB LDS buffer) keep two batches of lines in registers, which fits one
   // wave per SIMD and leaves LDS for a 32 KB visited table; other widths run
   // two waves per SIMD with a 16 KB table
   static constexpr bool kGathered = EXACT && NV4 % 8 == 0;
@@ -363,37 +364,17 @@ struct MetricF32 {
   // lane i.  One lane reading a whole vector would make every 16-byte load
   // instruction touch 64 different cache lines; instead the 8 lanes of a
   // group read 8 vectors, one at a time, each lane 16 bytes of every 128
-  // (so each load instruction covers whole lines), and an 8 x 8 transpose of
-  // the 16-byte blocks inside the group (three butterfly exchanges over
-  // lane distances 1, 2, 4) then leaves each lane holding one 128-byte line
-  // of one vector for the sequential sum.  Lane g * 8 + s ends with the
-  // vector of lane s * 8 + g (transposed_candidate).
-  __device__ __forceinline__ static uint32_t transposed_candidate() {
-    const uint32_t l = lane_id();
-    return ((l & 7u) << 3) | (l >> 3);
-  }
+  // (so each load instruction covers whole lines).  The 16-byte blocks then
+  // pass through LDS, half a batch at a time (32 vectors x 128 bytes = 4 KB),
+  // so that each lane gets one 128-byte line of its own candidate's vector
+  // for the sequential sum: no VALU work moves the blocks, and the LDS
+  // traffic runs beside the arithmetic.  Lane i ends with candidate i.
+  __device__ __forceinline__ static uint32_t transposed_candidate() { return lane_id(); }
 
-  // One butterfly stage of the 8 x 8 block transpose inside each group of 8
-  // lanes (x[r][c]: component c of block r).  Lanes with bit M of their
-  // group position set give away block r and receive into it; the others
-  // do so with block r + M (value selects only, so that the blocks stay in
-  // registers).  After the stages for M = 1, 2, 4, block r of lane t holds
-  // what block t of lane r held.
-  template <int M>
-  __device__ __forceinline__ static void transpose_stage(uint32_t (&x)[8][4], uint32_t gl) {
-    const bool hi = (gl & M) != 0;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int r = ((p & ~(M - 1)) << 1) | (p & (M - 1));  // the blocks with bit M clear
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const uint32_t a = x[r][c], b = x[r + M][c];
-        const uint32_t got = xor_lanes<M>(hi ? a : b);
-        x[r][c] = hi ? got : a;
-        x[r + M][c] = hi ? b : got;
-      }
-    }
-  }
+  // Block k of LDS row t sits at 16-byte position k ^ ((t >> 1) & 7): the
+  // writes of one round cover 1 KB contiguously and the reads (lane t, row
+  // t) spread any 16 consecutive lanes over all 64 banks.
+  __device__ __forceinline__ static uint32_t tpos(uint32_t row, uint32_t k) { return row * 8u + (k ^ ((row >> 1) & 7u)); }
 
   // Line j of the vectors of the group's 8 candidates: x[r][c] = float
   // 32 j + 4 gl + c of the vector of lane r * 8 + g.
@@ -412,20 +393,33 @@ struct MetricF32 {
     }
   }
 
-  // acc over line j of this lane's vector: after the transpose x[s][c] is
-  // float 32 j + 4 s + c, so s then c visits d in increasing order.
+  // acc over line j of this lane's vector.  x[r] holds block gl of line j of
+  // the vector of lane r * 8 + g; through LDS, lane i receives y[k] = block k
+  // of its own vector's line (floats 32 j + 4 k .. + 3), so k then the
+  // component visits d in increasing order.
   __device__ __forceinline__ float sum_line(float acc, uint32_t (&x)[8][4], int j) const {
-    const uint32_t gl = lane_id() & 7u;
-    transpose_stage<1>(x, gl);
-    transpose_stage<2>(x, gl);
-    transpose_stage<4>(x, gl);
+    __shared__ __align__(16) uint4 stage[32 * 8];
+    const uint32_t l = lane_id(), g = l >> 3, gl = l & 7u, t = l & 31u;
+    uint4 y[8];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const float4 qv = *reinterpret_cast<const float4 *>(qs + 32 * j + 4 * s);
-      acc = step(acc, qv.x, __uint_as_float(x[s][0]));
-      acc = step(acc, qv.y, __uint_as_float(x[s][1]));
-      acc = step(acc, qv.z, __uint_as_float(x[s][2]));
-      acc = step(acc, qv.w, __uint_as_float(x[s][3]));
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const uint32_t row = (uint32_t)rr * 8u + g;
+        stage[tpos(row, gl)] = make_uint4(x[4 * h + rr][0], x[4 * h + rr][1], x[4 * h + rr][2], x[4 * h + rr][3]);
+      }
+      if ((l >> 5) == (uint32_t)h) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) y[k] = stage[tpos(t, (uint32_t)k)];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float4 qv = *reinterpret_cast<const float4 *>(qs + 32 * j + 4 * k);
+      acc = step(acc, qv.x, __uint_as_float(y[k].x));
+      acc = step(acc, qv.y, __uint_as_float(y[k].y));
+      acc = step(acc, qv.z, __uint_as_float(y[k].z));
+      acc = step(acc, qv.w, __uint_as_float(y[k].w));
     }
     return acc;
   }

@@ -65,6 +65,8 @@ struct PagedParams {
   uint32_t *out_dists;                    // distance bits (int32 or float32)
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
   uint32_t oversub, max_pending;
+  uint32_t turn_passes;                   // host rounds: a query yields after this many passes over its
+                                          // candidates that found pages ready (0 = no limit)
   int blocking;
   unsigned long long *stats;              // [eval, reeval, exp, iter, hit, miss, served, park, resume, bad]
 };
@@ -76,7 +78,7 @@ struct QSlot {
   uint32_t bstate[kPagedMaxW];
   uint32_t cand[kCandCap];
   uint32_t cstate[kCandCap];
-  uint32_t qi, active, phase, nbeam, b0, ncand, ht_used, forgot, parked;
+  uint32_t qi, active, phase, nbeam, b0, ncand, ht_used, forgot, parked, yielded;
 };
 
 struct PagedCounters {
@@ -312,9 +314,11 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
 
   M m;
   m.load_query(p.queries, S.qi, p.D, qbuf);
+  if (l == 0) S.yielded = 0;
   __syncthreads();
   uint64_t F[KPL];
   load_frontier(S, F);
+  uint32_t passes = 0;
 
   for (uint32_t guard = 0; guard < 4u * p.n + 16u; ++guard) {
     if (S.phase == kPhSelect) {
@@ -490,8 +494,10 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
       bool left = false;
       for (uint32_t c = l; c < S.ncand; c += kWave) left |= S.cstate[c] != kDone;
       if (ballot(left) != 0) {
-        if (any_ready) continue;  // progress: pins were released, more requests may go out
-        break;                    // park until a page arrives
+        // progress: pins were released, more requests may go out
+        if (any_ready && (p.turn_passes == 0 || ++passes < p.turn_passes)) continue;
+        if (any_ready && l == 0) S.yielded = 1;  // turn over, though it could go on
+        break;                                   // park until a page arrives
       }
       // iteration group done
       S.b0 += min(S.nbeam - S.b0, GB);
@@ -636,11 +642,12 @@ __global__ __launch_bounds__(kWave) void search_paged(PagedParams p) {
 // the completion state the host schedules from.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kLaneWaitCap = 60;
-enum : uint32_t { kLaneIdle = 0, kLaneParked = 1, kLaneDone = 2 };
+enum : uint32_t { kLaneIdle = 0, kLaneParked = 1, kLaneDone = 2, kLaneYield = 3 };
 
 // What a lane reported at the end of its turn (host memory, one per lane).
 struct LaneOut {
-  uint32_t code;                 // kLaneIdle (not runnable, not run), kLaneParked, kLaneDone
+  uint32_t code;                 // kLaneIdle (not runnable, not run), kLaneParked, kLaneDone, kLaneYield
+                                 // (its turn ended while it could still proceed)
   uint32_t nwait;                // entries of wait[]
   uint32_t retry;                // 1: can proceed without one of wait[] arriving (requests it could
                                  // not issue for want of a free slot, or more waits than wait[] holds)
@@ -730,8 +737,9 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
     }
   } else {
     ++ctr.park;
+    __syncthreads();
     for (uint32_t i = l; i < r.state_words; i += kWave) st[i] = sw[i];
-    report_waits(p, S, o, kLaneParked);
+    report_waits(p, S, o, S.yielded ? kLaneYield : kLaneParked);
   }
   if (l == 0) {
     if (ctr.eval) atomicAdd(&p.stats[0], ctr.eval);

@@ -68,11 +68,14 @@ def assert_same(gi, gd, oids, od):
 # --------------------------------------------------------------------------- #
 # host-scheduled rounds
 # --------------------------------------------------------------------------- #
-@pytest.mark.parametrize("frac,latency,vfirst,lanes", [
-    (0.10, 0.0, False, 0), (0.10, 20.0, True, 0), (0.30, 5.0, False, 7), (0.05, 0.0, True, 1),
-], ids=["c10-l0", "c10-l20-vfirst", "c30-l5-7lanes", "c5-l0-1lane"])
-def test_host_rounds_match_oracle(torch_dev, small, frac, latency, vfirst, lanes):
+@pytest.mark.parametrize("frac,latency,vfirst,lanes,passes", [
+    (0.10, 0.0, False, 0, None), (0.10, 20.0, True, 0, None), (0.30, 5.0, False, 7, "3"), (0.05, 0.0, True, 1, None),
+    (0.10, 0.0, True, 0, "0"),
+], ids=["c10-l0", "c10-l20-vfirst", "c30-l5-7lanes-3passes", "c5-l0-1lane", "c10-l0-unbounded-turns"])
+def test_host_rounds_match_oracle(torch_dev, small, monkeypatch, frac, latency, vfirst, lanes, passes):
     a, q, oids, od, oc = small
+    if passes is not None:
+        monkeypatch.setenv("GORIO_TURN_PASSES", passes)
     ix = g.Index(a["x"], a["graph"], vectors_first=vfirst)
     ix.set_cache(max(int(frac * ix.info["index_bytes"]), 128 * 4096))
     ix.set_backing(latency_us=latency, mode=HOST)
