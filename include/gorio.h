@@ -164,8 +164,8 @@ gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes);
  *                        (the blocking demand-paging path the paper compares
  *                        against, Sec. 5.1, Table 2);
  *                    2 = host-scheduled rounds: a host thread (the caller's)
- *                        keeps the query lanes and launches one round kernel at a
- *                        time over the lanes whose pages have been filled, using
+ *                        keeps the query lanes and launches round kernels (up to
+ *                        two in flight) over the lanes whose pages have been filled, using
  *                        the same page cache, descriptors and proxy (the
  *                        GustANN-style scheduler over GORIO's backend that the
  *                        paper compares against, Sec. 5.1, Table 2).  oversub is

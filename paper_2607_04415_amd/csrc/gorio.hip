@@ -360,17 +360,22 @@ namespace {
 // Host-scheduled rounds (the GustANN-style comparison point of Sec. 5.1, over
 // the same page cache, miss descriptors and proxy): the calling thread owns
 // the query schedule.  It keeps `lanes` query lanes, starts queries in free
-// lanes in admission order, and launches one round kernel at a time over the
-// lanes it deems runnable.  A lane is runnable when one of the cache slots it
-// reported waiting for has been filled -- the fill waves publish, per
-// completion ring, how many completions they have copied, and the host reads
-// the filled {page, slot} entries back from the ring -- or, for a lane that
-// could not issue all of its requests, when any page has been filled.  A lane
-// not woken within a few milliseconds is run anyway, so a missed wake costs
-// time, never progress.
+// lanes in admission order, and launches round kernels over the lanes it
+// deems runnable, up to two rounds in flight on two streams (while one round
+// runs, the host reads the other's reports and gathers the next lanes).  A
+// lane is runnable when one of the cache slots it reported waiting for has
+// been filled -- the fill waves publish, per completion ring, how many
+// completions they have copied, and the host reads the filled {page, slot}
+// entries back from the ring -- or, for a lane that could not issue all of
+// its requests, when any page has been filled, or at once when its turn ended
+// while it could still proceed.  A slot filled while the lane's round ran is
+// caught by comparing when the host saw that fill with when the round was
+// launched.  A lane not woken within a few milliseconds is run anyway, so a
+// missed wake costs time, never progress.
 gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, const std::vector<uint32_t> &order,
                              hipStream_t s, double limit_s, bool &timed_out) {
   using Clock = std::chrono::steady_clock;
+  constexpr int kFlights = 2;  // round kernels in flight at once
   PagedState &P = *ix->paged;
   const uint32_t words = lane_state_words(pp.L);
   if ((uint64_t)lanes * words > P.lane_state_words) {
@@ -386,30 +391,39 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     P.h_round = P.d_round = nullptr;
     P.h_lane_out = P.d_lane_out = nullptr;
     P.round_cap = 0;
-    HIP_OR_FAIL(host_ring(&P.h_round, &P.d_round, 2 * (size_t)lanes));
+    HIP_OR_FAIL(host_ring(&P.h_round, &P.d_round, 2 * kFlights * (size_t)lanes));
     HIP_OR_FAIL(host_ring(&P.h_lane_out, &P.d_lane_out, lanes));
     P.round_cap = lanes;
   }
   if (!P.h_fill_head)
     HIP_OR_FAIL(host_ring(&P.h_fill_head, &P.d_fill_head, (size_t)PagedState::kMaxRings * PagedState::kTailStride));
   if (!P.fill_stream) HIP_OR_FAIL(hipStreamCreateWithFlags(&P.fill_stream, hipStreamNonBlocking));
-  if (!P.ev_round) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_round, hipEventDisableTiming));
+  if (!P.round_stream) HIP_OR_FAIL(hipStreamCreateWithFlags(&P.round_stream, hipStreamNonBlocking));
+  for (int i = 0; i < kFlights; ++i)
+    if (!P.ev_round[i]) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_round[i], hipEventDisableTiming));
   if (!P.ev_fill) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_fill, hipEventDisableTiming));
   const uint32_t rings = std::max(1u, pp.fill_waves);
   for (uint32_t r = 0; r < rings; ++r)
     __atomic_store_n(P.h_fill_head + (size_t)r * PagedState::kTailStride, 0ull, __ATOMIC_RELEASE);
   pp.fill_head = P.d_fill_head;
-  RoundParams rp;
-  rp.lanes = P.d_round;
-  rp.admit = P.d_round + lanes;
-  rp.state = P.d_lane_state;
-  rp.state_words = words;
-  rp.out = P.d_lane_out;
-  uint32_t *h_lanes = P.h_round, *h_admit = P.h_round + lanes;
+  const hipStream_t rstream[kFlights] = {s, P.round_stream};
+  RoundParams rp[kFlights];
+  uint32_t *h_lanes[kFlights], *h_admit[kFlights];
+  for (int i = 0; i < kFlights; ++i) {
+    rp[i].lanes = P.d_round + (size_t)2 * i * lanes;
+    rp[i].admit = P.d_round + (size_t)(2 * i + 1) * lanes;
+    rp[i].state = P.d_lane_state;
+    rp[i].state_words = words;
+    rp[i].out = P.d_lane_out;
+    h_lanes[i] = P.h_round + (size_t)2 * i * lanes;
+    h_admit[i] = P.h_round + (size_t)(2 * i + 1) * lanes;
+  }
 
-  // fill waves in a kernel of their own, after the control words were reset on s
+  // fill waves in a kernel of their own, and the second round stream, both
+  // after the control words were reset on s
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
   HIP_OR_FAIL(hipStreamWaitEvent(P.fill_stream, ix->ev_start, 0));
+  HIP_OR_FAIL(hipStreamWaitEvent(P.round_stream, ix->ev_start, 0));
   {
     const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, (int)pp.fill_waves, P.fill_stream)
                                                  : launch_paged_u8(pp, (int)pp.fill_waves, P.fill_stream);
@@ -429,6 +443,10 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   std::vector<std::vector<Waiter>> waiters(P.slots);
   std::vector<Waiter> any_fill;
   std::vector<uint64_t> ring_head(rings, 0);
+  // fill_seq counts the polls that found filled pages; slot_seq[s] is its
+  // value when a fill of slot s was last seen
+  uint64_t fill_seq = 0;
+  std::vector<uint64_t> slot_seq(P.slots, 0);
   const uint64_t cq_cap = P.cq_cap;
   auto wake = [&](uint32_t lane, uint32_t ep) {
     if (lstate[lane] == kWaiting && epoch[lane] == ep) {
@@ -442,15 +460,17 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
       const uint64_t fh = __atomic_load_n(P.h_fill_head + (size_t)r * PagedState::kTailStride, __ATOMIC_ACQUIRE);
       uint64_t &h = ring_head[r];
       if (fh <= h) continue;
+      if (!progress) ++fill_seq;
+      progress = true;
       if (fh - h > cq_cap) h = fh - cq_cap;  // entries already reused by the proxy: the fallback wakes them
       const unsigned long long *ring = P.h_cq + (size_t)r * cq_cap;
       for (; h < fh; ++h) {
         const uint32_t slot = (uint32_t)__atomic_load_n(&ring[h & (cq_cap - 1)], __ATOMIC_RELAXED);
         if (slot >= P.slots) continue;
+        slot_seq[slot] = fill_seq;
         for (const Waiter &w : waiters[slot]) wake(w.first, w.second);
         waiters[slot].clear();
       }
-      progress = true;
     }
     if (progress && !any_fill.empty()) {
       for (const Waiter &w : any_fill) wake(w.first, w.second);
@@ -458,15 +478,62 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     }
     return progress;
   };
+  struct Flight {
+    bool busy = false;
+    uint32_t n = 0;
+    uint64_t seq = 0;  // fill_seq at launch
+    Clock::time_point t0;
+  } fl[kFlights];
 
   const auto t0 = Clock::now();
   auto last_sweep = t0;
   const auto stale = std::chrono::milliseconds(4);
   uint64_t admitted = 0, finished = 0;
   // scheduler counters (printed to stderr with GORIO_ROUNDS_STATS=1)
-  uint64_t n_rounds = 0, n_lane_runs = 0, n_idle = 0, n_stale = 0;
+  uint64_t n_rounds = 0, n_lane_runs = 0, n_idle = 0, n_stale = 0, n_early = 0;
   double round_us = 0.0;
+  const uint32_t min_round = std::max(1u, lanes / 8);
   gorio_status st = GORIO_OK;
+  auto retire = [&](int i) {
+    const auto done_at = Clock::now();
+    ++n_rounds;
+    n_lane_runs += fl[i].n;
+    round_us += std::chrono::duration<double, std::micro>(done_at - fl[i].t0).count();
+    for (uint32_t k = 0; k < fl[i].n; ++k) {
+      const uint32_t lane = h_lanes[i][k];
+      const LaneOut &o = P.h_lane_out[lane];
+      if (o.code == kLaneIdle) ++n_idle;
+      if (o.code == kLaneDone) {
+        ++finished;
+        lstate[lane] = kFree;
+        freeq.push_back(lane);
+        continue;
+      }
+      const uint32_t ep = ++epoch[lane];
+      bool now = o.code == kLaneYield;  // its turn ended while it could still proceed
+      const uint32_t nw = std::min(o.nwait, kLaneWaitCap);
+      for (uint32_t j = 0; j < nw && !now; ++j) {
+        const uint32_t w = o.wait[j];
+        if (w >= P.slots) continue;
+        if (slot_seq[w] > fl[i].seq) now = true;  // filled while the round ran
+        else waiters[w].push_back({lane, ep});
+      }
+      if (!now && (o.retry || nw == 0)) {
+        if (fill_seq > fl[i].seq) now = true;
+        else any_fill.push_back({lane, ep});
+      }
+      if (now) {
+        if (o.code != kLaneYield) ++n_early;
+        lstate[lane] = kRunnable;
+        runq.push_back(lane);
+      } else {
+        lstate[lane] = kWaiting;
+        since[lane] = done_at;
+      }
+    }
+    fl[i].busy = false;
+  };
+
   while (finished < nq) {
     const auto now = Clock::now();
     if (std::chrono::duration<double>(now - t0).count() > limit_s) {
@@ -482,79 +549,77 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
           ++n_stale;
         }
     }
-    uint32_t nlist = 0;
-    for (uint32_t lane : runq) {
-      h_lanes[nlist] = lane;
-      h_admit[nlist] = kNone;
-      lstate[lane] = kRunning;
-      ++nlist;
-    }
-    runq.clear();
-    while (!freeq.empty() && admitted < nq) {
-      const uint32_t lane = freeq.back();
-      freeq.pop_back();
-      h_lanes[nlist] = lane;
-      h_admit[nlist] = order.empty() ? (uint32_t)admitted : order[admitted];
-      lstate[lane] = kRunning;
-      ++admitted;
-      ++nlist;
-    }
-    if (nlist == 0) {
-      if (!poll_fills()) {
-        for (int i = 0; i < 32; ++i) GORIO_CPU_PAUSE();
+    bool acted = false;
+    for (int i = 0; i < kFlights; ++i) {
+      if (!fl[i].busy) continue;
+      const hipError_t q = hipEventQuery(P.ev_round[i]);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) {
+        st = fail(GORIO_EDEVICE, "round failed: %s", hipGetErrorString(q));
+        break;
       }
-      continue;
+      retire(i);
+      acted = true;
     }
-    const hipError_t le = ix->dtype == GORIO_F32 ? launch_rounds_f32(pp, rp, (int)nlist, s)
-                                                 : launch_rounds_u8(pp, rp, (int)nlist, s);
-    if (le != hipSuccess) {
-      st = fail(GORIO_EDEVICE, "round launch failed: %s", hipGetErrorString(le));
-      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
-      break;
-    }
-    HIP_OR_FAIL(hipEventRecord(P.ev_round, s));
-    hipError_t q;
-    while ((q = hipEventQuery(P.ev_round)) == hipErrorNotReady) GORIO_CPU_PAUSE();
-    if (q != hipSuccess) {
-      st = fail(GORIO_EDEVICE, "round failed: %s", hipGetErrorString(q));
-      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
-      break;
-    }
-    const auto done_at = Clock::now();
-    ++n_rounds;
-    n_lane_runs += nlist;
-    round_us += std::chrono::duration<double, std::micro>(done_at - now).count();
-    for (uint32_t i = 0; i < nlist; ++i) {
-      const uint32_t lane = h_lanes[i];
-      const LaneOut &o = P.h_lane_out[lane];
-      if (o.code == kLaneIdle) ++n_idle;
-      if (o.code == kLaneDone) {
-        ++finished;
-        lstate[lane] = kFree;
-        freeq.push_back(lane);
-        continue;
+    if (st != GORIO_OK) break;
+    acted |= poll_fills();
+    int busy = 0;
+    for (int i = 0; i < kFlights; ++i) busy += fl[i].busy ? 1 : 0;
+    for (int i = 0; i < kFlights; ++i) {
+      if (fl[i].busy) continue;
+      const uint64_t avail = runq.size() + std::min<uint64_t>(freeq.size(), nq - admitted);
+      // with another round running, wait for a worthwhile number of lanes
+      if (avail == 0 || (busy > 0 && avail < min_round)) break;
+      uint32_t n = 0;
+      for (uint32_t lane : runq) {
+        h_lanes[i][n] = lane;
+        h_admit[i][n] = kNone;
+        lstate[lane] = kRunning;
+        ++n;
       }
-      const uint32_t ep = ++epoch[lane];
-      if (o.code == kLaneYield) {  // its turn ended while it could still proceed: next round
-        lstate[lane] = kRunnable;
-        runq.push_back(lane);
-        continue;
+      runq.clear();
+      while (!freeq.empty() && admitted < nq) {
+        const uint32_t lane = freeq.back();
+        freeq.pop_back();
+        h_lanes[i][n] = lane;
+        h_admit[i][n] = order.empty() ? (uint32_t)admitted : order[admitted];
+        lstate[lane] = kRunning;
+        ++admitted;
+        ++n;
       }
-      lstate[lane] = kWaiting;
-      since[lane] = done_at;
-      const uint32_t nw = std::min(o.nwait, kLaneWaitCap);
-      for (uint32_t j = 0; j < nw; ++j)
-        if (o.wait[j] < P.slots) waiters[o.wait[j]].push_back({lane, ep});
-      if (o.retry || nw == 0) any_fill.push_back({lane, ep});
+      fl[i].t0 = Clock::now();
+      fl[i].seq = fill_seq;
+      const hipError_t le = ix->dtype == GORIO_F32 ? launch_rounds_f32(pp, rp[i], (int)n, rstream[i])
+                                                   : launch_rounds_u8(pp, rp[i], (int)n, rstream[i]);
+      if (le != hipSuccess) {
+        st = fail(GORIO_EDEVICE, "round launch failed: %s", hipGetErrorString(le));
+        break;
+      }
+      const hipError_t re = hipEventRecord(P.ev_round[i], rstream[i]);
+      if (re != hipSuccess) {
+        st = fail(GORIO_EDEVICE, "hipEventRecord: %s", hipGetErrorString(re));
+        break;
+      }
+      fl[i].busy = true;
+      fl[i].n = n;
+      ++busy;
+      acted = true;
     }
-    poll_fills();
+    if (st != GORIO_OK) break;
+    if (!acted)
+      for (int i = 0; i < 16; ++i) GORIO_CPU_PAUSE();
   }
+  if (st != GORIO_OK || timed_out) __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+  // rounds still in flight (after an error or the watchdog) finish: every lane
+  // turn is bounded and stops at once on the abort flag
+  for (int i = 0; i < kFlights; ++i)
+    if (fl[i].busy) (void)hipEventSynchronize(P.ev_round[i]);
   if (env_int("GORIO_ROUNDS_STATS", 0))
     fprintf(stderr, "[gorio rounds] lanes %u, rounds %llu, lane runs %llu (%.1f per round, %llu not runnable), "
-            "stale wakes %llu, %.1f us per round (launch to done), %.3f s in all\n", lanes,
-            (unsigned long long)n_rounds, (unsigned long long)n_lane_runs,
+            "woken at retirement %llu, stale wakes %llu, %.1f us per round (launch to retirement), %.3f s in all\n",
+            lanes, (unsigned long long)n_rounds, (unsigned long long)n_lane_runs,
             n_rounds ? (double)n_lane_runs / n_rounds : 0.0, (unsigned long long)n_idle,
-            (unsigned long long)n_stale, n_rounds ? round_us / n_rounds : 0.0,
+            (unsigned long long)n_early, (unsigned long long)n_stale, n_rounds ? round_us / n_rounds : 0.0,
             std::chrono::duration<double>(Clock::now() - t0).count());
   // the fill waves leave once every query is done (or on abort)
   HIP_OR_FAIL(hipEventRecord(P.ev_fill, P.fill_stream));
@@ -569,6 +634,8 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     std::this_thread::sleep_for(std::chrono::microseconds(50));
   }
   HIP_OR_FAIL(hipStreamWaitEvent(s, P.ev_fill, 0));
+  HIP_OR_FAIL(hipEventRecord(P.ev_round[1], P.round_stream));
+  HIP_OR_FAIL(hipStreamWaitEvent(s, P.ev_round[1], 0));
   HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
   return st;
 }
@@ -677,7 +744,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.oversub = oversub;
   pp.max_pending = max_pending;
   pp.blocking = blocking ? 1 : 0;
-  pp.turn_passes = host_rounds ? (uint32_t)std::max(0, env_int("GORIO_TURN_PASSES", 1)) : 0u;
+  pp.turn_passes = host_rounds ? (uint32_t)std::max(0, env_int("GORIO_TURN_PASSES", 2)) : 0u;
   pp.stats = rp.stats;
 
   // test hooks: random extra delay per request (completions leave out of
