@@ -42,6 +42,16 @@ KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp", "paper_2607_0
                   "paper_2607_04415_amd/csrc/metric.hpp", "paper_2607_04415_amd/csrc/launch.hpp",
                   "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
 MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
+# Scheduler shapes of the paged legs (oversub = query slots per wave, query_waves; 0 = the
+# library's default, which runs as many queries as the cache's pins allow).  When the host
+# link is the bound, fewer queries in flight keep the link full and share the cache better
+# (a sweep on the full query counts: 1M index, 10% cache, 0 us: 30 waves x 1 slot 6,544
+# queries/s, 40 waves 6,477, 156 queries in 39 waves x 4 slots 5,716; 10M float32, 5%
+# cache: 60 waves x 1 slot 3,015, 1,302 queries in 326 waves x 4 slots 2,131).  The 100k
+# query 20 us configuration asks for 4 query slots per wave; 30 waves gave 7,400 against
+# 7,414 for the default 39, so it keeps the default.
+SHAPE_C3 = {"oversub": 1, "query_waves": 30}
+SHAPE_C5 = {"oversub": 1, "query_waves": 60}
 T_START = time.perf_counter()
 
 
@@ -473,18 +483,21 @@ def main():
         clustered = args.paged_clusters != 0
         w3 = WORKLOADS["u8-1m-cache10-lat0"]
         n3 = w3.queries.nq if args.paged_sample < 0 else min(args.paged_sample, w3.queries.nq)
-        # C3 legs: split-phase, blocking (one query per wave: equal live queries),
-        # identity placement, host-scheduled rounds
-        plan = [(0, clustered, "split-phase"), (1, clustered, "blocking"),
-                (0, False, "split-phase, identity placement"), (2, clustered, "host-scheduled")]
-        for mode, use_cl, label in plan:
+        # C3 legs: split-phase and blocking in the same shape (one query per wave),
+        # the identity placement, the default shape (as many queries as the pins
+        # allow, 4 per wave), host-scheduled rounds (lanes: the default)
+        plan = [(0, clustered, "split-phase", SHAPE_C3), (1, clustered, "blocking", SHAPE_C3),
+                (0, False, "split-phase, identity placement", SHAPE_C3),
+                (0, clustered, "split-phase, default shape", {}),
+                (2, clustered, "host-scheduled", {})]
+        for mode, use_cl, label, shape in plan:
             if use_cl is False and not clustered and label.endswith("identity placement"):
                 continue
             if not fits(f"{w3.name} {label}", 6 + 3.0 * args.paged_repeats):
                 continue
             cl = placement(n3) if use_cl else None
             leg, pi, pd, pq = paged_leg(torch, g, a, w3, n3, qps, mode, vfirst, args.paged_repeats, cl,
-                                        label=label)
+                                        label=label, **shape)
             check(leg, pi, pd, pq, w3)
             legs.append(leg)
         by_label = {l["label"]: l for l in legs}
@@ -496,6 +509,9 @@ def main():
         if "split-phase" in by_label and "split-phase, identity placement" in by_label:
             paged["clusters_vs_identity"] = round(
                 by_label["split-phase"]["qps"] / by_label["split-phase, identity placement"]["qps"], 3)
+        if "split-phase" in by_label and "split-phase, default shape" in by_label:
+            paged["tuned_vs_default_shape"] = round(
+                by_label["split-phase"]["qps"] / by_label["split-phase, default shape"]["qps"], 3)
         if "split-phase" in by_label and "host-scheduled" in by_label:
             paged["gpu_vs_host_scheduled"] = round(
                 by_label["split-phase"]["qps"] / by_label["host-scheduled"]["qps"], 3)
@@ -601,7 +617,7 @@ def main():
                 log(f"{wp.name}: cluster placement ({args.f32_clusters}) in {time.perf_counter() - t0:.2f} s")
                 leg, pi, pd, _ = paged_leg(torch, g, af, wp, len(qf), rqps, 0, True,
                                            args.large_repeats if len(qf) > 20000 else args.paged_repeats,
-                                           fcl, warmup_nq=10000)
+                                           fcl, warmup_nq=10000, **SHAPE_C5)
                 leg["equals_resident"] = bool(np.array_equal(pi, r["ids"]) and
                                               np.array_equal(pd.view(np.uint32), r["dists"].view(np.uint32)))
                 if packed is not None:

@@ -31,12 +31,13 @@
  * degree][R x uint32 ids, padded with UINT32_MAX]).  A graph row's UINT32_MAX
  * entries mean "no edge"; the block keeps the row's other ids in order and
  * degree = their count.  Inside a page (bytes not covered below are zero):
- *   contiguous (default): record i at byte i * record_bytes, the adjacency
- *     block right after the vector;
- *   vectors first: vector i at byte i * V, where V = vector bytes rounded up
- *     to 16, then adjacency block i at byte records_per_page * V +
- *     i * (record_bytes - V).  For 128-byte vectors every vector starts on a
- *     128-byte line, so a distance evaluation reads one line instead of two.
+ *   vectors first (the default): vector i at byte i * V, where V = vector
+ *     bytes rounded up to 16, then adjacency block i at byte
+ *     records_per_page * V + i * (record_bytes - V).  For 128-byte vectors
+ *     every vector starts on a 128-byte line, so a distance evaluation reads
+ *     one line instead of two;
+ *   contiguous: record i at byte i * record_bytes, the adjacency block right
+ *     after the vector (DiskANN's record order).
  * Both layouts put the same nodes in the same pages; only the bytes inside a
  * page move.
  *
@@ -76,6 +77,13 @@ typedef enum {
 
 typedef enum { GORIO_U8 = 0, GORIO_F32 = 1 } gorio_dtype;
 
+/* Arrangement of the bytes inside a page (see the top of this file). */
+typedef enum {
+    GORIO_LAYOUT_DEFAULT = 0,        /* vectors first */
+    GORIO_LAYOUT_VECTORS_FIRST = 1,
+    GORIO_LAYOUT_CONTIGUOUS = 2
+} gorio_arrangement;
+
 /* Node-record placement in pages.  Zero fields take the default. */
 typedef struct {
     uint32_t page_bytes;          /* page size; default 4096; multiple of 16 */
@@ -83,7 +91,7 @@ typedef struct {
                                      (contiguous) or vec_bytes rounded up to 16 (vectors
                                      first); >= that default's minimum, multiple of 4 */
     uint32_t records_per_page;    /* default page_bytes / record_bytes */
-    uint32_t vectors_first;       /* 0: contiguous records (default); 1: vectors first */
+    uint32_t arrangement;         /* gorio_arrangement; 0 = default (vectors first) */
     const uint32_t *node_to_slot; /* host array of n entries, a permutation of [0, n); NULL = identity */
 } gorio_page_layout;
 
@@ -111,7 +119,7 @@ typedef struct {
     uint64_t n;
     uint32_t D, R;
     uint32_t page_bytes, record_bytes, records_per_page;
-    int vectors_first;         /* page layout (see above) */
+    int vectors_first;         /* 1: vectors-first pages, 0: contiguous records */
     uint64_t num_pages;
     uint64_t index_bytes;      /* num_pages * page_bytes */
     uint32_t entry;            /* entry node used by every search */

@@ -16,6 +16,7 @@ LIB_PATH = _PKG / "libgorio.so"
 
 OK, EINVAL, ENOMEM, EDEVICE, ETIMEOUT, EUNSUPPORTED = range(6)
 U8, F32 = 0, 1
+LAYOUT_DEFAULT, LAYOUT_VECTORS_FIRST, LAYOUT_CONTIGUOUS = 0, 1, 2
 NO_EDGE = 0xFFFFFFFF
 _STATUS = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "EDEVICE", 4: "ETIMEOUT", 5: "EUNSUPPORTED"}
 
@@ -28,7 +29,7 @@ class GorioError(RuntimeError):
 
 class PageLayout(ctypes.Structure):
     _fields_ = [("page_bytes", ctypes.c_uint32), ("record_bytes", ctypes.c_uint32),
-                ("records_per_page", ctypes.c_uint32), ("vectors_first", ctypes.c_uint32),
+                ("records_per_page", ctypes.c_uint32), ("arrangement", ctypes.c_uint32),
                 ("node_to_slot", ctypes.c_void_p)]
 
 
@@ -146,7 +147,9 @@ class Index:
     def __init__(self, vectors: np.ndarray, graph: np.ndarray, page_bytes: int = 0,
                  record_bytes: int = 0, records_per_page: int = 0,
                  node_to_slot: np.ndarray | None = None, entry: int | None = None,
-                 vectors_first: bool = False):
+                 vectors_first: bool | None = None):
+        """vectors_first: True = vectors-first pages, False = contiguous records,
+        None = the library's default (vectors first)."""
         vectors = np.ascontiguousarray(vectors)
         graph = np.ascontiguousarray(graph, dtype=np.uint32)
         if vectors.dtype == np.uint8:
@@ -159,8 +162,9 @@ class Index:
         if graph.shape[0] != n:
             raise ValueError("graph must have one row per vector")
         self._n2s = None if node_to_slot is None else np.ascontiguousarray(node_to_slot, np.uint32)
-        layout = PageLayout(page_bytes, record_bytes, records_per_page, int(bool(vectors_first)),
-                            _ptr(self._n2s))
+        arrangement = LAYOUT_DEFAULT if vectors_first is None else (
+            LAYOUT_VECTORS_FIRST if vectors_first else LAYOUT_CONTIGUOUS)
+        layout = PageLayout(page_bytes, record_bytes, records_per_page, arrangement, _ptr(self._n2s))
         h = ctypes.c_void_p()
         _check(lib().gorio_build_index(self.dtype, vectors.ctypes.data, n, D, graph.ctypes.data,
                                        graph.shape[1], ctypes.byref(layout),

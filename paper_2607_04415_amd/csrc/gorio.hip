@@ -115,8 +115,10 @@ extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors
   if (entry != UINT32_MAX && entry >= n) return fail(GORIO_EINVAL, "entry %u >= n", entry);
 
   const uint32_t vb = vec_bytes_of(dtype, D);
-  const bool vfirst = layout && layout->vectors_first;
-  if (layout && layout->vectors_first > 1) return fail(GORIO_EINVAL, "vectors_first must be 0 or 1");
+  const uint32_t arrangement = layout ? layout->arrangement : (uint32_t)GORIO_LAYOUT_DEFAULT;
+  if (arrangement > (uint32_t)GORIO_LAYOUT_CONTIGUOUS)
+    return fail(GORIO_EINVAL, "arrangement=%u is not a gorio_arrangement", arrangement);
+  const bool vfirst = arrangement != (uint32_t)GORIO_LAYOUT_CONTIGUOUS;
   // vectors first: each vector slot is rounded up to 16 bytes
   const uint32_t min_rec = (vfirst ? ((vb + 15u) & ~15u) : vb) + 4 + 4 * R;
   uint32_t page_bytes = layout && layout->page_bytes ? layout->page_bytes : 4096;

@@ -59,7 +59,7 @@ def _build(lib, dtype=0, n=10, D=8, R=4, layout=None, entry=g.NO_EDGE, vectors=T
     dict(layout=g.PageLayout(4096, 10, 0, 0, None)),       # record smaller than its contents
     dict(layout=g.PageLayout(4096, 26, 0, 0, None)),       # record not a multiple of 4
     dict(layout=g.PageLayout(4096, 0, 1000, 0, None)),     # too many records per page
-    dict(layout=g.PageLayout(4096, 0, 0, 2, None)),        # unknown layout
+    dict(layout=g.PageLayout(4096, 0, 0, 3, None)),        # unknown arrangement
     dict(D=4, R=4, layout=g.PageLayout(4096, 24, 0, 1, None)),  # vectors first: 16 + 4 + 16 > 24
 ])
 def test_build_rejects_bad_arguments(lib, kw):

@@ -130,11 +130,12 @@ def test_parity_random_graph_with_missing_edges(orc, torch_dev):
     dict(vectors_first=True), dict(vectors_first=True, node_to_slot="perm", record_bytes=420),
 ], ids=["perm", "rec400", "rpp3", "page8k", "page16-tiny", "vfirst", "vfirst-perm-rec420"])
 def test_parity_layouts(orc, torch_dev, layout):
+    layout = {"vectors_first": False, **layout}   # the oracle packs contiguous records unless told otherwise
     rng = np.random.default_rng(2)
     n, D, R = 2000, 128, 64
     if layout.get("page_bytes") == 16:
         D, R = 4, 2
-        layout = dict(page_bytes=16)
+        layout = dict(page_bytes=16, vectors_first=False)
     spec = IndexSpec(n=n, D=D, dtype="u8", clusters=4, sigma=20.0, r_near=R // 2, r_rand=R // 2, seed=5)
     a = index_arrays(spec, use_cache=False)
     if layout.get("node_to_slot") == "perm":
@@ -328,7 +329,7 @@ def test_entry_rule_matches_oracle_f32(orc, torch_dev):
     rng = np.random.default_rng(14)
     x = rng.standard_normal((3000, 96)).astype(np.float32)
     graph = random_graph(rng, 3000, 8)
-    ix = g.Index(x, graph)
+    ix = g.Index(x, graph, vectors_first=False)
     assert ix.info["entry"] == orc.medoid(x)
     assert np.array_equal(ix.pages(), orc.pack(x, graph).pages)
 
@@ -341,10 +342,11 @@ def _workload_parity(orc, torch, name, threads=16):
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
     print(f"[{name}] n={w.index.n} nq={len(q)} k={w.k} L={w.L} W={w.W}", flush=True)
-    ix = g.Index(a["x"], a["graph"])
+    ix = g.Index(a["x"], a["graph"])     # the library's default arrangement: vectors first
+    assert ix.info["vectors_first"] == 1
     e = ix.info["entry"]
     assert e == orc.medoid(a["x"])
-    packed = orc.pack(a["x"], a["graph"])
+    packed = orc.pack(a["x"], a["graph"], vectors_first=True)
     assert np.array_equal(ix.pages(), packed.pages)
     oids, od, oc, _ = packed.search(q, w.k, w.L, w.W, e, threads=threads)
     gi, gd, st = run_gpu(torch, ix, q, w.k, w.L, w.W)
