@@ -391,3 +391,29 @@ def test_resident_random_configuration(orc, torch_dev, seed):
           flush=True)
     check_parity(orc, torch_dev, a["x"], a["graph"], q, k, L, W,
                  layout={kk: v for kk, v in layout.items()})
+
+
+def test_searches_on_two_streams_do_not_share_counters(orc, torch_dev):
+    """Two searches of one index queued back to back on different streams
+    without waiting (device buffers, no stats): each must write every row.
+    They share the index's query counter, so the library orders the second
+    after the first on the GPU."""
+    torch = torch_dev
+    spec = IndexSpec(n=30000, D=128, dtype="u8", clusters=8, sigma=20.0, r_near=16, r_rand=16, seed=91)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(6000, 92))
+    k, L, W = 10, 48, 4
+    ix = g.Index(a["x"], a["graph"])
+    ref_ids, ref_d, _ = run_gpu(torch, ix, q, k, L, W)
+    qd = torch.from_numpy(q).cuda()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = [(torch.full((len(q), k), -1, dtype=torch.int32, device="cuda"),
+             torch.full((len(q), k), -1, dtype=torch.int32, device="cuda")) for _ in range(4)]
+    torch.cuda.synchronize()          # the buffers are filled before either stream writes them
+    for s, (ids, dd) in zip((s1, s2, s1, s2), outs):
+        ix.search_into(qd, len(q), k, L, W, ids, dd, stream=s.cuda_stream, stats=False)
+    torch.cuda.synchronize()
+    for ids, dd in outs:
+        assert np.array_equal(ids.cpu().numpy().view(np.uint32), ref_ids)
+        assert np.array_equal(dd.cpu().numpy(), ref_d)
+    ix.close()
