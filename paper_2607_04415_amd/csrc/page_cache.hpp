@@ -4,7 +4,8 @@
 // slot_word[s] packs one cache slot's whole state so that one atomic decides
 // every transition:
 //   bits  0..23  pins     waves currently using or waiting on the slot
-//   bit   24     ref      clock reference bit (set when the page arrives)
+//   bit   24     ref      clock reference bit (set by a hit, or by a lookup that
+//                         joins a page still LOADING: the page is used more than once)
 //   bits 25..26  state    EMPTY / LOADING / READY
 //   bits 32..63  page id
 // page_slot[p] maps a page to its slot (kNone if not cached).
@@ -17,8 +18,10 @@
 //            slot's old page is unmapped, then page_slot[page] is CAS-ed from
 //            kNone (losing that race gives the slot back and joins the winner)
 //   fill     after the page bytes are written with device-coherent stores and
-//            those stores have completed, atomicAdd turns LOADING into READY
-//            with ref set
+//            those stores have completed, atomicAdd turns LOADING into READY;
+//            the page arrives unreferenced, so a page read once (most pages a
+//            random edge brings in) is the clock's first victim, and a page
+//            that is hit keeps its slot for another sweep
 //   unpin    atomicSub(1)
 #pragma once
 
@@ -97,6 +100,7 @@ __device__ __forceinline__ uint32_t acquire_page(const CacheView &c, uint32_t pa
       const uint64_t old = atomicAdd(&c.slot_word[s], 1ull);
       const uint64_t st = sw_state(old);
       if (sw_page(old) == page && (st == kLoading || st == kReady)) {
+        if (!(old & kRefBit)) atomicOr(&c.slot_word[s], (unsigned long long)kRefBit);
         slot_out = s;
         return st == kReady ? kAcqReady : kAcqWait;
       }
