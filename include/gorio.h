@@ -212,8 +212,14 @@ gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_waves, uint32_t
  *   Slots past the reachable set are padded with UINT32_MAX and INT32_MAX / +inf.
  *   stats:   NULL or a struct to fill; non-NULL makes the call wait for the search.
  *   stream:  hipStream_t to launch on (NULL = the null stream).  With device
- *            pointers and stats == NULL the call returns without waiting.
- * Requires 1 <= k <= L <= 256 and 1 <= W <= L.  nq == 0 is a no-op.
+ *            pointers and stats == NULL a resident search returns without
+ *            waiting; a paged search always returns when it is done (the
+ *            calling thread runs its watchdog, and in mode 2 its scheduler).
+ * Requires 1 <= k <= L <= 256 and 1 <= W <= L (paged: W <= 64).  nq == 0 is a
+ * no-op.  Errors: GORIO_EINVAL for arguments out of range, GORIO_EUNSUPPORTED
+ * for a paged W above 64, GORIO_ENOMEM / GORIO_EDEVICE from the device,
+ * GORIO_ETIMEOUT when a paged search made no progress within the watchdog
+ * limit (the counters so far are filled; the cache is reset).
  */
 gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq,
                           uint32_t k, uint32_t L, uint32_t W,

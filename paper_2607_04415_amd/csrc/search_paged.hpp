@@ -21,6 +21,11 @@
 // blocking = 1 replaces split-phase service with wait-in-place: one query per
 // wave and one outstanding page per lane (the blocking demand-paging path the
 // paper compares against).
+//
+// paged_round (at the end of this file) runs the same per-query code for the
+// host-scheduled mode: one workgroup per lane the host chose, the lane's
+// state loaded from and saved to HBM around one turn; the fill waves then run
+// as a kernel of their own (search_paged launched with only fill blocks).
 #pragma once
 
 #include "metric.hpp"
