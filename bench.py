@@ -51,6 +51,16 @@ MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
 # query 20 us configuration asks for 4 query slots per wave; 30 waves gave 7,400 against
 # 7,414 for the default 39, so it keeps the default.
 SHAPE_C3 = {"oversub": 1, "query_waves": 30}
+# The paper's own figures (Table 2: 10,000 SIFT1M queries over NVMe-oF on one NVIDIA L40S,
+# ConnectX-6 200 Gb/s InfiniBand, a remote NVMe SSD; Table 1).  Context, not targets: a
+# different machine, transport and dataset.
+PAPER_CONTEXT = {
+    "hardware": "NVIDIA L40S 48 GB, Xeon Silver 4316, ConnectX-6 200 Gb/s InfiniBand, remote NVMe SSD over NVMe-oF",
+    "workload": "SIFT1M DiskANN-style graph, 10,000 queries, top-10",
+    "qps": {"G-Gust (host scheduler over GORIO's backend)": 10058, "GustANN-SPDK": 7680,
+            "G-ABaM (GPU split-phase scheduler)": 5650, "G-BaM (blocking)": 1155, "GDS": 83},
+    "speedups": {"G-Gust vs GustANN-SPDK": 1.31, "G-ABaM vs G-BaM": 4.89},
+}
 SHAPE_C5 = {"oversub": 1, "query_waves": 60}
 T_START = time.perf_counter()
 
@@ -654,6 +664,7 @@ def main():
         "resident_legs": resident_legs,
         "paged": paged,
         "skipped": skipped,
+        "paper_context": PAPER_CONTEXT,
         "bench_s": round(time.perf_counter() - T_START, 1),
     }
     print(json.dumps(out), flush=True)
