@@ -53,8 +53,9 @@ struct PageGeom {
   FastDiv rpp;             // records per page
   const uint32_t *node_to_slot;  // nullptr: slot = node id
   // 16-byte units: when every vector starts on a 16-byte boundary and the
-  // index has fewer than 2^31 units (units16 != 0), a vector is also named by
-  // its locator page * page16 + i * vec16, the index of its first unit.
+  // index spans at most 4 GiB (units16 != 0: a buffer instruction's byte
+  // offset, index x stride, is 32 bits), a vector is also named by its
+  // locator page * page16 + i * vec16, the index of its first unit.
   uint32_t units16;
   FastDiv page16;          // page_bytes / 16
   FastDiv vec16;           // vec_stride / 16

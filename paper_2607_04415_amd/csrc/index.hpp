@@ -178,8 +178,10 @@ struct gorio_index {
     }
     g.rpp = gorio::make_fastdiv(rpp);
     g.node_to_slot = d_node_to_slot;
+    // a buffer instruction's offset (index x stride) is a 32-bit byte offset:
+    // locators address at most the first 4 GiB of the pages
     const uint64_t units = index_bytes() / 16;
-    const bool loc16 = g.vec_stride % 16 == 0 && page_bytes % 16 == 0 && units < (1ull << 31);
+    const bool loc16 = g.vec_stride % 16 == 0 && page_bytes % 16 == 0 && index_bytes() <= (1ull << 32);
     g.units16 = loc16 ? (uint32_t)units : 0u;
     g.page16 = gorio::make_fastdiv(loc16 ? page_bytes / 16 : 1u);
     g.vec16 = gorio::make_fastdiv(loc16 ? g.vec_stride / 16 : 1u);

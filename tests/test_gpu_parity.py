@@ -417,3 +417,23 @@ def test_searches_on_two_streams_do_not_share_counters(orc, torch_dev):
         assert np.array_equal(ids.cpu().numpy().view(np.uint32), ref_ids)
         assert np.array_equal(dd.cpu().numpy(), ref_d)
     ix.close()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.skipif(os.environ.get("GORIO_SKIP_BIG") == "1", reason="GORIO_SKIP_BIG=1: a 4.3 GB index")
+def test_index_above_4gib_is_exact(orc, torch_dev):
+    """A uint8 128-d index whose pages span more than 4 GiB (one 4 KB record
+    per page): vectors can no longer be named by 32-bit buffer offsets, so the
+    kernel must address them with 64-bit pointers; answers equal the oracle's."""
+    spec = IndexSpec(n=1_050_000, D=128, dtype="u8", clusters=16, sigma=20.0, r_near=8, r_rand=8, seed=93)
+    a = index_arrays(spec)
+    q = query_array(spec, QuerySpec(300, 94))
+    layout = dict(vectors_first=True, record_bytes=4096)
+    ix = g.Index(a["x"], a["graph"], **layout)
+    assert ix.info["index_bytes"] > (1 << 32)
+    e = ix.info["entry"]
+    gi, gd, st = run_gpu(torch_dev, ix, q, 10, 32, 4)
+    ix.close()
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"], **layout).search(q, 10, 32, 4, e, threads=16)
+    assert np.array_equal(gi, oids) and np.array_equal(gd, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
