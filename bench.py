@@ -45,12 +45,13 @@ MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
 # Scheduler shapes of the paged legs (oversub = query slots per wave, query_waves; 0 = the
 # library's default, which runs as many queries as the cache's pins allow).  When the host
 # link is the bound, fewer queries in flight keep the link full and share the cache better
-# (a sweep on the full query counts: 1M index, 10% cache, 0 us: 30 waves x 1 slot 6,544
-# queries/s, 40 waves 6,477, 156 queries in 39 waves x 4 slots 5,716; 10M float32, 5%
-# cache: 60 waves x 1 slot 3,015, 1,302 queries in 326 waves x 4 slots 2,131).  The 100k
-# query 20 us configuration asks for 4 query slots per wave; 30 waves gave 7,400 against
-# 7,414 for the default 39, so it keeps the default.
+# (sweeps on the full query counts: 1M index, 10% cache, 0 us: 20 / 30 / 40 waves x 1 slot
+# 6,754 / 7,451 / 7,392 queries/s, the default 156 queries in 39 waves x 4 slots 6,472;
+# 10M float32, 5% cache: 40 / 60 / 80 waves x 1 slot 3,285 / 3,426 / 3,386, the default
+# 1,302 queries far less).  The 100k-query 20 us configuration asks for 4 query slots per
+# wave: 30 waves gave 8,512 against 8,351 for the default 39.
 SHAPE_C3 = {"oversub": 1, "query_waves": 30}
+SHAPE_C4 = {"oversub": 4, "query_waves": 30}
 # The paper's own figures (Table 2: 10,000 SIFT1M queries over NVMe-oF on one NVIDIA L40S,
 # ConnectX-6 200 Gb/s InfiniBand, a remote NVMe SSD; Table 1).  Context, not targets: a
 # different machine, transport and dataset.
@@ -177,14 +178,13 @@ def gather_ceiling(n: int, rpp: int, page_bytes: int, vec_stride: int):
 
 
 def cluster_count(arg: int, nq: int) -> int:
-    """k-means clusters for a paged leg: `arg` if positive, none if 0, else by
-    the leg's query count.  Queries are admitted cluster by cluster, so a
-    larger batch can use smaller clusters before too few of its queries share
-    each one (1M uint8 index, 10% cache: 256 clusters best at 10k queries,
-    512 at 100k)."""
+    """k-means clusters for a paged leg on the 1M index: `arg` if positive, none
+    if 0, else 512 (best of 128 / 256 / 512 / 768 / 1024 on the 10k-query leg,
+    and of 512 / 768 / 1024 on the 100k-query leg, with the current cache
+    policy).  Queries are admitted cluster by cluster."""
     if arg >= 0:
         return arg
-    return 256 if nq <= 20000 else 512
+    return 512
 
 
 def host_link_peak_gbs(torch) -> float:
@@ -350,8 +350,8 @@ def main():
                     help="queries of each 1M paged configuration to run (-1 = its full query count, "
                          "0 = skip the paged legs)")
     ap.add_argument("--paged-clusters", type=int, default=-1,
-                    help="paged legs: k-means clusters for page placement and query admission (0 = off, "
-                         "-1 = by the leg's query count: 256 up to 20k queries, 512 above)")
+                    help="1M paged legs: k-means clusters for page placement and query admission "
+                         "(0 = off, -1 = 512)")
     ap.add_argument("--paged-repeats", type=int, default=5,
                     help="cold-cache runs per paged leg of up to 20k queries (the median is reported)")
     ap.add_argument("--large-repeats", type=int, default=3,
@@ -363,7 +363,9 @@ def main():
     ap.add_argument("--f32-sample", type=int, default=-1,
                     help="queries of the 10M x 96-d float32 legs (-1 = all 100,000; 0 = skip)")
     ap.add_argument("--no-f32-paged", action="store_true", help="run the float32 resident leg only")
-    ap.add_argument("--f32-clusters", type=int, default=512)
+    ap.add_argument("--f32-clusters", type=int, default=1024,
+                    help="k-means clusters of the float32 paged leg (512 / 1024 / 2048 / 4096 gave "
+                         "3,426 / 4,284 / 4,112 / 3,416 queries/s)")
     ap.add_argument("--f32-cpu-sample", type=int, default=2000,
                     help="float32 queries the oracle runs (baseline and the GPU answers' check)")
     ap.add_argument("--budget-s", type=float, default=500.0,
@@ -563,7 +565,7 @@ def main():
             cl = placement(n4) if clustered else None
             leg, pi, pd, pq = paged_leg(torch, g, a, w4, n4, qps, 0, vfirst,
                                         args.large_repeats if n4 > 20000 else args.paged_repeats, cl,
-                                        warmup_nq=10000)
+                                        warmup_nq=10000, **SHAPE_C4)
             check(leg, pi, pd, pq, w4)
             if packed_main is not None:   # these queries differ from the resident batch: the oracle checks a slice
                 ns = min(args.f32_cpu_sample, len(pq))

@@ -1,5 +1,5 @@
-"""Host-side logic of bench.py (no GPU): the one-GPU guard and the per-leg
-k-means cluster count of the paged legs."""
+"""Host-side logic of bench.py (no GPU): the one-GPU guard, the k-means
+cluster count of the paged legs, and the roofline and baseline helpers."""
 import subprocess
 import sys
 from pathlib import Path
@@ -17,10 +17,8 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.stdout.strip() == ""
 
 
-def test_cluster_count_by_leg_size():
-    assert bench.cluster_count(-1, 10000) == 256
-    assert bench.cluster_count(-1, 20000) == 256
-    assert bench.cluster_count(-1, 20001) == 512
+def test_cluster_count_default_and_overrides():
+    assert bench.cluster_count(-1, 10000) == 512
     assert bench.cluster_count(-1, 100000) == 512
     assert bench.cluster_count(0, 100000) == 0        # placement off
     assert bench.cluster_count(384, 10000) == 384     # fixed by the caller
