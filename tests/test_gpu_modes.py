@@ -126,11 +126,11 @@ def test_host_rounds_held_proxy_then_recover(torch_dev, small, monkeypatch):
 def test_host_rounds_1m_bench_configuration(orc, torch_dev):
     """The 1M uint8 index, 10% cold cache, 0 us, all 10,000 queries, in the
     benchmark's launch configuration for the host-scheduled leg (vectors-first
-    pages placed by 256 clusters, queries admitted by cluster)."""
+    pages placed by 512 clusters, queries admitted by cluster)."""
     w = WORKLOADS["u8-1m-cache10-lat0"]
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
-    n2s, cent = g.cluster_order(a["x"], 256)
+    n2s, cent = g.cluster_order(a["x"], 512)
     ix = g.Index(a["x"], a["graph"], vectors_first=True, node_to_slot=n2s)
     ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))
     ix.set_backing(latency_us=w.latency_us, mode=HOST)
@@ -188,8 +188,8 @@ F32_10M = WORKLOADS["f32-10m-cache5-lat20"]
 def test_workload_f32_10m_full(orc, torch_dev):
     """All 100,000 queries of the 10M x 96-d float32 configuration, in the
     benchmark's launch configurations: the HBM-resident search (vectors-first
-    pages) and the paged search (5% cold cache, 20 us per request, 4 query
-    slots per wave, pages placed by 512 clusters, queries admitted by
+    pages) and the paged search (5% cold cache, 20 us per request, 60 query
+    waves of one query, pages placed by 1024 clusters, queries admitted by
     cluster).  Both equal the oracle element by element: ids and distance bits,
     after the 1e-5 relative / 0.999 id-overlap acceptance bound."""
     w = F32_10M
@@ -201,10 +201,11 @@ def test_workload_f32_10m_full(orc, torch_dev):
     ri, rd, rst = search(torch_dev, ix, q, w.k, w.L, w.W)
     ix.close()
     print(f"[f32 10m full] resident search done ({rst['kernel_ms']:.1f} ms)", flush=True)
-    n2s, cent = g.cluster_order(a["x"], 512)
+    n2s, cent = g.cluster_order(a["x"], 1024)
     px = g.Index(a["x"], a["graph"], vectors_first=True, node_to_slot=n2s)
     px.set_cache(int(w.cache_frac * px.info["index_bytes"]))
-    px.set_backing(latency_us=w.latency_us, oversub=w.oversub)
+    px.set_backing(latency_us=w.latency_us, oversub=1)
+    px.set_scheduler(query_waves=60)
     px.set_query_order(cent)
     gi, gd, st = search(torch_dev, px, q, w.k, w.L, w.W)
     px.close()

@@ -236,19 +236,20 @@ def test_paged_1m_index_slice(orc, torch_dev):
           f"{st['bytes_served'] / st['kernel_ms'] / 1e6:.2f} GB/s", flush=True)
 
 
-@pytest.mark.parametrize("name", ["u8-1m-cache10-lat0", "u8-1m-cache10-lat20"])
-def test_paged_1m_bench_configuration(orc, torch_dev, name):
+@pytest.mark.parametrize("name,oversub,waves", [("u8-1m-cache10-lat0", 1, 30), ("u8-1m-cache10-lat20", 4, 30)])
+def test_paged_1m_bench_configuration(orc, torch_dev, name, oversub, waves):
     """The benchmark's paged legs at full size and in its launch configuration
-    (vectors-first pages placed by 256 clusters, queries admitted by cluster,
-    cold 10% cache, the workload's latency and query slots): every query of
-    the configuration equals the oracle."""
+    (vectors-first pages placed by 512 clusters, queries admitted by cluster,
+    cold 10% cache, the workload's latency, the bench's scheduler shape):
+    every query of the configuration equals the oracle."""
     w = WORKLOADS[name]
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
-    n2s, cent = g.cluster_order(a["x"], 256)
+    n2s, cent = g.cluster_order(a["x"], 512)
     ix = g.Index(a["x"], a["graph"], vectors_first=True, node_to_slot=n2s)
     ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))
-    ix.set_backing(latency_us=w.latency_us, oversub=w.oversub)
+    ix.set_backing(latency_us=w.latency_us, oversub=oversub)
+    ix.set_scheduler(query_waves=waves)
     ix.set_query_order(cent)
     gi, gd, st = search(torch_dev, ix, q, w.k, w.L, w.W)
     e = ix.info["entry"]
