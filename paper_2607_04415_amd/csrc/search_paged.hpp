@@ -197,7 +197,7 @@ __device__ __forceinline__ void fill_entries(const PagedParams &p, unsigned long
     }
     wait_stores_performed();
     if ((uint32_t)l >= i0 && (uint32_t)l < min(i0 + kFillBatch, n))
-      atomicAdd(&p.cache.slot_word[(uint32_t)e], 1ull << kStateShift);
+      mark_ready(p.cache, (uint32_t)e);
   }
 }
 
