@@ -45,13 +45,15 @@ MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
 # Scheduler shapes of the paged legs (oversub = query slots per wave, query_waves; 0 = the
 # library's default, which runs as many queries as the cache's pins allow).  When the host
 # link is the bound, fewer queries in flight keep the link full and share the cache better
-# (sweeps on the full query counts: 1M index, 10% cache, 0 us: 20 / 30 / 40 waves x 1 slot
-# 6,754 / 7,451 / 7,392 queries/s, the default 156 queries in 39 waves x 4 slots 6,472;
-# 10M float32, 5% cache: 40 / 60 / 80 waves x 1 slot 3,285 / 3,426 / 3,386, the default
-# 1,302 queries far less).  The 100k-query 20 us configuration asks for 4 query slots per
-# wave: 30 waves gave 8,512 against 8,351 for the default 39.
+# (sweeps on the full query counts: 1M index, 10% cache, 0 us, 256 clusters: 20 / 30 / 40
+# waves x 1 slot 6,754 / 7,451 / 7,392 queries/s; 512 clusters: 30 x 1 7,597 against 6,260
+# for the default 156 queries in 39 waves x 4 slots; 10M float32, 5% cache, 512 clusters:
+# 40 / 60 / 80 waves x 1 slot 3,285 / 3,426 / 3,386, the default 1,302 queries far less).
+# The 100k-query 20 us configuration asks for 4 query slots per wave: 30 waves gave 8,512
+# against 8,351 for the default 39.
 SHAPE_C3 = {"oversub": 1, "query_waves": 30}
 SHAPE_C4 = {"oversub": 4, "query_waves": 30}
+SHAPE_C5 = {"oversub": 1, "query_waves": 60}
 # The paper's own figures (Table 2: 10,000 SIFT1M queries over NVMe-oF on one NVIDIA L40S,
 # ConnectX-6 200 Gb/s InfiniBand, a remote NVMe SSD; Table 1).  Context, not targets: a
 # different machine, transport and dataset.
@@ -62,7 +64,6 @@ PAPER_CONTEXT = {
             "G-ABaM (GPU split-phase scheduler)": 5650, "G-BaM (blocking)": 1155, "GDS": 83},
     "speedups": {"G-Gust vs GustANN-SPDK": 1.31, "G-ABaM vs G-BaM": 4.89},
 }
-SHAPE_C5 = {"oversub": 1, "query_waves": 60}
 T_START = time.perf_counter()
 
 
