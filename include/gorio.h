@@ -53,6 +53,19 @@
  *     may be used from different threads.
  *   - The device is the HIP device current when gorio_build_index is called;
  *     later calls switch to it and restore the caller's device.
+ *
+ * Environment (read by each paged search; tuning and test hooks, none needed
+ * for normal use):
+ *   GORIO_FILL_WAVES       waves that only copy arriving pages (default 32, at most 64)
+ *   GORIO_MAX_PENDING      page requests per query, overriding gorio_set_scheduler's
+ *   GORIO_TURN_PASSES      host-scheduled rounds: passes before a lane yields (default 2)
+ *   GORIO_ROUNDS_STATS     1: print the host scheduler's counters to stderr
+ *   GORIO_WATCHDOG_S       a paged search still running after this many seconds is
+ *                          aborted with GORIO_ETIMEOUT (default 120)
+ *   GORIO_PROXY_JITTER_US  extra random delay per page request (completions reorder)
+ *   GORIO_PROXY_HOLD       1: the proxy completes nothing (exercises the watchdog)
+ *   GORIO_CTRL_STRIDE      spacing of the paged search's control words, in 8-byte words
+ *                          (default 32, read when the cache is set)
  */
 #ifndef GORIO_H
 #define GORIO_H
@@ -71,7 +84,7 @@ typedef enum {
     GORIO_EINVAL = 1,        /* an argument is out of range or inconsistent */
     GORIO_ENOMEM = 2,        /* device or pinned host allocation failed */
     GORIO_EDEVICE = 3,       /* a HIP runtime call or a kernel failed */
-    GORIO_ETIMEOUT = 4,      /* paged search made no progress within the watchdog limit */
+    GORIO_ETIMEOUT = 4,      /* paged search did not finish within the watchdog limit */
     GORIO_EUNSUPPORTED = 5   /* valid request the library does not implement */
 } gorio_status;
 
@@ -218,7 +231,7 @@ gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_waves, uint32_t
  * Requires 1 <= k <= L <= 256 and 1 <= W <= L (paged: W <= 64).  nq == 0 is a
  * no-op.  Errors: GORIO_EINVAL for arguments out of range, GORIO_EUNSUPPORTED
  * for a paged W above 64, GORIO_ENOMEM / GORIO_EDEVICE from the device,
- * GORIO_ETIMEOUT when a paged search made no progress within the watchdog
+ * GORIO_ETIMEOUT when a paged search did not finish within the watchdog
  * limit (the counters so far are filled; the cache is reset).
  */
 gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq,

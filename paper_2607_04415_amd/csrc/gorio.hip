@@ -889,7 +889,7 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
     stats->proxy_peak = ix->paged ? ix->paged->proxy.max_in_flight() : 0;
     stats->wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
   }
-  if (timed_out) return fail(GORIO_ETIMEOUT, "paged search made no progress within the watchdog limit");
+  if (timed_out) return fail(GORIO_ETIMEOUT, "paged search did not finish within the watchdog limit");
   return GORIO_OK;
 }
 
