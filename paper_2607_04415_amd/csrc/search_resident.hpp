@@ -8,9 +8,9 @@
 // compute distances, update the frontier):
 //   select  - the first W unexpanded slots of F (ballot + prefix count);
 //   expand  - one round trip reads the degree and id list of every chosen
-//             node of a beam group (up to 256 ids, 4 per lane); a beam of
-//             several groups reads the next group's lists while the current
-//             one is filtered and evaluated;
+//             node of a beam group (up to 256 ids, 4 per lane); with float32
+//             line-gathered rows a beam of several groups reads the next
+//             group's lists while the current one is filtered and evaluated;
 //   filter  - ids already in the visited filter are dropped (LDS atomics),
 //             the rest compacted into an LDS candidate list;
 //   evaluate- one round trip gathers a batch of candidate vectors; the
@@ -160,9 +160,12 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
       // ---- expand: degrees (lane b) and all id slots of a beam group at once.
       // Loads are unconditional (lanes past the group read the group's first
       // record) so that no branch separates them: one round trip per group.
-      // When the beam spans several groups, the next group's lists are read
-      // while this group is filtered and evaluated, so only the first group's
-      // round trip is exposed.
+      // Float32 line-gathered rows (W=8, R=64: two groups per beam) read the
+      // next group's lists while this group is filtered and evaluated, so only
+      // the first group's round trip is exposed.  Other metrics read a group's
+      // lists when they reach it: a uint8 beam at W=4 fits one group, and a
+      // second set of list registers would only constrain the allocator.
+      constexpr bool kAhead = M::kGathered;
       struct AdjLoad {
         uint64_t off;  // lane b: adjacency block of the group's beam b
         uint32_t deg;  // lane b: its degree
@@ -182,21 +185,45 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
           A.ids[t] = reinterpret_cast<const uint32_t *>(p.pages + adj + 4)[pos - b * p.R];
         }
       };
-      AdjLoad cur, nxt;
-      issue_adj(0, cur);
+      [[maybe_unused]] AdjLoad cur, nxt;
+      if constexpr (kAhead) issue_adj(0, cur);
       for (uint32_t b0 = 0; b0 < nbeam; b0 += beams_per_group) {
         const uint32_t nb = min(nbeam - b0, beams_per_group);
         const uint32_t nslots = nb * p.R;
-        if (b0 + beams_per_group < nbeam) issue_adj(b0 + beams_per_group, nxt);
         uint32_t ids[kIdsPerLane];
         bool valid[kIdsPerLane];
+        if constexpr (kAhead) {
+          if (b0 + beams_per_group < nbeam) issue_adj(b0 + beams_per_group, nxt);
 #pragma unroll
-        for (int t = 0; t < kIdsPerLane; ++t) {
-          const uint32_t pos = min(t * kWave + (uint32_t)l, nslots - 1);
-          const uint32_t b = fastdiv(pos, p.Rdiv);
-          const uint32_t deg = min((uint32_t)__shfl((int)cur.deg, (int)b), p.R);
-          ids[t] = cur.ids[t];
-          valid[t] = (uint32_t)(t * kWave + l) < nslots && pos - b * p.R < deg && ids[t] < p.n;
+          for (int t = 0; t < kIdsPerLane; ++t) {
+            const uint32_t pos = min(t * kWave + (uint32_t)l, nslots - 1);
+            const uint32_t b = fastdiv(pos, p.Rdiv);
+            const uint32_t deg = min((uint32_t)__shfl((int)cur.deg, (int)b), p.R);
+            ids[t] = cur.ids[t];
+            valid[t] = (uint32_t)(t * kWave + l) < nslots && pos - b * p.R < deg && ids[t] < p.n;
+          }
+        } else {
+          const uint32_t my_beam = beam[b0 + min((uint32_t)l, nb - 1)];
+          const uint64_t my_adj = adj_offset(p.geom, slot_ct<N2S>(p.geom, my_beam));
+          const uint32_t my_deg = *reinterpret_cast<const uint32_t *>(p.pages + my_adj);
+          uint32_t slot_beam[kIdsPerLane], slot_j[kIdsPerLane];
+#pragma unroll
+          for (int t = 0; t < kIdsPerLane; ++t) {
+            const uint32_t pos = min(t * kWave + (uint32_t)l, nslots - 1);
+            const uint32_t b = fastdiv(pos, p.Rdiv);
+            slot_beam[t] = b;
+            slot_j[t] = pos - b * p.R;
+          }
+#pragma unroll
+          for (int t = 0; t < kIdsPerLane; ++t) {
+            const uint64_t adj = __shfl(my_adj, (int)slot_beam[t]);
+            ids[t] = reinterpret_cast<const uint32_t *>(p.pages + adj + 4)[slot_j[t]];
+          }
+#pragma unroll
+          for (int t = 0; t < kIdsPerLane; ++t) {
+            const uint32_t deg = min((uint32_t)__shfl((int)my_deg, (int)slot_beam[t]), p.R);
+            valid[t] = (uint32_t)(t * kWave + l) < nslots && slot_j[t] < deg && ids[t] < p.n;
+          }
         }
         // ---- filter through the visited table, compact the new ids ------------
         bool isnew[kIdsPerLane], recorded[kIdsPerLane];
@@ -251,7 +278,7 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
           }
         }
         __syncthreads();
-        cur = nxt;
+        if constexpr (kAhead) cur = nxt;
       }
     }
 
