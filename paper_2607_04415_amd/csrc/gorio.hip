@@ -150,8 +150,9 @@ extern "C" gorio_status gorio_build_index(gorio_dtype dtype, const void *vectors
   HIP_OR_FAIL(hipEventCreate(&ix->ev_start));
   HIP_OR_FAIL(hipEventCreate(&ix->ev_stop));
   HIP_OR_FAIL(hipEventCreateWithFlags(&ix->ev_done, hipEventDisableTiming));
-  HIP_OR_FAIL(hipMalloc(&ix->d_stats, sizeof(unsigned long long) * kStatWords));
+  HIP_OR_FAIL(hipMalloc(&ix->d_stats, sizeof(unsigned long long) * 2 * kStatWords));
   hipStream_t s = ix->stream;
+  fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(ix->d_stats), 4 * kStatWords, 0u);
 
   DevBuf d_vec, d_graph, d_flags;
   HIP_OR_FAIL(d_vec.alloc((size_t)n * vb));
@@ -830,10 +831,14 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   if (!i_dev) { HIP_OR_FAIL(ibuf.alloc(obytes)); d_ids = ibuf.as<uint32_t>(); }
   if (!d_dev) { HIP_OR_FAIL(dbuf.alloc(obytes)); d_dists = dbuf.p; }
 
-  // the previous search of this index, on whatever stream it ran, finishes
-  // before this one clears the counters it shares
-  if (ix->ev_done_recorded) HIP_OR_FAIL(hipStreamWaitEvent(s, ix->ev_done, 0));
-  fill_u32<<<1, 64, 0, s>>>(reinterpret_cast<uint32_t *>(ix->d_stats), 2 * kStatWords, 0u);
+  // the previous search of this index finishes before this one uses the
+  // counters they share: on the same stream by stream order, on another
+  // stream by waiting for the event it recorded last
+  if (ix->ev_done_recorded && ix->last_stream != s) HIP_OR_FAIL(hipStreamWaitEvent(s, ix->ev_done, 0));
+  // the counters only grow; a search that reports them reports the growth
+  if (stats)
+    HIP_OR_FAIL(hipMemcpyAsync(ix->d_stats + kStatWords, ix->d_stats, kStatWords * sizeof(unsigned long long),
+                               hipMemcpyDeviceToDevice, s));
 
   ResidentParams p;
   p.pages = ix->d_pages;
@@ -852,14 +857,16 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   p.out_dists = static_cast<uint32_t *>(d_dists);
   p.stats = ix->d_stats;
   p.next_query = ix->d_stats + kStatNextQuery;
+  p.next_base = ix->next_base;
 
   gorio_status st;
   bool timed_out = false;
   if (ix->resident) {
     const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
-    HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+    if (stats) HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
     HIP_OR_FAIL(ix->dtype == GORIO_F32 ? launch_resident_f32(p, grid, s) : launch_resident_u8(p, grid, s));
-    HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+    ix->next_base += nq;  // every query takes one ticket
+    if (stats) HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
   } else {
     st = run_paged(ix, p, s, timed_out);
     if (st != GORIO_OK) return st;
@@ -867,25 +874,27 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
 
   if (!i_dev) HIP_OR_FAIL(hipMemcpyAsync(ids, d_ids, obytes, hipMemcpyDeviceToHost, s));
   if (!d_dev) HIP_OR_FAIL(hipMemcpyAsync(dists, d_dists, obytes, hipMemcpyDeviceToHost, s));
-  unsigned long long h_stats[kStatWords] = {};
-  if (stats) HIP_OR_FAIL(hipMemcpyAsync(h_stats, ix->d_stats, sizeof h_stats, hipMemcpyDeviceToHost, s));
+  unsigned long long h_cnt[2 * kStatWords] = {};  // counters after, then before
+  if (stats) HIP_OR_FAIL(hipMemcpyAsync(h_cnt, ix->d_stats, sizeof h_cnt, hipMemcpyDeviceToHost, s));
   HIP_OR_FAIL(hipEventRecord(ix->ev_done, s));
   ix->ev_done_recorded = true;
+  ix->last_stream = s;
   if (stats || !i_dev || !d_dev || !q_dev) HIP_OR_FAIL(hipStreamSynchronize(s));
   if (stats) {
     float ms = 0.f;
     HIP_OR_FAIL(hipEventElapsedTime(&ms, ix->ev_start, ix->ev_stop));
     stats->kernel_ms = ms;
-    stats->evaluations = h_stats[kStatEval];
-    stats->reevaluations = h_stats[kStatReeval];
-    stats->expansions = h_stats[kStatExp];
-    stats->iterations = h_stats[kStatIter];
-    stats->hits = h_stats[kStatHit];
-    stats->misses = h_stats[kStatMiss];
-    stats->pages_served = h_stats[kStatServed];
-    stats->bytes_served = h_stats[kStatServed] * ix->page_bytes;
-    stats->parks = h_stats[kStatPark];
-    stats->resumes = h_stats[kStatResume];
+    auto grown = [&](int w) { return h_cnt[w] - h_cnt[kStatWords + w]; };
+    stats->evaluations = grown(kStatEval);
+    stats->reevaluations = grown(kStatReeval);
+    stats->expansions = grown(kStatExp);
+    stats->iterations = grown(kStatIter);
+    stats->hits = grown(kStatHit);
+    stats->misses = grown(kStatMiss);
+    stats->pages_served = grown(kStatServed);
+    stats->bytes_served = grown(kStatServed) * ix->page_bytes;
+    stats->parks = grown(kStatPark);
+    stats->resumes = grown(kStatResume);
     stats->proxy_peak = ix->paged ? ix->paged->proxy.max_in_flight() : 0;
     stats->wall_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
   }

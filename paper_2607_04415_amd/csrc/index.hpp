@@ -27,7 +27,8 @@ enum StatWord : int {
   kStatServed,
   kStatPark,
   kStatResume,
-  kStatNextQuery,  // resident kernel: queries handed out past the first grid
+  kStatNextQuery,  // resident kernel: query tickets (grows by nq per launch)
+  kStatMalformed,  // paged kernel: completion entries it could not use
   kStatWords = 16
 };
 
@@ -158,7 +159,13 @@ struct gorio_index {
   // issued on different streams never share the counters below at once.
   hipEvent_t ev_done = nullptr;
   bool ev_done_recorded = false;
+  hipStream_t last_stream = nullptr;  // stream of the last search (its ev_done)
+  // Counters (kStatWords 64-bit words) that only grow, then a snapshot of
+  // them taken before a search that reports statistics (it reports the
+  // difference).  next_base is the query-ticket counter's value when the next
+  // resident launch starts.
   unsigned long long *d_stats = nullptr;
+  uint64_t next_base = 0;
 
   uint64_t index_bytes() const { return num_pages * (uint64_t)page_bytes; }
 

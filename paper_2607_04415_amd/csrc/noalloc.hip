@@ -94,7 +94,7 @@ extern "C" gorio_status gorio_search_noalloc(gorio_index *ix, const void *querie
     if (e != hipSuccess) return fail(GORIO_EDEVICE, "%s: %s", #expr, hipGetErrorString(e)); \
   } while (0)
   // after the previous search of this index (its events are reused here)
-  if (ix->ev_done_recorded) NOALLOC_HIP(hipStreamWaitEvent(s, ix->ev_done, 0));
+  if (ix->ev_done_recorded && ix->last_stream != s) NOALLOC_HIP(hipStreamWaitEvent(s, ix->ev_done, 0));
   zero_words<<<1, 64, 0, s>>>(sc, kScratchWords);
   NOALLOC_HIP(hipGetLastError());
 
@@ -115,6 +115,7 @@ extern "C" gorio_status gorio_search_noalloc(gorio_index *ix, const void *querie
   p.out_dists = static_cast<uint32_t *>(dists);
   p.stats = sc;
   p.next_query = sc + kStatNextQuery;
+  p.next_base = 0;  // cleared above
   const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
   NOALLOC_HIP(hipEventRecord(ix->ev_start, s));
   NOALLOC_HIP(ix->dtype == GORIO_F32 ? launch_resident_f32(p, grid, s) : launch_resident_u8(p, grid, s));
@@ -123,6 +124,7 @@ extern "C" gorio_status gorio_search_noalloc(gorio_index *ix, const void *querie
   if (stats) NOALLOC_HIP(hipMemcpyAsync(h, sc, sizeof h, hipMemcpyDeviceToHost, s));
   NOALLOC_HIP(hipEventRecord(ix->ev_done, s));
   ix->ev_done_recorded = true;
+  ix->last_stream = s;
   if (stats) {
     NOALLOC_HIP(hipStreamSynchronize(s));
     float ms = 0.f;

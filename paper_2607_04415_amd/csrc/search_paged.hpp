@@ -172,7 +172,7 @@ __device__ __forceinline__ uint32_t load_completions(const PagedParams &p, const
   const uint32_t pg = (uint32_t)(e >> 32) - 1u, sl = (uint32_t)e;
   const uint64_t mbad = ballot((uint32_t)l < n && (pg >= p.num_pages || sl >= p.cache.slots));
   if (mbad == 0) return n;
-  if (l == 0) atomicAdd(&p.stats[9], (unsigned long long)__popcll(mbad));
+  if (l == 0) atomicAdd(&p.stats[10], (unsigned long long)__popcll(mbad));  // malformed completions
   return (uint32_t)__builtin_ctzll(mbad);
 }
 

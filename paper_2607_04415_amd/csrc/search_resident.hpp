@@ -41,7 +41,12 @@ struct ResidentParams {
   uint32_t *out_ids;       // nq x k
   uint32_t *out_dists;     // nq x k distance bits (int32 or float32)
   unsigned long long *stats;  // [evaluations, reevaluations, expansions, iterations]
-  unsigned long long *next_query;  // zero at launch: queries handed out past the first grid
+  // Queries past the first grid are handed out by a counter that only grows:
+  // every completed query takes one ticket, so a launch adds exactly nq, and
+  // next_base is the counter's value when this launch starts (no reset between
+  // launches).
+  unsigned long long *next_query;
+  unsigned long long next_base;
 };
 
 // Evaluates NCH chunks of 64 compacted candidates (locator metrics) and
@@ -293,7 +298,7 @@ __global__ __launch_bounds__(kWave, M::kWavesPerSimd) void search_resident(Resid
       }
     }
     uint32_t next = 0;
-    if (l == 0) next = (uint32_t)atomicAdd(p.next_query, 1ull);
+    if (l == 0) next = (uint32_t)(atomicAdd(p.next_query, 1ull) - p.next_base);
     qi = gridDim.x + first_lane_value(next);
   }
 

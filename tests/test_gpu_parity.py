@@ -419,6 +419,49 @@ def test_searches_on_two_streams_do_not_share_counters(orc, torch_dev):
     ix.close()
 
 
+def test_back_to_back_searches_without_stats_then_with(orc, torch_dev):
+    """The query-ticket counter and the statistics counters are never reset
+    between searches: searches of different sizes queued back to back without
+    statistics (one stream, then a second), and a paged search in between, must
+    each answer every query exactly; a search that asks for statistics then
+    reports its own counts only (the oracle's expansions and iterations)."""
+    torch = torch_dev
+    spec = IndexSpec(n=20000, D=128, dtype="u8", clusters=8, sigma=20.0, r_near=16, r_rand=16, seed=95)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(3000, 96))
+    k, L, W = 10, 32, 4
+    ix = g.Index(a["x"], a["graph"])
+    e = ix.info["entry"]
+    oids, od, oc, _ = orc.pack(a["x"], a["graph"]).search(q, k, L, W, e, threads=16)
+    qd = torch.from_numpy(q).cuda()
+    sizes = [3000, 1, 1777, 3000, 64, 2500]
+    outs = [(torch.full((m, k), -1, dtype=torch.int32, device="cuda"),
+             torch.full((m, k), -1, dtype=torch.int32, device="cuda")) for m in sizes]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for i, (m, (ids, dd)) in enumerate(zip(sizes, outs)):
+        s = s1 if i < 4 else s2
+        ix.search_into(qd[:m], m, k, L, W, ids, dd, stream=s.cuda_stream, stats=False)
+    torch.cuda.synchronize()
+    for m, (ids, dd) in zip(sizes, outs):
+        assert np.array_equal(ids.cpu().numpy().view(np.uint32), oids[:m]), m
+        assert np.array_equal(dd.cpu().numpy(), od[:m]), m
+    gi, gd, st = run_gpu(torch, ix, q, k, L, W)
+    assert np.array_equal(gi, oids) and np.array_equal(gd, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+    assert st["iterations"] == int(oc["iterations"].sum())
+    # a paged search on the same index, then resident again: counts stay per search
+    ix.set_cache(int(0.2 * ix.info["index_bytes"]))
+    pi, pd, pst = run_gpu(torch, ix, q[:500], k, L, W)
+    assert np.array_equal(pi, oids[:500]) and np.array_equal(pd, od[:500])
+    assert pst["expansions"] == int(oc["expansions"][:500].sum())
+    ix.set_cache(ix.info["index_bytes"])
+    gi, gd, st = run_gpu(torch, ix, q[:2000], k, L, W)
+    assert np.array_equal(gi, oids[:2000]) and np.array_equal(gd, od[:2000])
+    assert st["expansions"] == int(oc["expansions"][:2000].sum())
+    ix.close()
+
+
 @pytest.mark.timeout(900)
 @pytest.mark.skipif(os.environ.get("GORIO_SKIP_BIG") == "1", reason="GORIO_SKIP_BIG=1: a 4.3 GB index")
 def test_index_above_4gib_is_exact(orc, torch_dev):
