@@ -68,6 +68,14 @@ __device__ __forceinline__ uint64_t load_word(const unsigned long long *p) {
 // Result of looking a page up for one record access.
 enum : uint32_t { kAcqReady = 0, kAcqWait = 1, kAcqNoSlot = 2 };
 
+// A point where a host test may stretch the time between two steps of a
+// transition (the CPU harness delays a thread there to widen races); empty in
+// the library.
+#ifndef GORIO_SLOT_PAUSE
+#define GORIO_SLOT_PAUSE(where)
+#endif
+enum : int { kPauseAfterLookup = 0, kPauseAfterClaim = 1, kPauseBeforeGiveBack = 2 };
+
 // Publish a miss descriptor {page, slot} to the proxy (8 bytes, nonzero).
 __device__ __forceinline__ void publish_miss(const CacheView &c, uint32_t page, uint32_t slot) {
   const unsigned long long t = atomicAdd(c.mq_tail, 1ull);
@@ -107,9 +115,21 @@ __device__ __forceinline__ uint32_t acquire_page(const CacheView &c, uint32_t pa
   for (int attempt = 0; attempt < 64; ++attempt) {
     const uint32_t s = __hip_atomic_load(&c.page_slot[page], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (s != kNone) {
+      GORIO_SLOT_PAUSE(kPauseAfterLookup);
       const uint64_t old = atomicAdd(&c.slot_word[s], 1ull);
       const uint64_t st = sw_state(old);
       if (sw_page(old) == page && (st == kLoading || st == kReady)) {
+        // The lookup may be stale: the slot can have been evicted and claimed
+        // again for this same page by a wave that then loses the race to map
+        // it and gives the slot back, unfilled.  A LOADING slot is joined only
+        // while the page maps to it (only that claim's successful map can make
+        // it so, and a pinned slot is never claimed again); a READY slot is
+        // always mapped.  The load is issued after the pin has returned.
+        if (st == kLoading &&
+            __hip_atomic_load(&c.page_slot[page], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != s) {
+          atomicSub(&c.slot_word[s], 1ull);
+          continue;
+        }
         if (!(old & kRefBit)) atomicOr(&c.slot_word[s], (unsigned long long)kRefBit);
         slot_out = s;
         return st == kReady ? kAcqReady : kAcqWait;
@@ -120,10 +140,12 @@ __device__ __forceinline__ uint32_t acquire_page(const CacheView &c, uint32_t pa
     if (!allow_claim) return kAcqNoSlot;
     const uint32_t ns = claim_slot(c, page);
     if (ns == kNone) return kAcqNoSlot;
+    GORIO_SLOT_PAUSE(kPauseAfterClaim);
     if (atomicCAS(&c.page_slot[page], kNone, ns) != kNone) {
       // another wave mapped the page first: give the slot back in one atomic
       // (LOADING -> EMPTY and our pin dropped; pins of concurrent lookups
       // stay), then join the winner's slot
+      GORIO_SLOT_PAUSE(kPauseBeforeGiveBack);
       atomicSub(&c.slot_word[ns], (kLoading << kStateShift) | 1ull);
       continue;
     }

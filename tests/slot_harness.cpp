@@ -25,10 +25,11 @@
 // buffer operations and waits in page_cache.hpp).
 //
 // usage: slot_harness slots pages queries_in_flight max_pending queries
-//                     accesses fillers latency_us seed stall_s [control]
+//                     accesses fillers latency_us seed stall_s [control [pause_us]]
 // control (negative controls, which the stamp check must catch): 1 = a query
 // unpins before it reads the page; 2 = a fill marks the slot READY before it
-// writes the page.
+// writes the page.  pause_us > 0 makes a thread sleep that long, now and then,
+// at the state machine's pause points (between a lookup and its pin).
 #include <atomic>
 #include <chrono>
 #include <cstdint>
@@ -53,6 +54,18 @@ template <class T, class U, class V> inline T atomicCAS(T *p, U expected, V desi
   return e;
 }
 
+// Delays at the state machine's pause points (pause_us > 0): a thread sleeps
+// there now and then, so that other threads run whole transitions in between.
+static double g_pause_us = 0.0;
+static thread_local uint64_t t_pause_rng = 0x853c49e6748fea9bull;
+static inline void slot_pause() {
+  if (g_pause_us <= 0.0) return;
+  t_pause_rng = t_pause_rng * 6364136223846793005ull + 1442695040888963407ull;
+  if ((t_pause_rng >> 59) == 0)  // 1 in 32
+    std::this_thread::sleep_for(std::chrono::nanoseconds((int64_t)(g_pause_us * 1000)));
+}
+#define GORIO_SLOT_PAUSE(where) slot_pause()
+
 #include "../paper_2607_04415_amd/csrc/slot_state.hpp"
 
 using namespace gorio;
@@ -68,7 +81,7 @@ static uint64_t splitmix64(uint64_t x) {
 int main(int argc, char **argv) {
   if (argc < 11) {
     fprintf(stderr, "usage: %s slots pages queries_in_flight max_pending queries accesses fillers "
-                    "latency_us seed stall_s [control]\n", argv[0]);
+                    "latency_us seed stall_s [control [pause_us]]\n", argv[0]);
     return 2;
   }
   const uint32_t slots = (uint32_t)atoi(argv[1]);
@@ -83,6 +96,7 @@ int main(int argc, char **argv) {
   const double stall_s = atof(argv[10]);
   const int control = argc > 11 ? atoi(argv[11]) : 0;
   const bool read_after_unpin = control == 1, ready_before_bytes = control == 2;
+  g_pause_us = argc > 12 ? atof(argv[12]) : 0.0;
   if (slots == 0 || pages == 0 || live <= 0 || max_pending == 0 || fillers <= 0) return 2;
 
   uint32_t ring = 1;
@@ -176,7 +190,15 @@ int main(int argc, char **argv) {
         else
           std::this_thread::yield();
       }
-      for (const Pending &p : pend) unpin(c, p.slot);  // only on stop
+      for (const Pending &p : pend) {  // only on stop
+        if (stalled.load()) {
+          const uint64_t w = __atomic_load_n(&slot_word[p.slot], __ATOMIC_SEQ_CST);
+          fprintf(stderr, "stuck: page %u slot %u state %llu page-in-slot %u pins %llu page_slot[page] %u\n",
+                  p.page, p.slot, (unsigned long long)sw_state(w), sw_page(w), (unsigned long long)sw_pins(w),
+                  __atomic_load_n(&page_slot[p.page], __ATOMIC_SEQ_CST));
+        }
+        unpin(c, p.slot);
+      }
       done_queries.fetch_add(1);
     }
     (void)t;

@@ -8,7 +8,9 @@ access completed, no page read through a slot that held another page, no pin
 left, no slot left LOADING, a consistent page-to-slot map and no descriptor
 left; the same runs once more under ThreadSanitizer. Two negative controls
 (a read after the unpin; READY published before the page bytes) show that
-the read check catches the mistakes it is there for.
+the read check catches the mistakes it is there for.  Runs with pauses at the
+state machine's pause points (GORIO_SLOT_PAUSE) widen its races; one of them
+is the regression test of a stale lookup joining a slot that was given back.
 
 The first two configurations are the paged search's smallest tested cache:
 128 slots (two query slots per wave, float32 rows of 96 dimensions with R=8,
@@ -37,8 +39,8 @@ def harness(tmp_path_factory):
 
 
 def run(exe, slots, pages, live, pending, queries, accesses, fillers, latency_us, seed, control=0,
-        stall_s=10, timeout=120):
-    args = [slots, pages, live, pending, queries, accesses, fillers, latency_us, seed, stall_s, control]
+        stall_s=10, timeout=120, pause_us=0):
+    args = [slots, pages, live, pending, queries, accesses, fillers, latency_us, seed, stall_s, control, pause_us]
     p = subprocess.run([str(exe), *map(str, args)], capture_output=True, text=True, timeout=timeout)
     assert p.returncode == 0, p.stdout + p.stderr
     # ThreadSanitizer reports on stderr and keeps going; any report fails
@@ -75,10 +77,36 @@ def test_slot_state_machine(harness, name):
     assert r["misses"] > 0 and r["hits"] > 0
 
 
+@pytest.mark.parametrize("seed", [9, 10, 11, 12])
+def test_stale_lookup_never_joins_a_slot_given_back(harness, seed):
+    """A lookup that read a page's slot, then paused while the slot was
+    evicted, claimed again for the same page by a wave that lost the race to
+    map it and was given back unfilled, must not wait on that slot: it joins a
+    LOADING slot only while the page maps to it.  Threads pause at the state
+    machine's pause points (after a lookup, after a claim, before a give-back)
+    to make that interleaving common; without the check every run of this
+    configuration left queries waiting on EMPTY slots for good."""
+    r = run(harness["plain"], 8, 24, 6, 4, 2000, 100, 2, 0.0, seed=seed, stall_s=5, pause_us=100)
+    assert_clean(r)
+
+
+@pytest.mark.parametrize("cfg", [(2, 10, 2, 1, 400, 50, 1), (4, 40, 3, 2, 400, 100, 2), (32, 200, 12, 4, 200, 100, 3)],
+                         ids=["2-slots-1-request", "4-slots", "32-slots-12-queries"])
+def test_slot_state_machine_with_pauses(harness, cfg):
+    slots, pages, live, pending, queries, accesses, fillers = cfg
+    r = run(harness["plain"], slots, pages, live, pending, queries, accesses, fillers, 0.0, seed=21, pause_us=50)
+    assert_clean(r)
+
+
 @pytest.mark.parametrize("name", ["128-slots-2x32-l20", "8-slots"])
 def test_slot_state_machine_tsan(harness, name):
     slots, pages, live, pending, queries, accesses, fillers, lat = CONFIGS[name]
     r = run(harness["tsan"], slots, pages, live, pending, min(queries, 200), accesses, fillers, lat, seed=9)
+    assert_clean(r)
+
+
+def test_slot_state_machine_tsan_with_pauses(harness):
+    r = run(harness["tsan"], 8, 24, 6, 4, 300, 100, 2, 0.0, seed=13, pause_us=100)
     assert_clean(r)
 
 
