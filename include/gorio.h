@@ -47,10 +47,11 @@
  *   - The caller owns every array it passes; the library copies what it keeps.
  *   - One thread at a time per index; no call on an index may overlap a
  *     search on it from another thread.  Searches of one index issued on
- *     different streams run one after another: each search's work waits on
- *     the GPU for the previous search of the index (an event the index
- *     records), because they share the index's counters.  Different indexes
- *     may be used from different threads.
+ *     different streams run one after another: a search on another stream
+ *     than the previous search of the index waits on the GPU for that search
+ *     (an event the index records), because they share the index's counters;
+ *     on the same stream, stream order does it.  Different indexes may be
+ *     used from different threads.
  *   - The device is the HIP device current when gorio_build_index is called;
  *     later calls switch to it and restore the caller's device.
  *
