@@ -60,6 +60,8 @@
  *   GORIO_FILL_WAVES       waves that only copy arriving pages (default 32, at most 64)
  *   GORIO_MAX_PENDING      page requests per query, overriding gorio_set_scheduler's
  *   GORIO_TURN_PASSES      host-scheduled rounds: passes before a lane yields (default 2)
+ *   GORIO_FILL_BUDGET_US   host-scheduled rounds: the fill kernel leaves after this long
+ *                          and is launched again (default 2000)
  *   GORIO_ROUNDS_STATS     1: print the host scheduler's counters to stderr
  *   GORIO_WATCHDOG_S       a paged search still running after this many seconds is
  *                          aborted with GORIO_ETIMEOUT (default 120)

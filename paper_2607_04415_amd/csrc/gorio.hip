@@ -423,13 +423,29 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   }
 
   // fill waves in a kernel of their own, and the second round stream, both
-  // after the control words were reset on s
+  // after the control words were reset on s.  The fill kernel leaves after
+  // about two milliseconds and is launched again (from the ring positions it
+  // published) as soon as it has: no kernel of this mode waits on the GPU
+  // for work of another stream, so progress does not depend on how the
+  // runtime maps streams to hardware queues (streams that share a queue run
+  // one after another).
+  int clock_khz = 0;
+  HIP_OR_FAIL(hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, ix->device));
+  const int budget_us = std::max(50, env_int("GORIO_FILL_BUDGET_US", 2000));
+  pp.fill_budget = (unsigned long long)std::max(1.0, (double)clock_khz * budget_us / 1000.0);
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
   HIP_OR_FAIL(hipStreamWaitEvent(P.fill_stream, ix->ev_start, 0));
   HIP_OR_FAIL(hipStreamWaitEvent(P.round_stream, ix->ev_start, 0));
+  bool fill_busy = false;
+  auto launch_fill = [&]() -> hipError_t {
+    hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, (int)pp.fill_waves, P.fill_stream)
+                                           : launch_paged_u8(pp, (int)pp.fill_waves, P.fill_stream);
+    if (le == hipSuccess) le = hipEventRecord(P.ev_fill, P.fill_stream);
+    fill_busy = le == hipSuccess;
+    return le;
+  };
   {
-    const hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, (int)pp.fill_waves, P.fill_stream)
-                                                 : launch_paged_u8(pp, (int)pp.fill_waves, P.fill_stream);
+    const hipError_t le = launch_fill();
     if (le != hipSuccess) return fail(GORIO_EDEVICE, "fill kernel launch failed: %s", hipGetErrorString(le));
   }
 
@@ -565,6 +581,22 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
       acted = true;
     }
     if (st != GORIO_OK) break;
+    if (fill_busy) {
+      const hipError_t q = hipEventQuery(P.ev_fill);
+      if (q == hipSuccess) {
+        fill_busy = false;
+      } else if (q != hipErrorNotReady) {
+        st = fail(GORIO_EDEVICE, "fill kernel failed: %s", hipGetErrorString(q));
+        break;
+      }
+    }
+    if (!fill_busy) {
+      const hipError_t le = launch_fill();
+      if (le != hipSuccess) {
+        st = fail(GORIO_EDEVICE, "fill kernel launch failed: %s", hipGetErrorString(le));
+        break;
+      }
+    }
     acted |= poll_fills();
     int busy = 0;
     for (int i = 0; i < kFlights; ++i) busy += fl[i].busy ? 1 : 0;
@@ -624,7 +656,7 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
             n_rounds ? (double)n_lane_runs / n_rounds : 0.0, (unsigned long long)n_idle,
             (unsigned long long)n_early, (unsigned long long)n_stale, n_rounds ? round_us / n_rounds : 0.0,
             std::chrono::duration<double>(Clock::now() - t0).count());
-  // the fill waves leave once every query is done (or on abort)
+  // the last fill kernel leaves once every query is done (or on abort)
   HIP_OR_FAIL(hipEventRecord(P.ev_fill, P.fill_stream));
   for (;;) {
     const hipError_t q = hipEventQuery(P.ev_fill);
@@ -740,6 +772,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   }
   pp.done_queries = reinterpret_cast<unsigned int *>(P.ctrl(PagedState::kDoneQueries));
   pp.fill_head = nullptr;
+  pp.fill_budget = 0;  // host rounds set their own
   pp.fill_waves = (uint32_t)fwaves;
   pp.out_ids = rp.out_ids;
   pp.out_dists = rp.out_dists;

@@ -65,7 +65,10 @@ struct PagedParams {
   const uint32_t *order;                  // nullptr: queries in index order; else admission order
   unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
   unsigned long long *fill_head;          // host memory or nullptr: completions of ring k filled so far,
-                                          // at fill_head[k * tail_stride] (host-scheduled rounds)
+                                          // at fill_head[k * tail_stride] (host-scheduled rounds); a
+                                          // fill wave starts from there
+  unsigned long long fill_budget;         // nonzero: a fill wave leaves after this many wall-clock
+                                          // ticks (host-scheduled rounds relaunch it)
   uint32_t *out_ids;
   uint32_t *out_dists;                    // distance bits (int32 or float32)
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
@@ -73,7 +76,7 @@ struct PagedParams {
   uint32_t turn_passes;                   // host rounds: a query yields after this many passes over its
                                           // candidates that found pages ready (0 = no limit)
   int blocking;
-  unsigned long long *stats;              // [eval, reeval, exp, iter, hit, miss, served, park, resume, bad]
+  unsigned long long *stats;              // [eval, reeval, exp, iter, hit, miss, served, park, resume, -, bad]
 };
 
 template <int KPL>
@@ -517,19 +520,28 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
 }
 
 // Fill wave k: consumes completion ring k (its own: no atomics on the ring)
-// and copies the pages until every query is done.  Wave 0 also mirrors the
-// host abort flag.
+// and copies the pages until every query is done, or, with a budget, until
+// the budget has passed (host-scheduled rounds: the host launches the fill
+// waves again, and they go on from the ring position they published, so no
+// kernel of that mode ever waits for another stream's work).  Wave 0 also
+// mirrors the host abort flag.
 __device__ void fill_loop(const PagedParams &p, uint32_t k) {
   const int l = lane_id();
   const unsigned long long *ring = p.cq + (uint64_t)k * (p.cq_mask + 1);
   const unsigned long long *tail = p.cq_tail + (uint64_t)k * p.tail_stride;
-  unsigned long long head = 0, served = 0;
-  uint32_t idle = 0;
   unsigned long long *filled = p.fill_head ? p.fill_head + (uint64_t)k * p.tail_stride : nullptr;
+  unsigned long long head = 0, served = 0;
+  if (filled) {
+    if (l == 0) head = __hip_atomic_load(filled, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    head = readlane64(head, 0);
+  }
+  const unsigned long long t_end = p.fill_budget ? (unsigned long long)wall_clock64() + p.fill_budget : ~0ull;
+  uint32_t idle = 0;
   for (;;) {
     if (k == 0 && l == 0) refresh_abort(p);
     if (aborted(p)) break;
     if (__hip_atomic_load(p.done_queries, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.nq) break;
+    if (p.fill_budget && (unsigned long long)wall_clock64() >= t_end) break;
     unsigned long long t = 0;
     if (l == 0) t = __hip_atomic_load(tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     t = readlane64(t, 0);

@@ -123,6 +123,37 @@ def test_host_rounds_held_proxy_then_recover(torch_dev, small, monkeypatch):
     ix.close()
 
 
+def test_host_rounds_with_many_streams_alive(torch_dev, small, monkeypatch):
+    """Host-scheduled rounds while the process holds many more streams than
+    the device has hardware queues, so streams share queues (and work on a
+    shared queue may run one item after another).  Every kernel of this mode
+    is bounded in time (the fill kernel leaves after a budget and is launched
+    again), so the search finishes, exactly, with the fill kernel relaunched
+    many times."""
+    torch = torch_dev
+    a, q, oids, od, oc = small
+    streams = [torch.cuda.Stream() for _ in range(12)]
+    keep = []
+    for s in streams:   # use every stream once, so each holds its queue
+        with torch.cuda.stream(s):
+            keep.append(torch.ones(1024, device="cuda") * 2)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("GORIO_WATCHDOG_S", "60")
+    ix = g.Index(a["x"], a["graph"], vectors_first=True)
+    ix.set_cache(int(0.10 * ix.info["index_bytes"]))
+    ix.set_backing(latency_us=5.0, mode=HOST)
+    qd = torch.from_numpy(np.ascontiguousarray(q)).cuda()
+    torch.cuda.synchronize()          # the queries are in place before another stream reads them
+    for s in (streams[3], streams[7]):
+        ids, dists, st = ix.search(qd, 10, 32, 4, stream=s.cuda_stream)
+        torch.cuda.synchronize()
+        assert_same(ids.cpu().numpy().view(np.uint32), dists.cpu().numpy(), oids, od)
+        assert st["expansions"] == int(oc["expansions"].sum())
+        assert st["pages_served"] > 0
+    ix.close()
+    assert all(float(k.sum()) == 2048.0 for k in keep)
+
+
 def test_host_rounds_1m_bench_configuration(orc, torch_dev):
     """The 1M uint8 index, 10% cold cache, 0 us, all 10,000 queries, in the
     benchmark's launch configuration for the host-scheduled leg (vectors-first
