@@ -62,6 +62,8 @@
  *   GORIO_TURN_PASSES      host-scheduled rounds: passes before a lane yields (default 2)
  *   GORIO_FILL_BUDGET_US   host-scheduled rounds: the fill kernel leaves after this long
  *                          and is launched again (default 2000)
+ *   GORIO_ROUND_FLIGHTS    host-scheduled rounds: round kernels in flight, each on a
+ *                          stream of its own (default 2, at most 8)
  *   GORIO_ROUNDS_STATS     1: print the host scheduler's counters to stderr
  *   GORIO_WATCHDOG_S       a paged search still running after this many seconds is
  *                          aborted with GORIO_ETIMEOUT (default 120)

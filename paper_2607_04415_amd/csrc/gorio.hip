@@ -378,7 +378,9 @@ namespace {
 gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, const std::vector<uint32_t> &order,
                              hipStream_t s, double limit_s, bool &timed_out) {
   using Clock = std::chrono::steady_clock;
-  constexpr int kFlights = 2;  // round kernels in flight at once
+  constexpr int kMaxFlights = PagedState::kMaxFlights;
+  // round kernels in flight at once (each on a stream of its own)
+  const int flights = std::max(1, std::min(kMaxFlights, env_int("GORIO_ROUND_FLIGHTS", 2)));
   PagedState &P = *ix->paged;
   const uint32_t words = lane_state_words(pp.L);
   if ((uint64_t)lanes * words > P.lane_state_words) {
@@ -394,25 +396,27 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     P.h_round = P.d_round = nullptr;
     P.h_lane_out = P.d_lane_out = nullptr;
     P.round_cap = 0;
-    HIP_OR_FAIL(host_ring(&P.h_round, &P.d_round, 2 * kFlights * (size_t)lanes));
+    HIP_OR_FAIL(host_ring(&P.h_round, &P.d_round, 2 * kMaxFlights * (size_t)lanes));
     HIP_OR_FAIL(host_ring(&P.h_lane_out, &P.d_lane_out, lanes));
     P.round_cap = lanes;
   }
   if (!P.h_fill_head)
     HIP_OR_FAIL(host_ring(&P.h_fill_head, &P.d_fill_head, (size_t)PagedState::kMaxRings * PagedState::kTailStride));
   if (!P.fill_stream) HIP_OR_FAIL(hipStreamCreateWithFlags(&P.fill_stream, hipStreamNonBlocking));
-  if (!P.round_stream) HIP_OR_FAIL(hipStreamCreateWithFlags(&P.round_stream, hipStreamNonBlocking));
-  for (int i = 0; i < kFlights; ++i)
+  for (int i = 1; i < flights; ++i)
+    if (!P.round_stream[i]) HIP_OR_FAIL(hipStreamCreateWithFlags(&P.round_stream[i], hipStreamNonBlocking));
+  for (int i = 0; i < flights; ++i)
     if (!P.ev_round[i]) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_round[i], hipEventDisableTiming));
   if (!P.ev_fill) HIP_OR_FAIL(hipEventCreateWithFlags(&P.ev_fill, hipEventDisableTiming));
   const uint32_t rings = std::max(1u, pp.fill_waves);
   for (uint32_t r = 0; r < rings; ++r)
     __atomic_store_n(P.h_fill_head + (size_t)r * PagedState::kTailStride, 0ull, __ATOMIC_RELEASE);
   pp.fill_head = P.d_fill_head;
-  const hipStream_t rstream[kFlights] = {s, P.round_stream};
-  RoundParams rp[kFlights];
-  uint32_t *h_lanes[kFlights], *h_admit[kFlights];
-  for (int i = 0; i < kFlights; ++i) {
+  hipStream_t rstream[kMaxFlights];
+  RoundParams rp[kMaxFlights];
+  uint32_t *h_lanes[kMaxFlights], *h_admit[kMaxFlights];
+  for (int i = 0; i < flights; ++i) {
+    rstream[i] = i == 0 ? s : P.round_stream[i];
     rp[i].lanes = P.d_round + (size_t)2 * i * lanes;
     rp[i].admit = P.d_round + (size_t)(2 * i + 1) * lanes;
     rp[i].state = P.d_lane_state;
@@ -435,7 +439,7 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   pp.fill_budget = (unsigned long long)std::max(1.0, (double)clock_khz * budget_us / 1000.0);
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
   HIP_OR_FAIL(hipStreamWaitEvent(P.fill_stream, ix->ev_start, 0));
-  HIP_OR_FAIL(hipStreamWaitEvent(P.round_stream, ix->ev_start, 0));
+  for (int i = 1; i < flights; ++i) HIP_OR_FAIL(hipStreamWaitEvent(P.round_stream[i], ix->ev_start, 0));
   bool fill_busy = false;
   auto launch_fill = [&]() -> hipError_t {
     hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, (int)pp.fill_waves, P.fill_stream)
@@ -500,9 +504,16 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   struct Flight {
     bool busy = false;
     uint32_t n = 0;
-    uint64_t seq = 0;  // fill_seq at launch
     Clock::time_point t0;
-  } fl[kFlights];
+  } fl[kMaxFlights];
+  // A lane is retired as soon as its report says its turn is over (the
+  // sequence number it publishes last), not when its launch ends: a round
+  // lasts as long as its slowest lane, and the others go on meanwhile.
+  std::vector<uint64_t> lane_fill_seq(lanes, 0);  // fill_seq when the lane's round was launched
+  std::vector<uint32_t> out_seq(lanes);           // the last sequence number seen per lane
+  for (uint32_t l = 0; l < lanes; ++l) out_seq[l] = __atomic_load_n(&P.h_lane_out[l].seq, __ATOMIC_ACQUIRE);
+  std::vector<uint32_t> running;
+  running.reserve(lanes);
 
   const auto t0 = Clock::now();
   auto last_sweep = t0;
@@ -511,46 +522,59 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   // scheduler counters (printed to stderr with GORIO_ROUNDS_STATS=1)
   uint64_t n_rounds = 0, n_lane_runs = 0, n_idle = 0, n_stale = 0, n_early = 0;
   double round_us = 0.0;
-  const uint32_t min_round = std::max(1u, lanes / 8);
+  const uint32_t min_round = std::max(1u, lanes / (4u * (uint32_t)flights));
   gorio_status st = GORIO_OK;
-  auto retire = [&](int i) {
+  // the lane's turn is over: act on its report
+  auto retire_lane = [&](uint32_t lane, Clock::time_point done_at) {
+    ++n_lane_runs;
+    const LaneOut &o = P.h_lane_out[lane];
+    if (o.code == kLaneIdle) ++n_idle;
+    if (o.code == kLaneDone) {
+      ++finished;
+      lstate[lane] = kFree;
+      freeq.push_back(lane);
+      return;
+    }
+    const uint32_t ep = ++epoch[lane];
+    bool now = o.code == kLaneYield;  // its turn ended while it could still proceed
+    const uint32_t nw = std::min(o.nwait, kLaneWaitCap);
+    for (uint32_t j = 0; j < nw && !now; ++j) {
+      const uint32_t w = o.wait[j];
+      if (w >= P.slots) continue;
+      if (slot_seq[w] > lane_fill_seq[lane]) now = true;  // filled while the lane ran
+      else waiters[w].push_back({lane, ep});
+    }
+    if (!now && (o.retry || nw == 0)) {
+      if (fill_seq > lane_fill_seq[lane]) now = true;
+      else any_fill.push_back({lane, ep});
+    }
+    if (now) {
+      if (o.code != kLaneYield) ++n_early;
+      lstate[lane] = kRunnable;
+      runq.push_back(lane);
+    } else {
+      lstate[lane] = kWaiting;
+      since[lane] = done_at;
+    }
+  };
+  // lanes whose turn is over, whatever their launch is doing
+  auto reap = [&]() {
+    bool any = false;
     const auto done_at = Clock::now();
-    ++n_rounds;
-    n_lane_runs += fl[i].n;
-    round_us += std::chrono::duration<double, std::micro>(done_at - fl[i].t0).count();
-    for (uint32_t k = 0; k < fl[i].n; ++k) {
-      const uint32_t lane = h_lanes[i][k];
-      const LaneOut &o = P.h_lane_out[lane];
-      if (o.code == kLaneIdle) ++n_idle;
-      if (o.code == kLaneDone) {
-        ++finished;
-        lstate[lane] = kFree;
-        freeq.push_back(lane);
+    for (size_t k = 0; k < running.size();) {
+      const uint32_t lane = running[k];
+      const uint32_t sq = __atomic_load_n(&P.h_lane_out[lane].seq, __ATOMIC_ACQUIRE);
+      if (sq == out_seq[lane]) {
+        ++k;
         continue;
       }
-      const uint32_t ep = ++epoch[lane];
-      bool now = o.code == kLaneYield;  // its turn ended while it could still proceed
-      const uint32_t nw = std::min(o.nwait, kLaneWaitCap);
-      for (uint32_t j = 0; j < nw && !now; ++j) {
-        const uint32_t w = o.wait[j];
-        if (w >= P.slots) continue;
-        if (slot_seq[w] > fl[i].seq) now = true;  // filled while the round ran
-        else waiters[w].push_back({lane, ep});
-      }
-      if (!now && (o.retry || nw == 0)) {
-        if (fill_seq > fl[i].seq) now = true;
-        else any_fill.push_back({lane, ep});
-      }
-      if (now) {
-        if (o.code != kLaneYield) ++n_early;
-        lstate[lane] = kRunnable;
-        runq.push_back(lane);
-      } else {
-        lstate[lane] = kWaiting;
-        since[lane] = done_at;
-      }
+      out_seq[lane] = sq;
+      running[k] = running.back();
+      running.pop_back();
+      retire_lane(lane, done_at);
+      any = true;
     }
-    fl[i].busy = false;
+    return any;
   };
 
   while (finished < nq) {
@@ -568,8 +592,8 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
           ++n_stale;
         }
     }
-    bool acted = false;
-    for (int i = 0; i < kFlights; ++i) {
+    bool acted = reap();
+    for (int i = 0; i < flights; ++i) {
       if (!fl[i].busy) continue;
       const hipError_t q = hipEventQuery(P.ev_round[i]);
       if (q == hipErrorNotReady) continue;
@@ -577,7 +601,11 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
         st = fail(GORIO_EDEVICE, "round failed: %s", hipGetErrorString(q));
         break;
       }
-      retire(i);
+      // the launch is over (its lanes reported before it ended): its stream
+      // and lane list are free again
+      ++n_rounds;
+      round_us += std::chrono::duration<double, std::micro>(Clock::now() - fl[i].t0).count();
+      fl[i].busy = false;
       acted = true;
     }
     if (st != GORIO_OK) break;
@@ -599,8 +627,8 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     }
     acted |= poll_fills();
     int busy = 0;
-    for (int i = 0; i < kFlights; ++i) busy += fl[i].busy ? 1 : 0;
-    for (int i = 0; i < kFlights; ++i) {
+    for (int i = 0; i < flights; ++i) busy += fl[i].busy ? 1 : 0;
+    for (int i = 0; i < flights; ++i) {
       if (fl[i].busy) continue;
       const uint64_t avail = runq.size() + std::min<uint64_t>(freeq.size(), nq - admitted);
       // with another round running, wait for a worthwhile number of lanes
@@ -622,8 +650,11 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
         ++admitted;
         ++n;
       }
+      for (uint32_t k = 0; k < n; ++k) {
+        lane_fill_seq[h_lanes[i][k]] = fill_seq;
+        running.push_back(h_lanes[i][k]);
+      }
       fl[i].t0 = Clock::now();
-      fl[i].seq = fill_seq;
       const hipError_t le = ix->dtype == GORIO_F32 ? launch_rounds_f32(pp, rp[i], (int)n, rstream[i])
                                                    : launch_rounds_u8(pp, rp[i], (int)n, rstream[i]);
       if (le != hipSuccess) {
@@ -647,7 +678,7 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   if (st != GORIO_OK || timed_out) __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
   // rounds still in flight (after an error or the watchdog) finish: every lane
   // turn is bounded and stops at once on the abort flag
-  for (int i = 0; i < kFlights; ++i)
+  for (int i = 0; i < flights; ++i)
     if (fl[i].busy) (void)hipEventSynchronize(P.ev_round[i]);
   if (env_int("GORIO_ROUNDS_STATS", 0))
     fprintf(stderr, "[gorio rounds] lanes %u, rounds %llu, lane runs %llu (%.1f per round, %llu not runnable), "
@@ -669,8 +700,10 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     std::this_thread::sleep_for(std::chrono::microseconds(50));
   }
   HIP_OR_FAIL(hipStreamWaitEvent(s, P.ev_fill, 0));
-  HIP_OR_FAIL(hipEventRecord(P.ev_round[1], P.round_stream));
-  HIP_OR_FAIL(hipStreamWaitEvent(s, P.ev_round[1], 0));
+  for (int i = 1; i < flights; ++i) {
+    HIP_OR_FAIL(hipEventRecord(P.ev_round[i], P.round_stream[i]));
+    HIP_OR_FAIL(hipStreamWaitEvent(s, P.ev_round[i], 0));
+  }
   HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
   return st;
 }

@@ -58,8 +58,11 @@ struct PagedState {
   // host-scheduled rounds: lane states (HBM), the round's lane list and the
   // lanes' reports (host memory the kernels read and write), and how far each
   // completion ring has been filled (written by the fill waves)
-  hipStream_t fill_stream = nullptr, round_stream = nullptr;
-  hipEvent_t ev_round[2] = {nullptr, nullptr}, ev_fill = nullptr;
+  // round kernels in flight at once: flight 0 on the search's stream, flight
+  // i > 0 on round_stream[i]
+  static constexpr int kMaxFlights = 8;
+  hipStream_t fill_stream = nullptr, round_stream[kMaxFlights] = {};
+  hipEvent_t ev_round[kMaxFlights] = {}, ev_fill = nullptr;
   uint32_t *d_lane_state = nullptr;
   uint64_t lane_state_words = 0;
   uint32_t *h_round = nullptr, *d_round = nullptr;   // 2 x round_cap: lanes, then admissions
@@ -87,7 +90,8 @@ struct PagedState {
     if (h_lane_out) (void)hipHostFree(h_lane_out);
     if (h_fill_head) (void)hipHostFree(h_fill_head);
     if (fill_stream) (void)hipStreamDestroy(fill_stream);
-    if (round_stream) (void)hipStreamDestroy(round_stream);
+    for (hipStream_t &r : round_stream)
+      if (r) (void)hipStreamDestroy(r);
     for (hipEvent_t &e : ev_round)
       if (e) (void)hipEventDestroy(e);
     if (ev_fill) (void)hipEventDestroy(ev_fill);
@@ -107,8 +111,11 @@ struct PagedState {
     h_lane_out = d_lane_out = nullptr;
     h_fill_head = d_fill_head = nullptr;
     fill_stream = nullptr;
-    round_stream = nullptr;
-    ev_round[0] = ev_round[1] = ev_fill = nullptr;
+    for (int i = 0; i < kMaxFlights; ++i) {
+      round_stream[i] = nullptr;
+      ev_round[i] = nullptr;
+    }
+    ev_fill = nullptr;
     h_mq = d_mq = h_cq = d_cq = h_cq_tail = d_cq_tail = nullptr;
     h_abort = d_abort = nullptr;
     slots = 0;

@@ -669,6 +669,9 @@ struct LaneOut {
   uint32_t retry;                // 1: can proceed without one of wait[] arriving (requests it could
                                  // not issue for want of a free slot, or more waits than wait[] holds)
   uint32_t qi;                   // the lane's query
+  uint32_t seq;                  // turns the lane has finished; written last, with a system-scope
+                                 // release, so a new value means the report and the lane's state
+                                 // in HBM are complete (the host need not wait for the launch)
   uint32_t wait[kLaneWaitCap];   // cache slots of the pages the lane waits for
 };
 
@@ -723,12 +726,21 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
   uint32_t *ht = p.ht_pool + ((uint64_t)lane << kPagedHtLog2);
   uint32_t *st = r.state + (uint64_t)lane * r.state_words;
   LaneOut &o = r.out[lane];
+  uint32_t seq0 = 0;
+  if (l == 0) seq0 = __hip_atomic_load(&o.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  // the turn is over: everything this wave wrote (the lane's state in HBM,
+  // its report in host memory, the counters) is performed before the new
+  // sequence number can be seen
+  auto finish_turn = [&]() {
+    if (l == 0) __hip_atomic_store(&o.seq, seq0 + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+  };
   if (aborted(p)) {
     if (l == 0) {
       o.code = kLaneIdle;
       o.nwait = 0;
       o.retry = 1;
     }
+    finish_turn();
     return;
   }
   PagedCounters ctr;
@@ -739,6 +751,7 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
     __syncthreads();
     if (!query_runnable(p, S)) {
       report_waits(p, S, o, kLaneIdle);
+      finish_turn();
       return;
     }
     ++ctr.resume;
@@ -768,6 +781,7 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
     if (ctr.park) atomicAdd(&p.stats[7], ctr.park);
     if (ctr.resume) atomicAdd(&p.stats[8], ctr.resume);
   }
+  finish_turn();
 }
 
 }  // namespace gorio

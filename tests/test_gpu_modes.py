@@ -90,6 +90,24 @@ def test_host_rounds_match_oracle(torch_dev, small, monkeypatch, frac, latency, 
     ix.close()
 
 
+@pytest.mark.parametrize("flights,lanes", [("4", 0), ("8", 12)])
+def test_host_rounds_more_flights(torch_dev, small, monkeypatch, flights, lanes):
+    """Several round kernels in flight on streams of their own, lanes retired
+    one by one as their reports arrive and launched again on whichever
+    stream is free: the answers and counts stay the oracle's."""
+    a, q, oids, od, oc = small
+    monkeypatch.setenv("GORIO_ROUND_FLIGHTS", flights)
+    ix = g.Index(a["x"], a["graph"], vectors_first=True)
+    ix.set_cache(int(0.10 * ix.info["index_bytes"]))
+    ix.set_backing(latency_us=5.0, mode=HOST)
+    ix.set_scheduler(query_waves=lanes)
+    gi, gd, st = search(torch_dev, ix, q, 10, 32, 4)
+    assert_same(gi, gd, oids, od)
+    assert st["expansions"] == int(oc["expansions"].sum())
+    assert st["iterations"] == int(oc["iterations"].sum())
+    ix.close()
+
+
 def test_host_rounds_f32_clusters(orc, torch_dev, small_f32):
     """float32 rows, cluster placement and cluster-ordered admission, host rounds."""
     a, q, oids, od, oc = small_f32
