@@ -52,6 +52,9 @@ MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
 # The 100k-query 20 us configuration asks for 4 query slots per wave: 30 waves gave 8,512
 # against 8,351 for the default 39.
 SHAPE_C3 = {"oversub": 1, "query_waves": 30}
+# host-scheduled lanes (persistent executor, turns until a lane parks): 30 / 40 / 50 / 60 /
+# 100 / 156 (the default) lanes gave 7.0k / 7.25k / 7.2k / 7.05k / 6.6k / 6.0k queries/s
+SHAPE_HOST = {"query_waves": 40}
 SHAPE_C4 = {"oversub": 4, "query_waves": 30}
 SHAPE_C5 = {"oversub": 1, "query_waves": 60}
 # The paper's own figures (Table 2: 10,000 SIFT1M queries over NVMe-oF on one NVIDIA L40S,
@@ -498,11 +501,11 @@ def main():
         n3 = w3.queries.nq if args.paged_sample < 0 else min(args.paged_sample, w3.queries.nq)
         # C3 legs: split-phase and blocking in the same shape (one query per wave),
         # the identity placement, the default shape (as many queries as the pins
-        # allow, 4 per wave), host-scheduled rounds (lanes: the default)
+        # allow, 4 per wave), host-scheduled lanes (40)
         plan = [(0, clustered, "split-phase", SHAPE_C3), (1, clustered, "blocking", SHAPE_C3),
                 (0, False, "split-phase, identity placement", SHAPE_C3),
                 (0, clustered, "split-phase, default shape", {}),
-                (2, clustered, "host-scheduled", {})]
+                (2, clustered, "host-scheduled", SHAPE_HOST)]
         for mode, use_cl, label, shape in plan:
             if use_cl is False and not clustered and label.endswith("identity placement"):
                 continue

@@ -59,11 +59,14 @@
  * for normal use):
  *   GORIO_FILL_WAVES       waves that only copy arriving pages (default 32, at most 64)
  *   GORIO_MAX_PENDING      page requests per query, overriding gorio_set_scheduler's
- *   GORIO_TURN_PASSES      host-scheduled rounds: passes before a lane yields (default 2)
- *   GORIO_FILL_BUDGET_US   host-scheduled rounds: the fill kernel leaves after this long
- *                          and is launched again (default 2000)
- *   GORIO_ROUND_FLIGHTS    host-scheduled rounds: round kernels in flight, each on a
- *                          stream of its own (default 2, at most 8)
+ *   GORIO_HOST_EXECUTOR    host-scheduled lanes: 1 (default) = one persistent launch runs
+ *                          the turns the host writes to a ring; 0 = a launch per round
+ *   GORIO_TURN_PASSES      host-scheduled lanes: passes that found pages ready before a lane
+ *                          yields (default: none with the executor, 2 with a launch per round)
+ *   GORIO_FILL_BUDGET_US   launch per round: the fill kernel leaves after this long and is
+ *                          launched again (default 2000)
+ *   GORIO_ROUND_FLIGHTS    launch per round: round kernels in flight, each on a stream of
+ *                          its own (default 2, at most 8)
  *   GORIO_ROUNDS_STATS     1: print the host scheduler's counters to stderr
  *   GORIO_WATCHDOG_S       a paged search still running after this many seconds is
  *                          aborted with GORIO_ETIMEOUT (default 120)

@@ -381,6 +381,12 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   constexpr int kMaxFlights = PagedState::kMaxFlights;
   // round kernels in flight at once (each on a stream of its own)
   const int flights = std::max(1, std::min(kMaxFlights, env_int("GORIO_ROUND_FLIGHTS", 2)));
+  // the lanes' turns are run by one persistent launch that takes them from a
+  // ring the host writes (the default), or by a launch per round
+  const bool executor = env_int("GORIO_HOST_EXECUTOR", 1) != 0;
+  // a turn ends when the lane parks; a launch per round also ends it after two
+  // passes that found pages ready, since the round waits for its slowest lane
+  pp.turn_passes = (uint32_t)std::max(0, env_int("GORIO_TURN_PASSES", executor ? 0 : 2));
   PagedState &P = *ix->paged;
   const uint32_t words = lane_state_words(pp.L);
   if ((uint64_t)lanes * words > P.lane_state_words) {
@@ -413,7 +419,7 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     __atomic_store_n(P.h_fill_head + (size_t)r * PagedState::kTailStride, 0ull, __ATOMIC_RELEASE);
   pp.fill_head = P.d_fill_head;
   hipStream_t rstream[kMaxFlights];
-  RoundParams rp[kMaxFlights];
+  RoundParams rp[kMaxFlights] = {};
   uint32_t *h_lanes[kMaxFlights], *h_admit[kMaxFlights];
   for (int i = 0; i < flights; ++i) {
     rstream[i] = i == 0 ? s : P.round_stream[i];
@@ -440,6 +446,46 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
   HIP_OR_FAIL(hipStreamWaitEvent(P.fill_stream, ix->ev_start, 0));
   for (int i = 1; i < flights; ++i) HIP_OR_FAIL(hipStreamWaitEvent(P.round_stream[i], ix->ev_start, 0));
+  // persistent launch: fill waves and executor waves in one kernel on s
+  uint64_t runq_tail = 0;
+  if (executor) {
+    uint32_t cap = 1;
+    while (cap < 2 * lanes + 64) cap <<= 1;
+    if (cap > P.runq_cap) {
+      if (P.h_runq) (void)hipHostFree(P.h_runq);
+      P.h_runq = P.d_runq = nullptr;
+      P.runq_cap = 0;
+      HIP_OR_FAIL(host_ring(&P.h_runq, &P.d_runq, cap));
+      P.runq_cap = cap;
+    }
+    if (!P.h_runq_ctl) HIP_OR_FAIL(host_ring(&P.h_runq_ctl, &P.d_runq_ctl, (size_t)PagedState::kTailStride));
+    memset(P.h_runq, 0, P.runq_cap * sizeof(unsigned long long));
+    __atomic_store_n(P.h_runq_ctl, 0ull, __ATOMIC_RELEASE);
+    RoundParams rx = {};
+    rx.state = P.d_lane_state;
+    rx.state_words = words;
+    rx.out = P.d_lane_out;
+    rx.runq = P.d_runq;
+    rx.runq_tail = P.d_runq_ctl;
+    rx.runq_head = P.ctrl(PagedState::kNextQuery);  // zeroed with the other control words
+    rx.runq_tail_seen = P.ctrl(PagedState::kRunqTailSeen);
+    rx.runq_mask = P.runq_cap - 1;
+    rx.out_lanes = lanes;
+    int cus = 0;
+    HIP_OR_FAIL(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ix->device));
+    const int execs = (int)std::min<uint64_t>(lanes, (uint64_t)cus * 4);
+    pp.fill_budget = 0;  // the fill waves stay until every query is done
+    const int grid = (int)pp.fill_waves + 1 + execs;  // fill waves, the tail mirror, executors
+    const hipError_t le = ix->dtype == GORIO_F32 ? launch_rounds_f32(pp, rx, grid, s)
+                                                 : launch_rounds_u8(pp, rx, grid, s);
+    if (le != hipSuccess) return fail(GORIO_EDEVICE, "executor launch failed: %s", hipGetErrorString(le));
+    HIP_OR_FAIL(hipEventRecord(P.ev_round[0], s));
+  }
+  auto push_lane = [&](uint32_t lane, uint32_t q) {  // q = kNone: go on with the lane's query
+    const unsigned long long e = ((unsigned long long)(q == kNone ? 0u : q + 1u) << 32) | (lane + 1u);
+    __atomic_store_n(&P.h_runq[runq_tail & (P.runq_cap - 1)], e, __ATOMIC_RELAXED);
+    ++runq_tail;
+  };
   bool fill_busy = false;
   auto launch_fill = [&]() -> hipError_t {
     hipError_t le = ix->dtype == GORIO_F32 ? launch_paged_f32(pp, (int)pp.fill_waves, P.fill_stream)
@@ -448,7 +494,7 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     fill_busy = le == hipSuccess;
     return le;
   };
-  {
+  if (!executor) {
     const hipError_t le = launch_fill();
     if (le != hipSuccess) return fail(GORIO_EDEVICE, "fill kernel launch failed: %s", hipGetErrorString(le));
   }
@@ -593,6 +639,45 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
         }
     }
     bool acted = reap();
+    if (executor) {
+      const hipError_t q = hipEventQuery(P.ev_round[0]);
+      if (q != hipErrorNotReady) {
+        // the launch leaves once every query is done, possibly before the
+        // last reports were read here
+        if (q == hipSuccess) {
+          reap();
+          if (finished >= nq) break;
+        }
+        st = fail(GORIO_EDEVICE, "executor launch ended with %llu of %llu queries done%s%s",
+                  (unsigned long long)finished, (unsigned long long)nq, q == hipSuccess ? "" : ": ",
+                  q == hipSuccess ? "" : hipGetErrorString(q));
+        break;
+      }
+      acted |= poll_fills();
+      if (!runq.empty() || (!freeq.empty() && admitted < nq)) {
+        for (uint32_t lane : runq) {
+          lstate[lane] = kRunning;
+          lane_fill_seq[lane] = fill_seq;
+          running.push_back(lane);
+          push_lane(lane, kNone);
+        }
+        runq.clear();
+        while (!freeq.empty() && admitted < nq) {
+          const uint32_t lane = freeq.back();
+          freeq.pop_back();
+          lstate[lane] = kRunning;
+          lane_fill_seq[lane] = fill_seq;
+          running.push_back(lane);
+          push_lane(lane, order.empty() ? (uint32_t)admitted : order[admitted]);
+          ++admitted;
+        }
+        __atomic_store_n(P.h_runq_ctl, (unsigned long long)runq_tail, __ATOMIC_RELEASE);
+        acted = true;
+      }
+      if (!acted)
+        for (int i = 0; i < 16; ++i) GORIO_CPU_PAUSE();
+      continue;
+    }
     for (int i = 0; i < flights; ++i) {
       if (!fl[i].busy) continue;
       const hipError_t q = hipEventQuery(P.ev_round[i]);
@@ -676,6 +761,26 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
       for (int i = 0; i < 16; ++i) GORIO_CPU_PAUSE();
   }
   if (st != GORIO_OK || timed_out) __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+  if (executor) {
+    // every wave of the launch leaves once every query is done (or on abort)
+    for (;;) {
+      const hipError_t q = hipEventQuery(P.ev_round[0]);
+      if (q == hipSuccess) break;
+      if (q != hipErrorNotReady) return fail(GORIO_EDEVICE, "executor launch failed: %s", hipGetErrorString(q));
+      if (!timed_out && std::chrono::duration<double>(Clock::now() - t0).count() > limit_s) {
+        timed_out = true;
+        __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      }
+      std::this_thread::sleep_for(std::chrono::microseconds(50));
+    }
+    if (env_int("GORIO_ROUNDS_STATS", 0))
+      fprintf(stderr, "[gorio rounds] lanes %u, executor, lane turns %llu (%llu not runnable), woken at report %llu, "
+              "stale wakes %llu, %.3f s in all\n", lanes, (unsigned long long)n_lane_runs,
+              (unsigned long long)n_idle, (unsigned long long)n_early, (unsigned long long)n_stale,
+              std::chrono::duration<double>(Clock::now() - t0).count());
+    HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+    return st;
+  }
   // rounds still in flight (after an error or the watchdog) finish: every lane
   // turn is bounded and stops at once on the abort flag
   for (int i = 0; i < flights; ++i)
@@ -813,7 +918,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   pp.oversub = oversub;
   pp.max_pending = max_pending;
   pp.blocking = blocking ? 1 : 0;
-  pp.turn_passes = host_rounds ? (uint32_t)std::max(0, env_int("GORIO_TURN_PASSES", 2)) : 0u;
+  pp.turn_passes = 0;  // host rounds set their own
   pp.stats = rp.stats;
 
   // test hooks: random extra delay per request (completions leave out of

@@ -39,8 +39,9 @@ struct PagedState {
   unsigned long long *d_slot_word = nullptr;  // slots
   uint32_t *d_page_slot = nullptr;            // num_pages
   // device control words (one allocation): clock hand, descriptor tail, shared
-  // completion head and tail mirror, poll lock, abort mirror, next query,
-  // finished queries
+  // completion head and tail mirror, poll lock, abort mirror, next query (or,
+  // for host-scheduled lanes, run-ring entries taken), finished queries,
+  // run-ring tail mirror
   unsigned long long *d_ctrl = nullptr;
   // host rings (coherent pinned memory) and their device-visible addresses
   unsigned long long *h_mq = nullptr, *d_mq = nullptr;
@@ -69,9 +70,17 @@ struct PagedState {
   uint32_t round_cap = 0;
   LaneOut *h_lane_out = nullptr, *d_lane_out = nullptr;
   unsigned long long *h_fill_head = nullptr, *d_fill_head = nullptr;
+  // host-scheduled lanes run by a persistent launch: the run ring the host
+  // writes and the kernel reads, and its tail (entries written)
+  unsigned long long *h_runq = nullptr, *d_runq = nullptr;
+  uint32_t runq_cap = 0;
+  unsigned long long *h_runq_ctl = nullptr, *d_runq_ctl = nullptr;
   Proxy proxy;
 
-  enum Ctrl { kClock = 0, kMqTail, kCqHead, kTailSeen, kPollLock, kAbortSeen, kNextQuery, kDoneQueries, kCtrlWords = 8 };
+  enum Ctrl {
+    kClock = 0, kMqTail, kCqHead, kTailSeen, kPollLock, kAbortSeen, kNextQuery, kDoneQueries, kRunqTailSeen,
+    kCtrlWords = 9
+  };
   // each control word on its own 256-byte line: they are hot atomics of
   // different waves and must not serialize on one L2 channel
   static constexpr uint32_t kCtrlStride = 32;  // u64 words
@@ -89,6 +98,8 @@ struct PagedState {
     if (h_round) (void)hipHostFree(h_round);
     if (h_lane_out) (void)hipHostFree(h_lane_out);
     if (h_fill_head) (void)hipHostFree(h_fill_head);
+    if (h_runq) (void)hipHostFree(h_runq);
+    if (h_runq_ctl) (void)hipHostFree(h_runq_ctl);
     if (fill_stream) (void)hipStreamDestroy(fill_stream);
     for (hipStream_t &r : round_stream)
       if (r) (void)hipStreamDestroy(r);
@@ -110,6 +121,9 @@ struct PagedState {
     round_cap = 0;
     h_lane_out = d_lane_out = nullptr;
     h_fill_head = d_fill_head = nullptr;
+    h_runq = d_runq = nullptr;
+    runq_cap = 0;
+    h_runq_ctl = d_runq_ctl = nullptr;
     fill_stream = nullptr;
     for (int i = 0; i < kMaxFlights; ++i) {
       round_stream[i] = nullptr;

@@ -676,11 +676,22 @@ struct LaneOut {
 };
 
 struct RoundParams {
-  const uint32_t *lanes;   // this launch's lanes, one per workgroup (host memory)
+  const uint32_t *lanes;   // this launch's lanes, one per workgroup (host memory); nullptr: a
+                           // persistent launch that takes its lanes from the run ring below
   const uint32_t *admit;   // per entry: query to start in the lane, or kNone to resume it
   uint32_t *state;         // per lane: its QSlot, state_words 32-bit words (HBM)
   uint32_t state_words;
   LaneOut *out;            // per lane (host memory)
+  // persistent launch: blocks [0, fill_waves) fill pages, block fill_waves
+  // mirrors the run ring's tail into device memory (so that idle waves poll
+  // HBM, not the host link), the others run lane turns in the order the host
+  // writes them to the run ring
+  const unsigned long long *runq;       // host memory: (query + 1) << 32 | (lane + 1), query 0 = resume
+  const unsigned long long *runq_tail;  // host memory: entries written
+  unsigned long long *runq_tail_seen;   // device: its mirror
+  unsigned long long *runq_head;        // device: entries taken
+  uint32_t runq_mask;
+  uint32_t out_lanes;                   // lanes (bounds the ring's lane ids)
 };
 
 // Record which cache slots a parked lane waits for.
@@ -714,15 +725,15 @@ __device__ __forceinline__ void report_waits(const PagedParams &p, const QSlot<K
   }
 }
 
+// One turn of lane `lane` (a new query qa, or kNone to go on with the one
+// it holds): load its state, run until it parks, yields or finishes, store
+// the state and report.
 template <int KPL, class M, bool N2S>
-__global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams r) {
-  extern __shared__ __align__(16) unsigned char lds[];
-  __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
+__device__ void lane_turn(const PagedParams &p, const RoundParams &r, uint32_t lane, uint32_t qa,
+                          unsigned char *lds, uint32_t *qbuf) {
   QSlot<KPL> &S = *reinterpret_cast<QSlot<KPL> *>(lds);
   uint32_t *sw = reinterpret_cast<uint32_t *>(lds);
   const int l = lane_id();
-  const uint32_t lane = r.lanes[blockIdx.x];
-  const uint32_t qa = r.admit[blockIdx.x];
   uint32_t *ht = p.ht_pool + ((uint64_t)lane << kPagedHtLog2);
   uint32_t *st = r.state + (uint64_t)lane * r.state_words;
   LaneOut &o = r.out[lane];
@@ -782,6 +793,77 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
     if (ctr.resume) atomicAdd(&p.stats[8], ctr.resume);
   }
   finish_turn();
+}
+
+template <int KPL, class M, bool N2S>
+__global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams r) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
+  if (r.lanes) {  // one lane per workgroup
+    lane_turn<KPL, M, N2S>(p, r, r.lanes[blockIdx.x], r.admit[blockIdx.x], lds, qbuf);
+    return;
+  }
+  if (blockIdx.x < p.fill_waves) {
+    fill_loop(p, blockIdx.x);
+    return;
+  }
+  const int l = lane_id();
+  auto all_done = [&]() {
+    return __hip_atomic_load(p.done_queries, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.nq;
+  };
+  uint32_t idle = 0;
+  if (blockIdx.x == p.fill_waves) {  // the tail mirror
+    unsigned long long seen = 0;
+    while (!aborted(p) && !all_done()) {
+      unsigned long long t = 0;
+      if (l == 0) t = __hip_atomic_load(r.runq_tail, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+      t = readlane64(t, 0);
+      if (t != seen) {
+        if (l == 0) __hip_atomic_store(r.runq_tail_seen, t, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        seen = t;
+        idle = 0;
+      } else if (++idle > 8) {
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    return;
+  }
+  // executor: take the next entry of the run ring, run that lane's turn; leave
+  // when every query is done (nothing more can be written) or on abort
+  for (;;) {
+    if (aborted(p)) break;
+    int got = 0;
+    unsigned long long idx = 0;
+    if (l == 0) {
+      const unsigned long long h = __hip_atomic_load(r.runq_head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const unsigned long long t = __hip_atomic_load(r.runq_tail_seen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+      if (h < t) {
+        if (atomicCAS(r.runq_head, h, h + 1) == h) {
+          got = 1;
+          idx = h;
+        }
+      } else if (all_done()) {
+        got = -1;
+      }
+    }
+    got = __shfl(got, 0);
+    if (got < 0) break;
+    if (got == 0) {
+      if (++idle > 8) __builtin_amdgcn_s_sleep(2);
+      continue;
+    }
+    idle = 0;
+    idx = readlane64(idx, 0);
+    unsigned long long e = 0;
+    if (l == 0) e = __hip_atomic_load(&r.runq[idx & r.runq_mask], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    e = readlane64(e, 0);
+    const uint32_t lane = (uint32_t)e - 1u, q1 = (uint32_t)(e >> 32);
+    if ((uint32_t)e == 0u || lane >= r.out_lanes) break;  // malformed: leave (the watchdog ends the search)
+    // the lane's state and visited table were written by whichever wave ran
+    // its last turn, which released them before its report
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    lane_turn<KPL, M, N2S>(p, r, lane, q1 ? q1 - 1u : kNone, lds, qbuf);
+  }
 }
 
 }  // namespace gorio

@@ -1,7 +1,8 @@
 """GPU parity of the scheduling modes and scheduler shapes of the paged search.
 
-Host-scheduled rounds (mode 2: a host thread owns the query lanes and
-launches one round kernel at a time over the lanes whose pages were filled),
+Host-scheduled lanes (mode 2: a host thread owns the query lanes and decides
+which run, as their pages are filled; a persistent executor launch runs the
+turns it hands over through a ring, or a launch per round runs them),
 the blocking and split-phase modes at an equal number of query waves
 (gorio_set_scheduler), and the full 10M x 96-d float32 configuration: every
 result must equal the CPU oracle bit for bit (float32 distances compared as
@@ -90,13 +91,18 @@ def test_host_rounds_match_oracle(torch_dev, small, monkeypatch, frac, latency, 
     ix.close()
 
 
-@pytest.mark.parametrize("flights,lanes", [("4", 0), ("8", 12)])
-def test_host_rounds_more_flights(torch_dev, small, monkeypatch, flights, lanes):
-    """Several round kernels in flight on streams of their own, lanes retired
-    one by one as their reports arrive and launched again on whichever
-    stream is free: the answers and counts stay the oracle's."""
+@pytest.mark.parametrize("flights,lanes,passes", [("2", 0, None), ("4", 0, None), ("8", 12, "0")])
+def test_host_rounds_launch_per_round(torch_dev, small, monkeypatch, flights, lanes, passes):
+    """Host-scheduled lanes run by a launch per round (instead of the
+    persistent executor), with one or several round kernels in flight on
+    streams of their own, lanes retired one by one as their reports arrive and
+    launched again on whichever stream is free: the answers and counts stay
+    the oracle's."""
     a, q, oids, od, oc = small
+    monkeypatch.setenv("GORIO_HOST_EXECUTOR", "0")
     monkeypatch.setenv("GORIO_ROUND_FLIGHTS", flights)
+    if passes is not None:
+        monkeypatch.setenv("GORIO_TURN_PASSES", passes)
     ix = g.Index(a["x"], a["graph"], vectors_first=True)
     ix.set_cache(int(0.10 * ix.info["index_bytes"]))
     ix.set_backing(latency_us=5.0, mode=HOST)
@@ -141,15 +147,17 @@ def test_host_rounds_held_proxy_then_recover(torch_dev, small, monkeypatch):
     ix.close()
 
 
-def test_host_rounds_with_many_streams_alive(torch_dev, small, monkeypatch):
-    """Host-scheduled rounds while the process holds many more streams than
+@pytest.mark.parametrize("executor", ["1", "0"], ids=["executor", "launch-per-round"])
+def test_host_rounds_with_many_streams_alive(torch_dev, small, monkeypatch, executor):
+    """Host-scheduled lanes while the process holds many more streams than
     the device has hardware queues, so streams share queues (and work on a
-    shared queue may run one item after another).  Every kernel of this mode
-    is bounded in time (the fill kernel leaves after a budget and is launched
-    again), so the search finishes, exactly, with the fill kernel relaunched
-    many times."""
+    shared queue may run one item after another).  No kernel of the mode waits
+    for another stream's work (the executor is one launch; with a launch per
+    round the fill kernel leaves after a budget and is launched again), so the
+    search finishes, exactly."""
     torch = torch_dev
     a, q, oids, od, oc = small
+    monkeypatch.setenv("GORIO_HOST_EXECUTOR", executor)
     streams = [torch.cuda.Stream() for _ in range(12)]
     keep = []
     for s in streams:   # use every stream once, so each holds its queue
@@ -174,8 +182,9 @@ def test_host_rounds_with_many_streams_alive(torch_dev, small, monkeypatch):
 
 def test_host_rounds_1m_bench_configuration(orc, torch_dev):
     """The 1M uint8 index, 10% cold cache, 0 us, all 10,000 queries, in the
-    benchmark's launch configuration for the host-scheduled leg (vectors-first
-    pages placed by 512 clusters, queries admitted by cluster)."""
+    benchmark's launch configuration for the host-scheduled leg (40 lanes run
+    by the persistent executor, vectors-first pages placed by 512 clusters,
+    queries admitted by cluster)."""
     w = WORKLOADS["u8-1m-cache10-lat0"]
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
@@ -183,6 +192,7 @@ def test_host_rounds_1m_bench_configuration(orc, torch_dev):
     ix = g.Index(a["x"], a["graph"], vectors_first=True, node_to_slot=n2s)
     ix.set_cache(int(w.cache_frac * ix.info["index_bytes"]))
     ix.set_backing(latency_us=w.latency_us, mode=HOST)
+    ix.set_scheduler(query_waves=40)
     ix.set_query_order(cent)
     gi, gd, st = search(torch_dev, ix, q, w.k, w.L, w.W)
     e = ix.info["entry"]
