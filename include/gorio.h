@@ -192,9 +192,11 @@ gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes);
  *                    1 = wait in place for each missing page, one query per wave
  *                        (the blocking demand-paging path the paper compares
  *                        against, Sec. 5.1, Table 2);
- *                    2 = host-scheduled rounds: a host thread (the caller's)
- *                        keeps the query lanes and launches round kernels (up to
- *                        two in flight) over the lanes whose pages have been filled, using
+ *                    2 = host-scheduled lanes: a host thread (the caller's)
+ *                        keeps the query lanes and decides which runs next, as
+ *                        their pages are filled; a persistent GPU launch runs the
+ *                        turns it hands over through a ring in host memory (or,
+ *                        with GORIO_HOST_EXECUTOR=0, a launch per round), using
  *                        the same page cache, descriptors and proxy (the
  *                        GustANN-style scheduler over GORIO's backend that the
  *                        paper compares against, Sec. 5.1, Table 2).  oversub is

@@ -360,21 +360,23 @@ extern "C" gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_wave
 // ---------------------------------------------------------------------------
 namespace {
 
-// Host-scheduled rounds (the GustANN-style comparison point of Sec. 5.1, over
+// Host-scheduled lanes (the GustANN-style comparison point of Sec. 5.1, over
 // the same page cache, miss descriptors and proxy): the calling thread owns
 // the query schedule.  It keeps `lanes` query lanes, starts queries in free
-// lanes in admission order, and launches round kernels over the lanes it
-// deems runnable, up to two rounds in flight on two streams (while one round
-// runs, the host reads the other's reports and gathers the next lanes).  A
-// lane is runnable when one of the cache slots it reported waiting for has
-// been filled -- the fill waves publish, per completion ring, how many
+// lanes in admission order, and hands the lanes it deems runnable to the GPU:
+// by default to one persistent launch whose executor waves take them from a
+// ring in host memory, else (GORIO_HOST_EXECUTOR=0) in round kernels, up to
+// GORIO_ROUND_FLIGHTS in flight on streams of their own.  Each lane's report
+// ends with a sequence number, so a lane is retired as soon as its turn is
+// over.  A lane is runnable when one of the cache slots it reported waiting
+// for has been filled -- the fill waves publish, per completion ring, how many
 // completions they have copied, and the host reads the filled {page, slot}
 // entries back from the ring -- or, for a lane that could not issue all of
 // its requests, when any page has been filled, or at once when its turn ended
-// while it could still proceed.  A slot filled while the lane's round ran is
-// caught by comparing when the host saw that fill with when the round was
-// launched.  A lane not woken within a few milliseconds is run anyway, so a
-// missed wake costs time, never progress.
+// while it could still proceed.  A slot filled while the lane's turn ran is
+// caught by comparing when the host saw that fill with when the lane was
+// handed over.  A lane not woken within a few milliseconds is run anyway, so
+// a missed wake costs time, never progress.
 gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, const std::vector<uint32_t> &order,
                              hipStream_t s, double limit_s, bool &timed_out) {
   using Clock = std::chrono::steady_clock;
@@ -815,7 +817,7 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
 
 // Paged search: reset the per-search rings and counters, fill in the kernel
 // parameters, arm the proxy, then run either the persistent kernel (GPU
-// scheduler, split-phase or blocking) or host-scheduled rounds, under a
+// scheduler, split-phase or blocking) or host-scheduled lanes, under a
 // watchdog.
 gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s, bool &timed_out) {
   PagedState &P = *ix->paged;

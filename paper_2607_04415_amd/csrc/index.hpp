@@ -56,7 +56,7 @@ struct PagedState {
   static constexpr uint32_t kTailStride = 16;  // u64 words
   uint32_t *d_ht_pool = nullptr;
   uint64_t ht_pool_entries = 0;
-  // host-scheduled rounds: lane states (HBM), the round's lane list and the
+  // host-scheduled lanes: lane states (HBM), the round's lane list and the
   // lanes' reports (host memory the kernels read and write), and how far each
   // completion ring has been filled (written by the fill waves)
   // round kernels in flight at once: flight 0 on the search's stream, flight

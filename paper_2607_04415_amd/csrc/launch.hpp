@@ -22,7 +22,8 @@ hipError_t launch_resident_f32(const ResidentParams &p, int grid, hipStream_t s)
 hipError_t launch_paged_u8(const PagedParams &pp, int grid, hipStream_t s);
 hipError_t launch_paged_f32(const PagedParams &pp, int grid, hipStream_t s);
 
-// Host-scheduled rounds: one workgroup per listed lane.
+// Host-scheduled lanes: one workgroup per listed lane, or (no list) the
+// persistent launch of fill waves, the run ring's tail mirror and executors.
 hipError_t launch_rounds_u8(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s);
 hipError_t launch_rounds_f32(const PagedParams &pp, const RoundParams &rp, int grid, hipStream_t s);
 

@@ -65,10 +65,10 @@ struct PagedParams {
   const uint32_t *order;                  // nullptr: queries in index order; else admission order
   unsigned int *done_queries;             // device: queries finished (fill waves stop at nq)
   unsigned long long *fill_head;          // host memory or nullptr: completions of ring k filled so far,
-                                          // at fill_head[k * tail_stride] (host-scheduled rounds); a
+                                          // at fill_head[k * tail_stride] (host-scheduled lanes); a
                                           // fill wave starts from there
   unsigned long long fill_budget;         // nonzero: a fill wave leaves after this many wall-clock
-                                          // ticks (host-scheduled rounds relaunch it)
+                                          // ticks (a launch per round relaunches it)
   uint32_t *out_ids;
   uint32_t *out_dists;                    // distance bits (int32 or float32)
   uint32_t *ht_pool;                      // (grid * oversub) << kPagedHtLog2 entries
@@ -521,10 +521,10 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
 
 // Fill wave k: consumes completion ring k (its own: no atomics on the ring)
 // and copies the pages until every query is done, or, with a budget, until
-// the budget has passed (host-scheduled rounds: the host launches the fill
-// waves again, and they go on from the ring position they published, so no
-// kernel of that mode ever waits for another stream's work).  Wave 0 also
-// mirrors the host abort flag.
+// the budget has passed (host-scheduled lanes run by a launch per round: the
+// host launches the fill waves again, and they go on from the ring position
+// they published, so no kernel of that mode ever waits for another stream's
+// work).  Wave 0 also mirrors the host abort flag.
 __device__ void fill_loop(const PagedParams &p, uint32_t k) {
   const int l = lane_id();
   const unsigned long long *ring = p.cq + (uint64_t)k * (p.cq_mask + 1);
@@ -558,7 +558,7 @@ __device__ void fill_loop(const PagedParams &p, uint32_t k) {
       served += good;
       head += good < n ? good + 1 : n;  // step over a malformed entry
     }
-    // host-scheduled rounds: entries [0, head) of this ring are now READY
+    // host-scheduled lanes: entries [0, head) of this ring are now READY
     if (filled && l == 0) __hip_atomic_store(filled, head, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (l == 0) atomicAdd(&p.stats[6], served);
@@ -649,14 +649,16 @@ __global__ __launch_bounds__(kWave) void search_paged(PagedParams p) {
 
 
 // ---------------------------------------------------------------------------
-// Host-scheduled rounds (the host-scheduled comparison point of Sec. 5.1: a
+// Host-scheduled lanes (the host-scheduled comparison point of Sec. 5.1: a
 // query scheduler on the host coordinates many query lanes, over the same GPU
 // page cache, miss descriptors and proxy).  The host keeps the lanes' states
-// in HBM and chooses which lanes run in each launch; a launch runs every
-// chosen lane once, until its query finishes or parks, and reports what the
-// lane now waits for.  Fill waves run in a kernel of their own beside the
-// rounds and publish how far each completion ring has been filled, which is
-// the completion state the host schedules from.
+// in HBM and chooses which lane runs next; a turn runs the lane until its
+// query finishes or parks (or yields) and reports what the lane now waits for.
+// Turns are run by a persistent launch that takes them from a ring the host
+// writes, or by one launch per round with a workgroup per chosen lane.  Fill
+// waves (in the persistent launch, or in a kernel of their own beside the
+// rounds) publish how far each completion ring has been filled, which is the
+// completion state the host schedules from.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kLaneWaitCap = 60;
 enum : uint32_t { kLaneIdle = 0, kLaneParked = 1, kLaneDone = 2, kLaneYield = 3 };

@@ -67,7 +67,7 @@ def assert_same(gi, gd, oids, od):
 
 
 # --------------------------------------------------------------------------- #
-# host-scheduled rounds
+# host-scheduled lanes
 # --------------------------------------------------------------------------- #
 @pytest.mark.parametrize("frac,latency,vfirst,lanes,passes", [
     (0.10, 0.0, False, 0, None), (0.10, 20.0, True, 0, None), (0.30, 5.0, False, 7, "3"), (0.05, 0.0, True, 1, None),
