@@ -302,13 +302,15 @@ def test_paged_f32_generic_dims(orc, torch_dev):
     assert_same(gi, gd, oids, od)
 
 
-RANDOM_CONFIGS = 10
+RANDOM_CONFIGS = 16
 
 
 @pytest.mark.parametrize("seed", range(RANDOM_CONFIGS))
-def test_paged_random_configuration(orc, torch_dev, seed):
+def test_paged_random_configuration(orc, torch_dev, monkeypatch, seed):
     """Seeded random configurations of the whole paged path: dtype, sizes,
-    beam, page size and layout, cache size, latency, slots, blocking mode."""
+    beam, page size and layout, cache size, latency, slots, scheduling mode
+    (split-phase, blocking, or host-scheduled lanes run by the executor or by
+    a launch per round)."""
     rng = np.random.default_rng(1000 + seed)
     dtype = "u8" if rng.random() < 0.6 else "f32"
     D = int(rng.choice([4, 16, 64, 128]) if dtype == "u8" else rng.choice([7, 32, 96]))
@@ -340,11 +342,24 @@ def test_paged_random_configuration(orc, torch_dev, seed):
     pb = ix.info["page_bytes"]
     ix.set_cache(max(int(rng.uniform(0.02, 0.6) * ix.info["index_bytes"]), 128 * pb))
     blocking = bool(rng.random() < 0.25)
+    # host-scheduled lanes (their own stream of draws too)
+    hrng = np.random.default_rng(9000 + seed)
+    host = bool(hrng.random() < 0.35)
+    mode = 2 if host else int(blocking)
+    host_desc = ""
+    if host:
+        executor = bool(hrng.random() < 0.6)
+        passes = [None, "1", "3"][int(hrng.integers(0, 3))]
+        monkeypatch.setenv("GORIO_HOST_EXECUTOR", "1" if executor else "0")
+        if passes is not None:
+            monkeypatch.setenv("GORIO_TURN_PASSES", passes)
+        ix.set_scheduler(query_waves=int(hrng.choice([0, 1, 3, 16])))
+        host_desc = f" host executor={executor} passes={passes}"
     ix.set_backing(latency_us=float(rng.choice([0.0, 3.0, 20.0])), oversub=int(rng.choice([1, 2, 4, 8])),
-                   blocking=blocking)
+                   mode=mode)
     print(f"[random {seed}] {dtype} n={n} D={D} R={R} k={k} L={L} W={W} {layout.get('page_bytes')} "
           f"vfirst={layout['vectors_first']} perm={'node_to_slot' in layout} clusters={cent is not None} "
-          f"slots={ix.info['cache_slots']} blocking={blocking}", flush=True)
+          f"slots={ix.info['cache_slots']} mode={mode}{host_desc}", flush=True)
     gi, gd, st = search(torch_dev, ix, q, k, L, W)
     assert_same(gi, gd, oids, od)
     assert st["expansions"] == int(oc["expansions"].sum())
