@@ -242,7 +242,10 @@ gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_waves, uint32_t
  * no-op.  Errors: GORIO_EINVAL for arguments out of range, GORIO_EUNSUPPORTED
  * for a paged W above 64, GORIO_ENOMEM / GORIO_EDEVICE from the device,
  * GORIO_ETIMEOUT when a paged search did not finish within the watchdog
- * limit (the counters so far are filled; the cache is reset).
+ * limit (the counters so far are filled; the cache is reset), and
+ * GORIO_EUNSUPPORTED on a stream under graph capture (each search takes its
+ * query tickets from a base the host advances, so a replay would be wrong;
+ * gorio_search_noalloc is the entry point to capture).
  */
 gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq,
                           uint32_t k, uint32_t L, uint32_t W,
@@ -258,6 +261,10 @@ gorio_status gorio_search(gorio_index *ix, const void *queries, uint64_t nq,
  *   stats:   NULL, or filled with kernel_ms, evaluations, reevaluations,
  *            expansions and iterations (the call then waits for the search).
  *   stream:  hipStream_t (NULL = the null stream).
+ * Under graph capture on `stream` the call records and waits for no event
+ * (the caller orders the graph's replays with other work on the index) and
+ * takes no statistics (stats != NULL -> GORIO_EINVAL); every replay clears
+ * the scratch and runs the whole search again.
  * Scratch: the search's counters live in a fixed 128-byte device array of
  * the library, one per GPU, kept until the process ends; no batch size needs
  * more.  Each call clears it first.  Calls that overlap on one GPU (different

@@ -986,6 +986,14 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   DeviceGuard dg(ix->device);
   if (!dg.ok) return fail(GORIO_EDEVICE, "cannot select device %d", ix->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  {
+    // each search takes its query tickets from a base kept on the host, so a
+    // captured search would replay with a stale base
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_OR_FAIL(hipStreamIsCapturing(s, &cap));
+    if (cap != hipStreamCaptureStatusNone)
+      return fail(GORIO_EUNSUPPORTED, "gorio_search cannot be captured into a graph; use gorio_search_noalloc");
+  }
 
   const size_t qbytes = (size_t)nq * ix->vec_bytes;
   const size_t obytes = (size_t)nq * k * 4;

@@ -93,8 +93,17 @@ extern "C" gorio_status gorio_search_noalloc(gorio_index *ix, const void *querie
     e = (expr);                                                                             \
     if (e != hipSuccess) return fail(GORIO_EDEVICE, "%s: %s", #expr, hipGetErrorString(e)); \
   } while (0)
-  // after the previous search of this index (its events are reused here)
-  if (ix->ev_done_recorded && ix->last_stream != s) NOALLOC_HIP(hipStreamWaitEvent(s, ix->ev_done, 0));
+  // Under graph capture the graph orders the work: no event is recorded or
+  // waited for (the caller orders replays with its other work), and no
+  // statistics (they need a synchronisation).  Otherwise the call follows
+  // the previous search of this index, as gorio_search does.
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  NOALLOC_HIP(hipStreamIsCapturing(s, &cap));
+  const bool capturing = cap != hipStreamCaptureStatusNone;
+  if (capturing && stats)
+    return fail(GORIO_EINVAL, "gorio_search_noalloc under graph capture takes no statistics (pass NULL)");
+  if (!capturing && ix->ev_done_recorded && ix->last_stream != s)
+    NOALLOC_HIP(hipStreamWaitEvent(s, ix->ev_done, 0));
   zero_words<<<1, 64, 0, s>>>(sc, kScratchWords);
   NOALLOC_HIP(hipGetLastError());
 
@@ -117,14 +126,16 @@ extern "C" gorio_status gorio_search_noalloc(gorio_index *ix, const void *querie
   p.next_query = sc + kStatNextQuery;
   p.next_base = 0;  // cleared above
   const int grid = (int)std::min<uint64_t>(nq, 1u << 30);
-  NOALLOC_HIP(hipEventRecord(ix->ev_start, s));
+  if (stats) NOALLOC_HIP(hipEventRecord(ix->ev_start, s));
   NOALLOC_HIP(ix->dtype == GORIO_F32 ? launch_resident_f32(p, grid, s) : launch_resident_u8(p, grid, s));
-  NOALLOC_HIP(hipEventRecord(ix->ev_stop, s));
+  if (stats) NOALLOC_HIP(hipEventRecord(ix->ev_stop, s));
   unsigned long long h[kScratchWords] = {};
   if (stats) NOALLOC_HIP(hipMemcpyAsync(h, sc, sizeof h, hipMemcpyDeviceToHost, s));
-  NOALLOC_HIP(hipEventRecord(ix->ev_done, s));
-  ix->ev_done_recorded = true;
-  ix->last_stream = s;
+  if (!capturing) {
+    NOALLOC_HIP(hipEventRecord(ix->ev_done, s));
+    ix->ev_done_recorded = true;
+    ix->last_stream = s;
+  }
   if (stats) {
     NOALLOC_HIP(hipStreamSynchronize(s));
     float ms = 0.f;

@@ -83,3 +83,49 @@ def test_noalloc_rejects(torch_dev):
     ix.set_cache(64 * 4096)
     assert fn(ix._h, qd.data_ptr(), 50, 10, 32, 4, idd.data_ptr(), dd.data_ptr(), None, None) == g.EUNSUPPORTED
     ix.close()
+
+
+def test_noalloc_graph_replays(torch_dev):
+    """Captured into a HIP graph, gorio_search_noalloc replays the whole
+    search each time: every replay gives gorio_search's answers, with eager
+    searches (which reuse the same scratch words) between the replays."""
+    torch = torch_dev
+    spec = IndexSpec(n=20000, D=128, dtype="u8", clusters=16, sigma=20.0, r_near=16, r_rand=16, seed=76)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(2000, 77))
+    k, L, W = 10, 64, 4
+    nq = len(q)
+    ix = g.Index(a["x"], a["graph"], vectors_first=True)
+    qd = torch.from_numpy(q).cuda()
+    search, fn = g.lib().gorio_search, _noalloc()
+    ref_ids, ref_d, _ = _search(torch, search, ix, qd, nq, k, L, W, torch.int32)
+    ids = torch.full((nq, k), -7, dtype=torch.int32, device="cuda")
+    dists = torch.full((nq, k), -7, dtype=torch.int32, device="cuda")
+    # first call on this device outside the capture (it looks the scratch up)
+    _search(torch, fn, ix, qd, 100, k, L, W, torch.int32)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        # statistics need a synchronisation: refused under capture
+        assert fn(ix._h, qd.data_ptr(), nq, k, L, W, ids.data_ptr(), dists.data_ptr(),
+                  ctypes.byref(g.Stats()), s) == g.EINVAL
+        # gorio_search keeps a host-side ticket base: refused under capture
+        assert search(ix._h, qd.data_ptr(), nq, k, L, W, ids.data_ptr(), dists.data_ptr(), None, s) \
+            == g.EUNSUPPORTED
+        status = fn(ix._h, qd.data_ptr(), nq, k, L, W, ids.data_ptr(), dists.data_ptr(), None, s)
+    assert status == g.OK, g.lib().gorio_last_error().decode()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        ids.fill_(-7)
+        dists.fill_(-7)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(ids.cpu().numpy().view(np.uint32), ref_ids), rep
+        assert np.array_equal(dists.cpu().numpy(), ref_d), rep
+        # eager work on the same index and scratch between replays
+        e_ids, e_d, _ = _search(torch, fn, ix, qd, 300 + 200 * rep, k, L, W, torch.int32)
+        assert np.array_equal(e_ids, ref_ids[:300 + 200 * rep])
+        e_ids, e_d, _ = _search(torch, search, ix, qd, 500, k, L, W, torch.int32)
+        assert np.array_equal(e_ids, ref_ids[:500])
+    del graph
+    ix.close()
