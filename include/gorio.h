@@ -50,7 +50,10 @@
  *     different streams run one after another: a search on another stream
  *     than the previous search of the index waits on the GPU for that search
  *     (an event the index records), because they share the index's counters;
- *     on the same stream, stream order does it.  Different indexes may be
+ *     on the same stream, stream order does it where that stream is the null
+ *     or the per-thread stream; on a created stream the search waits for the
+ *     event all the same (a stream created after another was destroyed can
+ *     get the same handle).  Different indexes may be
  *     used from different threads.
  *   - The device is the HIP device current when gorio_build_index is called;
  *     later calls switch to it and restore the caller's device.

@@ -1013,9 +1013,9 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   if (!d_dev) { HIP_OR_FAIL(dbuf.alloc(obytes)); d_dists = dbuf.p; }
 
   // the previous search of this index finishes before this one uses the
-  // counters they share: on the same stream by stream order, on another
-  // stream by waiting for the event it recorded last
-  if (ix->ev_done_recorded && ix->last_stream != s) HIP_OR_FAIL(hipStreamWaitEvent(s, ix->ev_done, 0));
+  // counters they share: by stream order, or by waiting for the event it
+  // recorded last
+  if (ix->ev_done_recorded && !follows_last_search(ix, s)) HIP_OR_FAIL(hipStreamWaitEvent(s, ix->ev_done, 0));
   // the counters only grow; a search that reports them reports the growth
   if (stats)
     HIP_OR_FAIL(hipMemcpyAsync(ix->d_stats + kStatWords, ix->d_stats, kStatWords * sizeof(unsigned long long),

@@ -262,3 +262,12 @@ struct gorio_index {
     stream = nullptr;
   }
 };
+
+// True when stream order alone puts a search on `s` after the index's last
+// search: the same stream, and one that is never destroyed (the null stream or
+// the per-thread stream).  A created stream's handle is given to the next
+// stream created once it is destroyed, so on any other handle the search waits
+// for the last search's event.
+inline bool follows_last_search(const gorio_index *ix, hipStream_t s) {
+  return ix->last_stream == s && (s == nullptr || s == hipStreamPerThread);
+}

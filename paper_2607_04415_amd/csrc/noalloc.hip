@@ -102,7 +102,7 @@ extern "C" gorio_status gorio_search_noalloc(gorio_index *ix, const void *querie
   const bool capturing = cap != hipStreamCaptureStatusNone;
   if (capturing && stats)
     return fail(GORIO_EINVAL, "gorio_search_noalloc under graph capture takes no statistics (pass NULL)");
-  if (!capturing && ix->ev_done_recorded && ix->last_stream != s)
+  if (!capturing && ix->ev_done_recorded && !follows_last_search(ix, s))
     NOALLOC_HIP(hipStreamWaitEvent(s, ix->ev_done, 0));
   zero_words<<<1, 64, 0, s>>>(sc, kScratchWords);
   NOALLOC_HIP(hipGetLastError());

@@ -35,6 +35,18 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, name), name
 
 
+def test_library_loads_after_torchs_hip_runtime(lib):
+    """torch brings its own HIP runtime, which a process loads first; the
+    library may use only what that runtime exports (a symbol of a newer HIP
+    release leaves the library unloadable there)."""
+    import subprocess
+    import sys
+    code = ("import ctypes, torch; "
+            f"ctypes.CDLL({str(g.LIB_PATH)!r}); print('loaded')")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "loaded" in r.stdout, r.stderr[-2000:]
+
+
 def test_struct_sizes_match_header():
     # gorio_stats: 2 doubles + 11 uint64; gorio_page_layout: 4 uint32 + pointer
     assert ctypes.sizeof(g.Stats) == 2 * 8 + 11 * 8

@@ -10,6 +10,7 @@ well (compared as uint32 patterns) and so do the ids; the 1e-5 relative
 tolerance and 0.999 id overlap are checked first as the acceptance bound,
 then exactness.
 """
+import ctypes
 import json
 import os
 from pathlib import Path
@@ -414,6 +415,39 @@ def test_searches_on_two_streams_do_not_share_counters(orc, torch_dev):
         ix.search_into(qd, len(q), k, L, W, ids, dd, stream=s.cuda_stream, stats=False)
     torch.cuda.synchronize()
     for ids, dd in outs:
+        assert np.array_equal(ids.cpu().numpy().view(np.uint32), ref_ids)
+        assert np.array_equal(dd.cpu().numpy(), ref_d)
+    ix.close()
+
+
+def test_stream_created_after_another_is_destroyed(orc, torch_dev):
+    """A stream created after another was destroyed may get its handle; on
+    created streams the index always waits for its last search's event (here
+    one recorded on a stream since destroyed), and each search answers every
+    query.  Each stream is synchronized before it is destroyed."""
+    torch = torch_dev
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipStreamCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipStreamSynchronize.argtypes = [ctypes.c_void_p]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    spec = IndexSpec(n=20000, D=128, dtype="u8", clusters=8, sigma=20.0, r_near=16, r_rand=16, seed=97)
+    a = index_arrays(spec, use_cache=False)
+    q = query_array(spec, QuerySpec(2000, 98))
+    k, L, W = 10, 32, 4
+    ix = g.Index(a["x"], a["graph"])
+    ref_ids, ref_d, _ = run_gpu(torch, ix, q, k, L, W)
+    qd = torch.from_numpy(q).cuda()
+    ids = torch.full((len(q), k), -1, dtype=torch.int32, device="cuda")
+    dd = torch.full((len(q), k), -1, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        s = ctypes.c_void_p()
+        assert hip.hipStreamCreate(ctypes.byref(s)) == 0
+        ids.fill_(-1)
+        dd.fill_(-1)
+        torch.cuda.synchronize()
+        ix.search_into(qd, len(q), k, L, W, ids, dd, stream=s.value, stats=False)
+        assert hip.hipStreamSynchronize(s) == 0
+        assert hip.hipStreamDestroy(s) == 0
         assert np.array_equal(ids.cpu().numpy().view(np.uint32), ref_ids)
         assert np.array_equal(dd.cpu().numpy(), ref_d)
     ix.close()
