@@ -254,6 +254,30 @@ def resident_leg(torch, g, a, q, w, layout: str, steps: int, warmup: int):
             "ids": ids.cpu().numpy().view(np.uint32), "dists": dists.cpu().numpy()}
 
 
+def host_buffer_leg(g, a, q, w, layout: str, steps: int, ref_ids, ref_dists) -> dict:
+    """The same search with queries, ids and dists in pageable host memory: each
+    call stages the queries into HBM and the answers back over the host link and
+    returns when they are there.  A rate that includes the link, reported beside
+    the HBM-resident one, never as it."""
+    ix = g.Index(a["x"], a["graph"], vectors_first=layout == "vectors-first")
+    nq = len(q)
+    qh = np.ascontiguousarray(q)
+    ids = np.empty((nq, w.k), np.uint32)
+    dists = np.empty((nq, w.k), np.int32 if q.dtype == np.uint8 else np.float32)
+    ix.search_into(qh, nq, w.k, w.L, w.W, ids, dists, stats=False)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        ix.search_into(qh, nq, w.k, w.L, w.W, ids, dists, stats=False)
+    elapsed = time.perf_counter() - t0
+    ix.close()
+    out = {"value": round(nq * steps / elapsed, 1), "unit": "queries/s", "steps": steps,
+           "ms_per_step": round(elapsed * 1e3 / steps, 4),
+           "bytes_per_step": {"queries_in": int(qh.nbytes), "answers_out": int(ids.nbytes + dists.nbytes)},
+           "same_answers": bool(np.array_equal(ids, ref_ids) and np.array_equal(dists, ref_dists))}
+    log(f"{w.name} with host buffers: {out['ms_per_step']:.3f} ms/step, {out['value']:,.0f} queries/s")
+    return out
+
+
 def roofline_of(res: dict, w, R: int, oracle_evals, traffic, kernel: str) -> dict:
     st = res["stats"]
     alg, src = algorithmic_bytes(st, R, w.index.vec_bytes, oracle_evals)
@@ -339,6 +363,8 @@ def main():
     ap.add_argument("--layout", choices=LAYOUTS, default="vectors-first",
                     help="page layout of the timed index (the other one is timed too and reported)")
     ap.add_argument("--no-other-layout", action="store_true", help="do not time the other page layout")
+    ap.add_argument("--no-host-buffers", action="store_true",
+                    help="do not time the search with queries and answers in host memory")
     ap.add_argument("--cpu-sample", type=int, default=10000)
     ap.add_argument("--one-thread-sample", type=int, default=2000,
                     help="queries the 1-thread oracle baseline runs (0 = skip)")
@@ -427,6 +453,10 @@ def main():
                  "ms_per_step": round(o["elapsed"] * 1e3 / args.steps, 4),
                  "kernel_ms_avg": round(float(np.mean(o["kernel_ms"])), 4),
                  "same_answers": bool(np.array_equal(o["ids"], gi) and np.array_equal(o["dists"], gd))}
+
+    host_buffers = None
+    if not args.no_host_buffers:
+        host_buffers = host_buffer_leg(g, a, q, w, args.layout, args.steps, gi, gd)
 
     cpu = exact = ocounts = packed_main = None
     if not args.no_cpu_baseline:
@@ -658,6 +688,7 @@ def main():
                    "records_per_page": info["records_per_page"], "page_layout": args.layout,
                    "cache_frac": w.cache_frac, "resident": bool(info["resident"])},
         "other_layout": other,
+        "host_buffers": host_buffers,
         "oracle_exact": exact,
         "recall": recall,
         "achieved_hbm_gbs": roofline.get("traffic_gbs"),
