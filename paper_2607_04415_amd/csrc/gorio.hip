@@ -481,7 +481,14 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
     const hipError_t le = ix->dtype == GORIO_F32 ? launch_rounds_f32(pp, rx, grid, s)
                                                  : launch_rounds_u8(pp, rx, grid, s);
     if (le != hipSuccess) return fail(GORIO_EDEVICE, "executor launch failed: %s", hipGetErrorString(le));
-    HIP_OR_FAIL(hipEventRecord(P.ev_round[0], s));
+    const hipError_t re = hipEventRecord(P.ev_round[0], s);
+    if (re != hipSuccess) {
+      // the launch leaves on the abort flag; it is over before the caller
+      // stops the proxy it would wait on
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      (void)hipStreamSynchronize(s);
+      return fail(GORIO_EDEVICE, "hipEventRecord: %s", hipGetErrorString(re));
+    }
   }
   auto push_lane = [&](uint32_t lane, uint32_t q) {  // q = kNone: go on with the lane's query
     const unsigned long long e = ((unsigned long long)(q == kNone ? 0u : q + 1u) << 32) | (lane + 1u);
@@ -940,7 +947,14 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
       P.proxy.end();
       return fail(GORIO_EDEVICE, "paged search launch failed: %s", hipGetErrorString(le));
     }
-    HIP_OR_FAIL(hipEventRecord(ix->ev_stop, s));
+    const hipError_t re = hipEventRecord(ix->ev_stop, s);
+    if (re != hipSuccess) {  // the kernel leaves on the abort flag, before the proxy stops
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+      (void)hipStreamSynchronize(s);
+      P.proxy.end();
+      (void)ix->reset_cache();
+      return fail(GORIO_EDEVICE, "hipEventRecord: %s", hipGetErrorString(re));
+    }
     // watchdog: the kernel polls the abort flag (through its device mirror)
     const auto t0 = std::chrono::steady_clock::now();
     for (;;) {
@@ -948,6 +962,7 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
       if (q == hipSuccess) break;
       if (q != hipErrorNotReady) {
         P.proxy.end();
+        (void)ix->reset_cache();
         return fail(GORIO_EDEVICE, "paged search failed: %s", hipGetErrorString(q));
       }
       const double el = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
@@ -959,7 +974,13 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
     }
   }
   P.proxy.end();
-  if (st != GORIO_OK) return st;
+  if (st != GORIO_OK) {
+    // a search that failed part way leaves pins and LOADING slots behind, as an
+    // aborted one does; the first error is the one reported
+    const std::string msg = gorio_last_error();
+    (void)ix->reset_cache();
+    return fail(st, "%s", msg.c_str());
+  }
   if (timed_out) {
     gorio_status rs = ix->reset_cache();  // pins and LOADING slots of aborted queries
     if (rs != GORIO_OK) return rs;
