@@ -117,6 +117,24 @@ def _ptr(a):
     return a.data_ptr()
 
 
+def _check_buffer(name: str, a, count: int, dtypes: tuple):
+    """The C ABI takes plain pointers and cannot check what they hold: a
+    buffer of the wrong element type, not C-contiguous, or with fewer than
+    `count` elements is refused here, before the library reads or writes it."""
+    if a is None:
+        raise ValueError(f"{name} is None")
+    if isinstance(a, np.ndarray):
+        dt, size, contiguous = a.dtype.name, a.size, a.flags.c_contiguous
+    else:
+        dt, size, contiguous = str(a.dtype).replace("torch.", ""), a.numel(), a.is_contiguous()
+    if dt not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(dtypes)}, not {dt}")
+    if not contiguous:
+        raise ValueError(f"{name} must be C-contiguous")
+    if size < count:
+        raise ValueError(f"{name} holds {size} elements, the search needs {count}")
+
+
 def locality_order(graph: np.ndarray, entry: int, records_per_page: int) -> np.ndarray:
     """node_to_slot placing graph neighbours in the same pages (gorio_locality_order)."""
     graph = np.ascontiguousarray(graph, dtype=np.uint32)
@@ -220,7 +238,14 @@ class Index:
 
     def search_into(self, queries, nq: int, k: int, L: int, W: int, ids, dists,
                     stream=None, stats: bool = True):
-        """Raw call: queries/ids/dists are numpy arrays or device tensors."""
+        """Raw call: queries/ids/dists are numpy arrays or device tensors
+        (queries: nq x D of the index's element type; ids: nq x k int32 or
+        uint32; dists: nq x k int32 for uint8 indexes, float32 for float32)."""
+        if nq > 0:
+            u8 = self.dtype == U8
+            _check_buffer("queries", queries, nq * self.D, ("uint8",) if u8 else ("float32",))
+            _check_buffer("ids", ids, nq * k, ("int32", "uint32"))
+            _check_buffer("dists", dists, nq * k, ("int32",) if u8 else ("float32",))
         st = Stats()
         sp = None if stream is None else ctypes.c_void_p(stream)
         status = lib().gorio_search(self._h, _ptr(queries), nq, k, L, W, _ptr(ids), _ptr(dists),
@@ -232,7 +257,12 @@ class Index:
         return st.as_dict() if stats else None
 
     def search(self, queries, k: int, L: int, W: int, stream=None, stats: bool = True):
-        """Search a batch.  numpy in -> numpy out; torch device tensor in -> tensors out."""
+        """Search a batch.  numpy (or a CPU tensor) in -> numpy out; torch device
+        tensor in -> tensors out."""
+        if not isinstance(queries, np.ndarray) and not queries.is_cuda:
+            queries = queries.numpy()
+        if queries.shape[-1] != self.D or len(queries.shape) > 2:
+            raise ValueError(f"queries must be (nq, {self.D}) or ({self.D},), not {tuple(queries.shape)}")
         if isinstance(queries, np.ndarray):
             queries = np.ascontiguousarray(queries)
             nq = queries.shape[0] if queries.ndim == 2 else 1

@@ -47,6 +47,27 @@ def test_library_loads_after_torchs_hip_runtime(lib):
     assert r.returncode == 0 and "loaded" in r.stdout, r.stderr[-2000:]
 
 
+def test_buffers_are_checked_before_the_library_sees_them():
+    """Plain pointers cross the ABI, so the binding refuses a buffer of the
+    wrong element type, one that is not contiguous, or one too small."""
+    import torch
+    chk = g._check_buffer
+    chk("q", np.zeros((4, 8), np.uint8), 32, ("uint8",))
+    chk("ids", torch.zeros((4, 3), dtype=torch.int32), 12, ("int32", "uint32"))
+    with pytest.raises(ValueError, match="needs 33"):
+        chk("q", np.zeros((4, 8), np.uint8), 33, ("uint8",))
+    with pytest.raises(TypeError, match="float32"):
+        chk("q", np.zeros((4, 8), np.float64), 32, ("float32",))
+    with pytest.raises(ValueError, match="contiguous"):
+        chk("q", np.zeros((8, 4), np.uint8).T, 32, ("uint8",))
+    with pytest.raises(ValueError, match="contiguous"):
+        chk("ids", torch.zeros((3, 4), dtype=torch.int32).t(), 12, ("int32",))
+    with pytest.raises(ValueError, match="needs 13"):
+        chk("ids", torch.zeros((4, 3), dtype=torch.int32), 13, ("int32",))
+    with pytest.raises(ValueError, match="None"):
+        chk("dists", None, 1, ("int32",))
+
+
 def test_struct_sizes_match_header():
     # gorio_stats: 2 doubles + 11 uint64; gorio_page_layout: 4 uint32 + pointer
     assert ctypes.sizeof(g.Stats) == 2 * 8 + 11 * 8

@@ -267,6 +267,18 @@ def test_empty_batch_and_bad_arguments(torch_dev):
         with pytest.raises(g.GorioError) as e:
             ix.search(q, k, L, W)
         assert e.value.status == g.EINVAL
+    # buffers the search would overrun are refused before the library sees them
+    torch = torch_dev
+    qd = torch.zeros((4, 16), dtype=torch.uint8, device="cuda")
+    small = torch.empty((3, 1), dtype=torch.int32, device="cuda")
+    with pytest.raises(ValueError):
+        ix.search_into(qd, 4, 1, 4, 1, small, small)
+    with pytest.raises(ValueError):
+        ix.search_into(qd[:3], 4, 1, 4, 1, small, small)
+    with pytest.raises(ValueError):
+        ix.search(np.zeros((2, 15), np.uint8), 1, 4, 1)
+    ids, dists, _ = ix.search(qd, 1, 4, 1)        # the index is still usable
+    assert ids.shape == (4, 1)
 
 
 F32_CASES = [
