@@ -1021,17 +1021,33 @@ extern "C" gorio_status gorio_search(gorio_index *ix, const void *queries, uint6
   const bool q_dev = is_device_pointer(queries);
   const bool i_dev = is_device_pointer(ids);
   const bool d_dev = is_device_pointer(dists);
-  DevBuf qbuf, ibuf, dbuf;
   const void *d_q = queries;
   uint32_t *d_ids = ids;
   void *d_dists = dists;
-  if (!q_dev) {
-    HIP_OR_FAIL(qbuf.alloc(qbytes));
-    HIP_OR_FAIL(hipMemcpyAsync(qbuf.p, queries, qbytes, hipMemcpyHostToDevice, s));
-    d_q = qbuf.p;
+  if (!q_dev || !i_dev || !d_dev) {
+    // host buffers go through the index's staging buffer (grown when a batch
+    // needs more; the last search that used it has returned, so it is idle)
+    auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    const size_t need = (q_dev ? 0 : up(qbytes)) + (i_dev ? 0 : up(obytes)) + (d_dev ? 0 : up(obytes));
+    if (need > ix->stage_bytes) {
+      if (ix->d_stage) (void)hipFree(ix->d_stage);
+      ix->d_stage = nullptr;
+      ix->stage_bytes = 0;
+      HIP_OR_FAIL(hipMalloc(&ix->d_stage, need));
+      ix->stage_bytes = need;
+    }
+    uint8_t *at = ix->d_stage;
+    if (!q_dev) {
+      HIP_OR_FAIL(hipMemcpyAsync(at, queries, qbytes, hipMemcpyHostToDevice, s));
+      d_q = at;
+      at += up(qbytes);
+    }
+    if (!i_dev) {
+      d_ids = reinterpret_cast<uint32_t *>(at);
+      at += up(obytes);
+    }
+    if (!d_dev) d_dists = at;
   }
-  if (!i_dev) { HIP_OR_FAIL(ibuf.alloc(obytes)); d_ids = ibuf.as<uint32_t>(); }
-  if (!d_dev) { HIP_OR_FAIL(dbuf.alloc(obytes)); d_dists = dbuf.p; }
 
   // the previous search of this index finishes before this one uses the
   // counters they share: by stream order, or by waiting for the event it

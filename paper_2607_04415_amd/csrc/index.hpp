@@ -187,6 +187,10 @@ struct gorio_index {
   // resident launch starts.
   unsigned long long *d_stats = nullptr;
   uint64_t next_base = 0;
+  // device staging for searches handed host buffers: grow-only, used by one
+  // search at a time (such a search returns only after its copies)
+  uint8_t *d_stage = nullptr;
+  size_t stage_bytes = 0;
 
   uint64_t index_bytes() const { return num_pages * (uint64_t)page_bytes; }
 
@@ -245,6 +249,7 @@ struct gorio_index {
     if (h_backing) (void)hipHostFree(h_backing);
     if (d_node_to_slot) (void)hipFree(d_node_to_slot);
     if (d_stats) (void)hipFree(d_stats);
+    if (d_stage) (void)hipFree(d_stage);
     if (d_centroids) (void)hipFree(d_centroids);
     if (d_centroid_norms) (void)hipFree(d_centroid_norms);
     if (ev_start) (void)hipEventDestroy(ev_start);
@@ -255,6 +260,8 @@ struct gorio_index {
     h_backing = nullptr;
     d_node_to_slot = nullptr;
     d_stats = nullptr;
+    d_stage = nullptr;
+    stage_bytes = 0;
     d_centroids = d_centroid_norms = nullptr;
     order_clusters = 0;
     ev_start = ev_stop = ev_done = nullptr;

@@ -248,13 +248,33 @@ def test_single_node_and_widest_rows(orc, torch_dev):
 
 
 def test_host_pointers(orc, torch_dev):
+    """Host buffers go through the index's staging buffer: all on the host,
+    mixed with device buffers, and batches that shrink and then grow it."""
+    torch = torch_dev
     spec = IndexSpec(n=1000, D=32, dtype="u8", clusters=3, sigma=20.0, r_near=8, r_rand=8, seed=11)
     a = index_arrays(spec, use_cache=False)
-    q = query_array(spec, QuerySpec(40, 12))
+    q = query_array(spec, QuerySpec(600, 12))
     ix = g.Index(a["x"], a["graph"])
-    ids, dists, st = ix.search(q, 10, 20, 2)          # numpy in -> numpy out
     oids, od, _, _ = orc.pack(a["x"], a["graph"]).search(q, 10, 20, 2, ix.info["entry"])
-    assert np.array_equal(ids, oids) and np.array_equal(dists, od)
+    ids, dists, st = ix.search(q[:40], 10, 20, 2)     # numpy in -> numpy out
+    assert np.array_equal(ids, oids[:40]) and np.array_equal(dists, od[:40])
+    for nq, where in ((40, "qdev"), (40, "outdev"), (7, "host"), (600, "host"), (600, "qdev"),
+                      (250, "outdev"), (600, "idsdev")):
+        qh = np.ascontiguousarray(q[:nq])
+        qs = torch.from_numpy(qh).cuda() if where == "qdev" else qh
+        ih = np.full((nq, 10), 7, np.uint32)
+        dh = np.full((nq, 10), 7, np.int32)
+        idd = torch.full((nq, 10), 7, dtype=torch.int32, device="cuda")
+        ddd = torch.full((nq, 10), 7, dtype=torch.int32, device="cuda")
+        ids_buf = idd if where in ("outdev", "idsdev") else ih
+        d_buf = ddd if where == "outdev" else dh
+        ix.search_into(qs, nq, 10, 20, 2, ids_buf, d_buf)
+        torch.cuda.synchronize()
+        got_i = ids_buf.cpu().numpy().view(np.uint32) if ids_buf is idd else ids_buf
+        got_d = d_buf.cpu().numpy() if d_buf is ddd else d_buf
+        assert np.array_equal(got_i, oids[:nq]), (nq, where)
+        assert np.array_equal(got_d, od[:nq]), (nq, where)
+    ix.close()
 
 
 def test_empty_batch_and_bad_arguments(torch_dev):
