@@ -234,7 +234,10 @@ gorio_status gorio_set_scheduler(gorio_index *ix, uint32_t query_waves, uint32_t
  * or parked on a missing page and later resumed).
  *   queries: nq x D (uint8 or float32), host or device pointer.
  *   ids:     nq x k uint32 out; dists: nq x k out, int32 (uint8 data) or float32.
- *            Both host or device pointers (detected per pointer).
+ *            Both host or device pointers (detected per pointer).  Host
+ *            buffers are staged through a device buffer the index keeps
+ *            (grown when a batch needs more) and the call returns once the
+ *            answers are back in them.
  *   Slots past the reachable set are padded with UINT32_MAX and INT32_MAX / +inf.
  *   stats:   NULL or a struct to fill; non-NULL makes the call wait for the search.
  *   stream:  hipStream_t to launch on (NULL = the null stream).  With device
