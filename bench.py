@@ -360,6 +360,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="u8-1m-hbm")
+    ap.add_argument("--max-queries", type=int, default=0,
+                    help="time only the first N queries of the workload (profiling of small batches; 0 = all)")
     ap.add_argument("--layout", choices=LAYOUTS, default="vectors-first",
                     help="page layout of the timed index (the other one is timed too and reported)")
     ap.add_argument("--no-other-layout", action="store_true", help="do not time the other page layout")
@@ -438,6 +440,8 @@ def main():
     log(f"workload {w.name}: {w.description}")
     a = index_arrays(w.index)
     q = query_array(w.index, w.queries)
+    if args.max_queries > 0:
+        q = q[:args.max_queries]
     log("inputs ready")
     nq = len(q)
     main_res = resident_leg(torch, g, a, q, w, args.layout, args.steps, args.warmup)
