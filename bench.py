@@ -41,7 +41,7 @@ PROFILES = ROOT / "profiles"
 KERNEL_SOURCES = ["paper_2607_04415_amd/csrc/search_resident.hpp", "paper_2607_04415_amd/csrc/frontier.hpp",
                   "paper_2607_04415_amd/csrc/metric.hpp", "paper_2607_04415_amd/csrc/launch.hpp",
                   "paper_2607_04415_amd/csrc/common.hpp", "paper_2607_04415_amd/csrc/wave.hpp"]
-MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled"}
+MODES = {0: "split-phase", 1: "blocking", 2: "host-scheduled", 3: "gpu resume queue"}
 # Scheduler shapes of the paged legs (oversub = query slots per wave, query_waves; 0 = the
 # library's default, which runs as many queries as the cache's pins allow).  When the host
 # link is the bound, fewer queries in flight keep the link full and share the cache better
@@ -55,6 +55,10 @@ SHAPE_C3 = {"oversub": 1, "query_waves": 30}
 # host-scheduled lanes (persistent executor, turns until a lane parks): 30 / 40 / 50 / 60 /
 # 100 / 156 (the default) lanes gave 7.0k / 7.25k / 7.2k / 7.05k / 6.6k / 6.0k queries/s
 SHAPE_HOST = {"query_waves": 40}
+# GPU resume queue (fill waves queue the lanes parked on the pages they fill, executor
+# waves run them): 20 / 30 / 40 / 60 / 100 / 156 (the default) lanes gave 6.2k / 7.0k /
+# 7.1k / 7.0k / 6.6k / 6.0k queries/s
+SHAPE_QUEUE = {"query_waves": 40}
 SHAPE_C4 = {"oversub": 4, "query_waves": 30}
 SHAPE_C5 = {"oversub": 1, "query_waves": 60}
 # The paper's own figures (Table 2: 10,000 SIFT1M queries over NVMe-oF on one NVIDIA L40S,
@@ -535,11 +539,12 @@ def main():
         n3 = w3.queries.nq if args.paged_sample < 0 else min(args.paged_sample, w3.queries.nq)
         # C3 legs: split-phase and blocking in the same shape (one query per wave),
         # the identity placement, the default shape (as many queries as the pins
-        # allow, 4 per wave), host-scheduled lanes (40)
+        # allow, 4 per wave), host-scheduled lanes (40), the GPU resume queue (40 lanes)
         plan = [(0, clustered, "split-phase", SHAPE_C3), (1, clustered, "blocking", SHAPE_C3),
                 (0, False, "split-phase, identity placement", SHAPE_C3),
                 (0, clustered, "split-phase, default shape", {}),
-                (2, clustered, "host-scheduled", SHAPE_HOST)]
+                (2, clustered, "host-scheduled", SHAPE_HOST),
+                (3, clustered, "gpu resume queue", SHAPE_QUEUE)]
         for mode, use_cl, label, shape in plan:
             if use_cl is False and not clustered and label.endswith("identity placement"):
                 continue

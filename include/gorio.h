@@ -205,6 +205,15 @@ gorio_status gorio_set_cache(gorio_index *ix, uint64_t bytes);
  *                        paper compares against, Sec. 5.1, Table 2).  oversub is
  *                        ignored; the lanes are min(query_waves or 8 per compute
  *                        unit, slots / (2 * max_pending), nq, 8192).
+ *                    3 = GPU resume queue (Sec. 3.1, Fig. 1: a ready table
+ *                        feeding a resume queue): the same lanes, with their
+ *                        state in HBM, but nothing on the host except the proxy
+ *                        and the watchdog; a lane that parks joins the waiter
+ *                        set of each cache slot it waits for, the fill wave
+ *                        that makes a slot READY queues those lanes in a run
+ *                        queue in HBM, and executor waves of one persistent
+ *                        launch run the queued lanes' turns.  oversub is
+ *                        ignored; the lanes are counted as in mode 2.
  *                    Results are the same in every mode.
  * Takes effect at the next search.  Ignored in resident mode.
  * Errors: GORIO_EINVAL for a NULL index or an argument out of range.

@@ -212,7 +212,8 @@ class Index:
 
     def set_backing(self, latency_us: float = 0.0, max_outstanding: int = 0, oversub: int = 1,
                     blocking: bool = False, mode: int | None = None):
-        """mode: 0 split-phase, 1 blocking, 2 host-scheduled rounds (default: from `blocking`)."""
+        """mode: 0 split-phase, 1 blocking, 2 host-scheduled lanes, 3 GPU resume queue
+        (default: from `blocking`)."""
         m = int(bool(blocking)) if mode is None else int(mode)
         _check(lib().gorio_set_backing(self._h, float(latency_us), int(max_outstanding),
                                        int(oversub), m))

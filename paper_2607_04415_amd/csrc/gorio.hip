@@ -14,6 +14,7 @@
 #include "cluster.hpp"
 #include "index.hpp"
 #include "launch.hpp"
+#include "queue_launch.hpp"
 
 #if defined(__x86_64__)
 #include <immintrin.h>
@@ -338,7 +339,7 @@ extern "C" gorio_status gorio_set_backing(gorio_index *ix, double latency_us, ui
   if (!ix) return fail(GORIO_EINVAL, "index is NULL");
   if (!(latency_us >= 0.0) || latency_us > 1e7) return fail(GORIO_EINVAL, "latency_us=%g out of range", latency_us);
   if (oversub < 1 || oversub > 16) return fail(GORIO_EINVAL, "oversub=%u outside [1, 16]", oversub);
-  if (blocking < 0 || blocking > 2) return fail(GORIO_EINVAL, "mode (blocking) must be 0, 1 or 2");
+  if (blocking < 0 || blocking > 3) return fail(GORIO_EINVAL, "mode (blocking) must be 0, 1, 2 or 3");
   ix->latency_us = latency_us;
   ix->max_outstanding = max_outstanding ? max_outstanding : 4096;
   ix->oversub = oversub;
@@ -822,6 +823,96 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
   return st;
 }
 
+// GPU resume queue (mode 3): one persistent launch of fill waves and
+// executor waves; the fill waves queue the lanes parked on the slots they
+// fill and the executors run the queued lanes' turns (paged_queue).  The
+// host only runs the proxy and the watchdog.
+gorio_status run_gpu_queue(gorio_index *ix, PagedParams &pp, uint32_t lanes, hipStream_t s, double limit_s,
+                           bool &timed_out) {
+  PagedState &P = *ix->paged;
+  const uint32_t words = lane_state_words(pp.L);
+  if ((uint64_t)lanes * words > P.lane_state_words) {
+    if (P.d_lane_state) (void)hipFree(P.d_lane_state);
+    P.d_lane_state = nullptr;
+    P.lane_state_words = 0;
+    HIP_OR_FAIL(hipMalloc(&P.d_lane_state, (uint64_t)lanes * words * 4));
+    P.lane_state_words = (uint64_t)lanes * words;
+  }
+  if (lanes > P.lane_out_q_cap) {
+    if (P.d_lane_out_q) (void)hipFree(P.d_lane_out_q);
+    P.d_lane_out_q = nullptr;
+    P.lane_out_q_cap = 0;
+    HIP_OR_FAIL(hipMalloc(&P.d_lane_out_q, (size_t)lanes * sizeof(LaneOut)));
+    P.lane_out_q_cap = lanes;
+  }
+  // one buffer of 64-bit words: a waiter set per cache slot, the run queue,
+  // its head, its tail and the lane counter (each on a 256-byte line of its
+  // own), then the lanes' state words
+  const uint32_t wset = (lanes + 63) / 64;
+  uint32_t cap = 1;
+  while (cap < 2 * lanes + 64) cap <<= 1;
+  const uint64_t line = PagedState::kCtrlStride;
+  const uint64_t o_rq = P.slots * (uint64_t)wset, o_ctl = o_rq + cap, o_st = o_ctl + 3 * line;
+  const uint64_t total = o_st + (lanes + 1) / 2;
+  if (total > P.queue_words) {
+    if (P.d_queue) (void)hipFree(P.d_queue);
+    P.d_queue = nullptr;
+    P.queue_words = 0;
+    HIP_OR_FAIL(hipMalloc(&P.d_queue, total * sizeof(unsigned long long)));
+    P.queue_words = total;
+  }
+  fill_u32<<<grid_for(total * 2, 256), 256, 0, s>>>(reinterpret_cast<uint32_t *>(P.d_queue), total * 2, 0u);
+  const uint64_t out_words = (uint64_t)lanes * sizeof(LaneOut) / 4;
+  fill_u32<<<grid_for(out_words, 256), 256, 0, s>>>(reinterpret_cast<uint32_t *>(P.d_lane_out_q), out_words, 0u);
+  HIP_OR_FAIL(hipGetLastError());
+  QueueParams qp;
+  qp.lanes = lanes;
+  qp.words = wset;
+  qp.waiters = P.d_queue;
+  qp.rq = P.d_queue + o_rq;
+  qp.rq_mask = cap - 1;
+  qp.rq_head = P.d_queue + o_ctl;
+  qp.rq_tail = P.d_queue + o_ctl + line;
+  qp.next_lane = reinterpret_cast<unsigned int *>(P.d_queue + o_ctl + 2 * line);
+  qp.lane_st = reinterpret_cast<uint32_t *>(P.d_queue + o_st);
+  RoundParams rx = {};
+  rx.state = P.d_lane_state;
+  rx.state_words = words;
+  rx.out = P.d_lane_out_q;
+  rx.out_lanes = lanes;
+  pp.fill_head = nullptr;
+  pp.fill_budget = 0;
+  pp.turn_passes = 0;  // a turn runs until the lane parks
+  int cus = 0;
+  HIP_OR_FAIL(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ix->device));
+  const int execs = (int)std::min<uint64_t>(lanes, (uint64_t)cus * 4);
+  const int grid = (int)pp.fill_waves + execs;
+  HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));
+  const hipError_t le = ix->dtype == GORIO_F32 ? launch_queue_f32(pp, rx, qp, grid, s)
+                                               : launch_queue_u8(pp, rx, qp, grid, s);
+  if (le != hipSuccess) return fail(GORIO_EDEVICE, "queue launch failed: %s", hipGetErrorString(le));
+  const hipError_t re = hipEventRecord(ix->ev_stop, s);
+  if (re != hipSuccess) {  // the launch leaves on the abort flag, before the proxy stops
+    __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+    (void)hipStreamSynchronize(s);
+    return fail(GORIO_EDEVICE, "hipEventRecord: %s", hipGetErrorString(re));
+  }
+  // watchdog: the waves poll the abort flag (through its device mirror)
+  const auto t0 = std::chrono::steady_clock::now();
+  for (;;) {
+    const hipError_t q = hipEventQuery(ix->ev_stop);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) return fail(GORIO_EDEVICE, "queue search failed: %s", hipGetErrorString(q));
+    const double el = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    if (!timed_out && el > limit_s) {
+      timed_out = true;
+      __atomic_store_n(P.h_abort, 1u, __ATOMIC_RELEASE);
+    }
+    std::this_thread::sleep_for(std::chrono::microseconds(200));
+  }
+  return GORIO_OK;
+}
+
 // Paged search: reset the per-search rings and counters, fill in the kernel
 // parameters, arm the proxy, then run either the persistent kernel (GPU
 // scheduler, split-phase or blocking) or host-scheduled lanes, under a
@@ -829,8 +920,10 @@ gorio_status run_host_rounds(gorio_index *ix, PagedParams &pp, uint32_t lanes, c
 gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s, bool &timed_out) {
   PagedState &P = *ix->paged;
   const bool host_rounds = ix->blocking == 2;
+  const bool gpu_queue = ix->blocking == 3;
   const bool blocking = ix->blocking == 1;
-  const uint32_t oversub = (blocking || host_rounds) ? 1u : ix->oversub;
+  const bool lanes_mode = host_rounds || gpu_queue;  // query state in HBM, turns run by executors
+  const uint32_t oversub = (blocking || lanes_mode) ? 1u : ix->oversub;
   int dev = 0, cus = 0;
   HIP_OR_FAIL(hipGetDevice(&dev));
   HIP_OR_FAIL(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
@@ -840,14 +933,14 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   const uint32_t max_pending = (uint32_t)std::max(1, std::min(256, env_int("GORIO_MAX_PENDING", (int)pend_dflt)));
   const uint64_t q_cache = std::max<uint64_t>(1, P.slots / (2ull * max_pending));
   const uint64_t wave_cap = ix->query_waves ? ix->query_waves : (uint64_t)cus * 8;
-  const uint64_t q_live = std::min<uint64_t>({wave_cap * oversub, q_cache, rp.nq, host_rounds ? 8192ull : ~0ull});
+  const uint64_t q_live = std::min<uint64_t>({wave_cap * oversub, q_cache, rp.nq, lanes_mode ? 8192ull : ~0ull});
   // persistent kernel: query waves; host rounds: lanes
   const int qwaves = (int)std::max<uint64_t>(1, (q_live + oversub - 1) / oversub);
   // waves that only copy arriving pages, each from a completion ring of its
   // own, so the fill rate does not depend on how many queries run at once
   // and no two waves contend for completions (host rounds need them)
   int fwaves = std::max(0, std::min((int)PagedState::kMaxRings, env_int("GORIO_FILL_WAVES", 32)));
-  if (host_rounds) fwaves = std::max(fwaves, 1);
+  if (lanes_mode) fwaves = std::max(fwaves, 1);
   const uint32_t rings = (uint32_t)std::max(1, fwaves);
   const uint64_t ht_entries = (uint64_t)qwaves * oversub << kPagedHtLog2;
   if (ht_entries > P.ht_pool_entries) {
@@ -939,6 +1032,8 @@ gorio_status run_paged(gorio_index *ix, const ResidentParams &rp, hipStream_t s,
   gorio_status st = GORIO_OK;
   if (host_rounds) {
     st = run_host_rounds(ix, pp, (uint32_t)q_live, order, s, limit_s, timed_out);
+  } else if (gpu_queue) {
+    st = run_gpu_queue(ix, pp, (uint32_t)q_live, s, limit_s, timed_out);
   } else {
     const int grid = qwaves + fwaves;
     HIP_OR_FAIL(hipEventRecord(ix->ev_start, s));

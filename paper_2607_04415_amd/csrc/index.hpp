@@ -75,6 +75,12 @@ struct PagedState {
   unsigned long long *h_runq = nullptr, *d_runq = nullptr;
   uint32_t runq_cap = 0;
   unsigned long long *h_runq_ctl = nullptr, *d_runq_ctl = nullptr;
+  // GPU resume queue: waiter sets, run queue, its counters and the lanes'
+  // states in one device buffer, and the lanes' reports in HBM
+  unsigned long long *d_queue = nullptr;
+  uint64_t queue_words = 0;
+  LaneOut *d_lane_out_q = nullptr;
+  uint32_t lane_out_q_cap = 0;
   Proxy proxy;
 
   enum Ctrl {
@@ -100,6 +106,8 @@ struct PagedState {
     if (h_fill_head) (void)hipHostFree(h_fill_head);
     if (h_runq) (void)hipHostFree(h_runq);
     if (h_runq_ctl) (void)hipHostFree(h_runq_ctl);
+    if (d_queue) (void)hipFree(d_queue);
+    if (d_lane_out_q) (void)hipFree(d_lane_out_q);
     if (fill_stream) (void)hipStreamDestroy(fill_stream);
     for (hipStream_t &r : round_stream)
       if (r) (void)hipStreamDestroy(r);
@@ -124,6 +132,10 @@ struct PagedState {
     h_runq = d_runq = nullptr;
     runq_cap = 0;
     h_runq_ctl = d_runq_ctl = nullptr;
+    d_queue = nullptr;
+    queue_words = 0;
+    d_lane_out_q = nullptr;
+    lane_out_q_cap = 0;
     fill_stream = nullptr;
     for (int i = 0; i < kMaxFlights; ++i) {
       round_stream[i] = nullptr;

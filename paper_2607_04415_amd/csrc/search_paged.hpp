@@ -98,6 +98,64 @@ __device__ __forceinline__ bool aborted(const PagedParams &p) {
   return __hip_atomic_load(p.abort_seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
 }
 
+// GPU resume queue (Fig. 1's ready table feeding a resume queue, with nothing
+// on the host): lanes keep their query state in HBM as in the host-scheduled
+// mode; a lane that parks sets its bit in the waiter set of every cache slot
+// it waits for, the fill wave that makes a slot READY takes the slot's waiter
+// set and queues those lanes, and executor waves run the queued lanes' turns.
+// No wake is lost: the lane sets its bits, fences, then looks at the slots
+// again (and queues itself if one is READY), while the fill wave marks the
+// slot READY, fences, then takes the waiter set.  A lane is queued at most
+// once at a time (its state word goes PARKED -> QUEUED by one CAS), so the run
+// queue never holds more than `lanes` entries.  A wake that finds the lane's
+// pages not ready after all costs one turn that parks it again.
+enum : uint32_t { kLsRunning = 0, kLsParked = 1, kLsQueued = 2 };
+struct QueueParams {
+  uint32_t lanes;
+  uint32_t words;                 // 64-bit words of one waiter set (ceil(lanes / 64))
+  unsigned long long *waiters;    // per cache slot: the lanes parked on its page (slots x words)
+  uint32_t *lane_st;              // per lane: kLsRunning, kLsParked or kLsQueued
+  unsigned long long *rq;         // run queue: lane + 1 per entry, 0 = free
+  uint32_t rq_mask;               // capacity - 1 (capacity >= 2 x lanes, a power of two)
+  unsigned long long *rq_head;    // entries taken
+  unsigned long long *rq_tail;    // entries reserved
+  unsigned int *next_lane;        // lanes handed their first query so far
+};
+
+__device__ __forceinline__ bool queue_done(const PagedParams &p) {
+  return aborted(p) || __hip_atomic_load(p.done_queries, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.nq;
+}
+
+// Append `lane` (one calling lane of a wave).  The entry's previous occupant
+// was taken by the time the ring has come round to it, except for a reader
+// that claimed it and has not cleared it yet: wait for that.
+__device__ __forceinline__ void queue_push(const PagedParams &p, const QueueParams &q, uint32_t lane) {
+  const unsigned long long t = atomicAdd(q.rq_tail, 1ull);
+  unsigned long long *e = &q.rq[t & q.rq_mask];
+  while (__hip_atomic_load(e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull && !queue_done(p))
+    __builtin_amdgcn_s_sleep(1);
+  __hip_atomic_store(e, (unsigned long long)lane + 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The fill of n slots (lane i < n: slot (uint32_t)e) is complete: queue the
+// lanes parked on them.
+__device__ __forceinline__ void wake_filled(const PagedParams &p, const QueueParams &q, unsigned long long e,
+                                            uint32_t n) {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");  // READY before the waiter sets are taken
+  const uint32_t slot = (uint32_t)e;
+  if ((uint32_t)lane_id() >= n || slot >= p.cache.slots) return;
+  for (uint32_t w = 0; w < q.words; ++w) {
+    unsigned long long bits = atomicExch(&q.waiters[(uint64_t)slot * q.words + w], 0ull);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the lanes' PARKED states are seen
+    while (bits) {
+      const uint32_t lane = w * 64u + (uint32_t)__builtin_ctzll(bits);
+      bits &= bits - 1;
+      if (lane < q.lanes && atomicCAS(&q.lane_st[lane], (uint32_t)kLsParked, (uint32_t)kLsQueued) == kLsParked)
+        queue_push(p, q, lane);
+    }
+  }
+}
+
 // Byte offsets of node v's vector and adjacency block inside cache slot s.
 template <bool N2S>
 __device__ __forceinline__ uint32_t cached_vec(const PagedParams &p, uint32_t s, uint32_t v) {
@@ -525,7 +583,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
 // host launches the fill waves again, and they go on from the ring position
 // they published, so no kernel of that mode ever waits for another stream's
 // work).  Wave 0 also mirrors the host abort flag.
-__device__ void fill_loop(const PagedParams &p, uint32_t k) {
+__device__ void fill_loop(const PagedParams &p, uint32_t k, const QueueParams *wake = nullptr) {
   const int l = lane_id();
   const unsigned long long *ring = p.cq + (uint64_t)k * (p.cq_mask + 1);
   const unsigned long long *tail = p.cq_tail + (uint64_t)k * p.tail_stride;
@@ -555,6 +613,7 @@ __device__ void fill_loop(const PagedParams &p, uint32_t k) {
       unsigned long long e;
       const uint32_t good = load_completions(p, ring, head, n, e);
       fill_entries(p, e, good);
+      if (wake) wake_filled(p, *wake, e, good);
       served += good;
       head += good < n ? good + 1 : n;  // step over a malformed entry
     }
@@ -865,6 +924,110 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
     // its last turn, which released them before its report
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     lane_turn<KPL, M, N2S>(p, r, lane, q1 ? q1 - 1u : kNone, lds, qbuf);
+  }
+}
+
+// GPU resume queue: blocks [0, fill_waves) fill pages and queue the lanes
+// parked on them; the others are executors.  An executor takes a queued lane
+// (or, while there are lanes that never ran, hands the next lane the next
+// query), runs its turn, and acts on the lane's report: a finished lane takes
+// the next query at once, a lane that can go on is queued again, and a lane
+// that waits for pages parks on their slots.  Every wait ends when every
+// query is done or on abort.
+template <int KPL, class M, bool N2S>
+__global__ __launch_bounds__(kWave) void paged_queue(PagedParams p, RoundParams r, QueueParams q) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
+  if (blockIdx.x < p.fill_waves) {
+    fill_loop(p, blockIdx.x, &q);
+    return;
+  }
+  const int l = lane_id();
+  uint32_t idle = 0;
+  while (!queue_done(p)) {
+    // a queued lane, else a lane that has not run yet
+    uint32_t lane = kNone, qa = kNone;
+    if (l == 0) {
+      const unsigned long long h = __hip_atomic_load(q.rq_head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const unsigned long long t = __hip_atomic_load(q.rq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (h < t && atomicCAS(q.rq_head, h, h + 1) == h) {
+        unsigned long long *e = &q.rq[h & q.rq_mask];
+        unsigned long long v = 0;
+        while ((v = __hip_atomic_load(e, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)) == 0ull && !queue_done(p))
+          __builtin_amdgcn_s_sleep(1);
+        if (v != 0ull) {
+          __hip_atomic_store(e, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          lane = (uint32_t)(v - 1ull);
+        }
+      } else if (__hip_atomic_load(q.next_lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < q.lanes) {
+        const uint32_t nl = atomicAdd(q.next_lane, 1u);
+        if (nl < q.lanes) {
+          const uint32_t qi = atomicAdd(p.next_query, 1u);
+          if (qi < p.nq) {
+            lane = nl;
+            qa = p.order ? p.order[qi] : qi;
+          }
+        }
+      }
+    }
+    lane = first_lane_value(lane);
+    qa = first_lane_value(qa);
+    if (lane == kNone || lane >= q.lanes) {
+      if (++idle > 8) __builtin_amdgcn_s_sleep(2);
+      continue;
+    }
+    idle = 0;
+    if (l == 0) __hip_atomic_store(&q.lane_st[lane], (uint32_t)kLsRunning, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the lane's state and visited table were written by the wave that ran
+    // its last turn, released before the lane was queued
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    for (;;) {
+      lane_turn<KPL, M, N2S>(p, r, lane, qa, lds, qbuf);
+      // the report (written by several lanes of this wave) is complete and read from L2
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      __syncthreads();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      const LaneOut &o = r.out[lane];
+      const uint32_t code = o.code;
+      if (code == kLaneDone) {
+        uint32_t qi = 0;
+        if (l == 0) qi = atomicAdd(p.next_query, 1u);
+        qi = first_lane_value(qi);
+        if (qi >= p.nq) break;  // the lane retires
+        qa = p.order ? p.order[qi] : qi;
+        continue;
+      }
+      if (aborted(p)) break;
+      const uint32_t nw = min(o.nwait, kLaneWaitCap);
+      if (code == kLaneYield || o.retry || nw == 0) {
+        // it can go on without a page arriving (or could not report them all)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        if (l == 0) {
+          __hip_atomic_store(&q.lane_st[lane], (uint32_t)kLsQueued, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          queue_push(p, q, lane);
+        }
+        break;
+      }
+      // park: PARKED, then the bits, then a second look at the slots
+      if (l == 0) __hip_atomic_store(&q.lane_st[lane], (uint32_t)kLsParked, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      const uint64_t bit = 1ull << (lane & 63u);
+      const uint32_t word = lane >> 6;
+      for (uint32_t j = l; j < nw; j += kWave) {
+        const uint32_t sl = o.wait[j];
+        if (sl < p.cache.slots) atomicOr(&q.waiters[(uint64_t)sl * q.words + word], (unsigned long long)bit);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
+      bool ready = false;
+      for (uint32_t j = l; j < nw; j += kWave) {
+        const uint32_t sl = o.wait[j];
+        ready |= sl < p.cache.slots && slot_ready(p.cache, sl);
+      }
+      if (ballot(ready) != 0 && l == 0 &&
+          atomicCAS(&q.lane_st[lane], (uint32_t)kLsParked, (uint32_t)kLsQueued) == kLsParked)
+        queue_push(p, q, lane);
+      break;
+    }
   }
 }
 

@@ -230,7 +230,7 @@ def test_scheduler_rejects(torch_dev, small):
             ix.set_scheduler(**kw)
         assert e.value.status == g.EINVAL
     with pytest.raises(g.GorioError) as e:
-        ix.set_backing(mode=3)
+        ix.set_backing(mode=4)                           # modes are 0..3
     assert e.value.status == g.EINVAL
     ix.close()
 
