@@ -302,15 +302,16 @@ def test_paged_f32_generic_dims(orc, torch_dev):
     assert_same(gi, gd, oids, od)
 
 
-RANDOM_CONFIGS = 16
+RANDOM_CONFIGS = 22
+QUEUE_FROM = 16      # seeds from here on run the GPU resume queue
 
 
 @pytest.mark.parametrize("seed", range(RANDOM_CONFIGS))
 def test_paged_random_configuration(orc, torch_dev, monkeypatch, seed):
     """Seeded random configurations of the whole paged path: dtype, sizes,
     beam, page size and layout, cache size, latency, slots, scheduling mode
-    (split-phase, blocking, or host-scheduled lanes run by the executor or by
-    a launch per round)."""
+    (split-phase, blocking, host-scheduled lanes run by the executor or by
+    a launch per round, or, from seed QUEUE_FROM on, the GPU resume queue)."""
     rng = np.random.default_rng(1000 + seed)
     dtype = "u8" if rng.random() < 0.6 else "f32"
     D = int(rng.choice([4, 16, 64, 128]) if dtype == "u8" else rng.choice([7, 32, 96]))
@@ -344,9 +345,14 @@ def test_paged_random_configuration(orc, torch_dev, monkeypatch, seed):
     blocking = bool(rng.random() < 0.25)
     # host-scheduled lanes (their own stream of draws too)
     hrng = np.random.default_rng(9000 + seed)
-    host = bool(hrng.random() < 0.35)
-    mode = 2 if host else int(blocking)
+    queue = seed >= QUEUE_FROM
+    host = bool(hrng.random() < 0.35) and not queue
+    mode = 3 if queue else (2 if host else int(blocking))
     host_desc = ""
+    if queue:
+        qrng = np.random.default_rng(13000 + seed)
+        ix.set_scheduler(query_waves=int(qrng.choice([0, 1, 3, 16, 40])))
+        host_desc = " gpu resume queue"
     if host:
         executor = bool(hrng.random() < 0.6)
         passes = [None, "1", "3"][int(hrng.integers(0, 3))]
