@@ -865,7 +865,7 @@ gorio_status run_gpu_queue(gorio_index *ix, PagedParams &pp, uint32_t lanes, hip
   const uint64_t out_words = (uint64_t)lanes * sizeof(LaneOut) / 4;
   fill_u32<<<grid_for(out_words, 256), 256, 0, s>>>(reinterpret_cast<uint32_t *>(P.d_lane_out_q), out_words, 0u);
   HIP_OR_FAIL(hipGetLastError());
-  QueueParams qp;
+  RunQueue qp;
   qp.lanes = lanes;
   qp.words = wset;
   qp.waiters = P.d_queue;

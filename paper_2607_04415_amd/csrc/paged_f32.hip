@@ -14,7 +14,7 @@ hipError_t launch_rounds_f32(const PagedParams &pp, const RoundParams &rp, int g
   return detail::rounds<MetricF32<64, false>>(pp, rp, grid, s);
 }
 
-hipError_t launch_queue_f32(const PagedParams &pp, const RoundParams &rp, const QueueParams &qp, int grid,
+hipError_t launch_queue_f32(const PagedParams &pp, const RoundParams &rp, const RunQueue &qp, int grid,
                             hipStream_t s) {
   if (pp.D == 96) return detail::queue<MetricF32<24, true>>(pp, rp, qp, grid, s);
   return detail::queue<MetricF32<64, false>>(pp, rp, qp, grid, s);

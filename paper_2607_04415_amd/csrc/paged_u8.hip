@@ -20,7 +20,7 @@ hipError_t launch_rounds_u8(const PagedParams &pp, const RoundParams &rp, int gr
   return detail::rounds<MetricU8<16, false>>(pp, rp, grid, s);
 }
 
-hipError_t launch_queue_u8(const PagedParams &pp, const RoundParams &rp, const QueueParams &qp, int grid,
+hipError_t launch_queue_u8(const PagedParams &pp, const RoundParams &rp, const RunQueue &qp, int grid,
                            hipStream_t s) {
   if (pp.D == 128) return detail::queue<MetricU8<4, true>>(pp, rp, qp, grid, s);
   const uint32_t vdw = (pp.D / 4 + 7) / 8;

@@ -29,6 +29,7 @@
 #pragma once
 
 #include "metric.hpp"
+#include "resume_queue.hpp"
 
 namespace gorio {
 
@@ -100,60 +101,20 @@ __device__ __forceinline__ bool aborted(const PagedParams &p) {
 
 // GPU resume queue (Fig. 1's ready table feeding a resume queue, with nothing
 // on the host): lanes keep their query state in HBM as in the host-scheduled
-// mode; a lane that parks sets its bit in the waiter set of every cache slot
-// it waits for, the fill wave that makes a slot READY takes the slot's waiter
-// set and queues those lanes, and executor waves run the queued lanes' turns.
-// No wake is lost: the lane sets its bits, fences, then looks at the slots
-// again (and queues itself if one is READY), while the fill wave marks the
-// slot READY, fences, then takes the waiter set.  A lane is queued at most
-// once at a time (its state word goes PARKED -> QUEUED by one CAS), so the run
-// queue never holds more than `lanes` entries.  A wake that finds the lane's
-// pages not ready after all costs one turn that parks it again.
-enum : uint32_t { kLsRunning = 0, kLsParked = 1, kLsQueued = 2 };
-struct QueueParams {
-  uint32_t lanes;
-  uint32_t words;                 // 64-bit words of one waiter set (ceil(lanes / 64))
-  unsigned long long *waiters;    // per cache slot: the lanes parked on its page (slots x words)
-  uint32_t *lane_st;              // per lane: kLsRunning, kLsParked or kLsQueued
-  unsigned long long *rq;         // run queue: lane + 1 per entry, 0 = free
-  uint32_t rq_mask;               // capacity - 1 (capacity >= 2 x lanes, a power of two)
-  unsigned long long *rq_head;    // entries taken
-  unsigned long long *rq_tail;    // entries reserved
-  unsigned int *next_lane;        // lanes handed their first query so far
-};
-
+// mode, and the lane-state, waiter-set and run-queue transitions of
+// resume_queue.hpp decide which lane runs next.  Its waits end when every
+// query is done or on abort.
 __device__ __forceinline__ bool queue_done(const PagedParams &p) {
   return aborted(p) || __hip_atomic_load(p.done_queries, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= p.nq;
 }
 
-// Append `lane` (one calling lane of a wave).  The entry's previous occupant
-// was taken by the time the ring has come round to it, except for a reader
-// that claimed it and has not cleared it yet: wait for that.
-__device__ __forceinline__ void queue_push(const PagedParams &p, const QueueParams &q, uint32_t lane) {
-  const unsigned long long t = atomicAdd(q.rq_tail, 1ull);
-  unsigned long long *e = &q.rq[t & q.rq_mask];
-  while (__hip_atomic_load(e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull && !queue_done(p))
-    __builtin_amdgcn_s_sleep(1);
-  __hip_atomic_store(e, (unsigned long long)lane + 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // The fill of n slots (lane i < n: slot (uint32_t)e) is complete: queue the
 // lanes parked on them.
-__device__ __forceinline__ void wake_filled(const PagedParams &p, const QueueParams &q, unsigned long long e,
+__device__ __forceinline__ void wake_filled(const PagedParams &p, const RunQueue &q, unsigned long long e,
                                             uint32_t n) {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");  // READY before the waiter sets are taken
+  GORIO_QUEUE_FENCE_SEQ();  // READY before the waiter sets are taken
   const uint32_t slot = (uint32_t)e;
-  if ((uint32_t)lane_id() >= n || slot >= p.cache.slots) return;
-  for (uint32_t w = 0; w < q.words; ++w) {
-    unsigned long long bits = atomicExch(&q.waiters[(uint64_t)slot * q.words + w], 0ull);
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the lanes' PARKED states are seen
-    while (bits) {
-      const uint32_t lane = w * 64u + (uint32_t)__builtin_ctzll(bits);
-      bits &= bits - 1;
-      if (lane < q.lanes && atomicCAS(&q.lane_st[lane], (uint32_t)kLsParked, (uint32_t)kLsQueued) == kLsParked)
-        queue_push(p, q, lane);
-    }
-  }
+  if ((uint32_t)lane_id() < n && slot < p.cache.slots) wake_waiters(q, slot, [&]() { return queue_done(p); });
 }
 
 // Byte offsets of node v's vector and adjacency block inside cache slot s.
@@ -583,7 +544,7 @@ __device__ bool run_query(const PagedParams &p, QSlot<KPL> &S, uint32_t *ht, uin
 // host launches the fill waves again, and they go on from the ring position
 // they published, so no kernel of that mode ever waits for another stream's
 // work).  Wave 0 also mirrors the host abort flag.
-__device__ void fill_loop(const PagedParams &p, uint32_t k, const QueueParams *wake = nullptr) {
+__device__ void fill_loop(const PagedParams &p, uint32_t k, const RunQueue *wake = nullptr) {
   const int l = lane_id();
   const unsigned long long *ring = p.cq + (uint64_t)k * (p.cq_mask + 1);
   const unsigned long long *tail = p.cq_tail + (uint64_t)k * p.tail_stride;
@@ -935,7 +896,7 @@ __global__ __launch_bounds__(kWave) void paged_round(PagedParams p, RoundParams 
 // that waits for pages parks on their slots.  Every wait ends when every
 // query is done or on abort.
 template <int KPL, class M, bool N2S>
-__global__ __launch_bounds__(kWave) void paged_queue(PagedParams p, RoundParams r, QueueParams q) {
+__global__ __launch_bounds__(kWave) void paged_queue(PagedParams p, RoundParams r, RunQueue q) {
   extern __shared__ __align__(16) unsigned char lds[];
   __shared__ __align__(16) uint32_t qbuf[M::kQueryWords];
   if (blockIdx.x < p.fill_waves) {
@@ -943,25 +904,16 @@ __global__ __launch_bounds__(kWave) void paged_queue(PagedParams p, RoundParams 
     return;
   }
   const int l = lane_id();
+  auto stop = [&]() { return queue_done(p); };
   uint32_t idle = 0;
   while (!queue_done(p)) {
     // a queued lane, else a lane that has not run yet
-    uint32_t lane = kNone, qa = kNone;
+    uint32_t lane = kNoLane, qa = kNone;
     if (l == 0) {
-      const unsigned long long h = __hip_atomic_load(q.rq_head, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const unsigned long long t = __hip_atomic_load(q.rq_tail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (h < t && atomicCAS(q.rq_head, h, h + 1) == h) {
-        unsigned long long *e = &q.rq[h & q.rq_mask];
-        unsigned long long v = 0;
-        while ((v = __hip_atomic_load(e, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)) == 0ull && !queue_done(p))
-          __builtin_amdgcn_s_sleep(1);
-        if (v != 0ull) {
-          __hip_atomic_store(e, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          lane = (uint32_t)(v - 1ull);
-        }
-      } else if (__hip_atomic_load(q.next_lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < q.lanes) {
-        const uint32_t nl = atomicAdd(q.next_lane, 1u);
-        if (nl < q.lanes) {
+      lane = queue_take(q, stop);
+      if (lane == kNoLane) {
+        const uint32_t nl = take_fresh_lane(q);
+        if (nl != kNoLane) {
           const uint32_t qi = atomicAdd(p.next_query, 1u);
           if (qi < p.nq) {
             lane = nl;
@@ -972,21 +924,27 @@ __global__ __launch_bounds__(kWave) void paged_queue(PagedParams p, RoundParams 
     }
     lane = first_lane_value(lane);
     qa = first_lane_value(qa);
-    if (lane == kNone || lane >= q.lanes) {
+    if (lane >= q.lanes) {  // nothing to run (kNoLane), or not a lane
       if (++idle > 8) __builtin_amdgcn_s_sleep(2);
       continue;
     }
     idle = 0;
-    if (l == 0) __hip_atomic_store(&q.lane_st[lane], (uint32_t)kLsRunning, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (l == 0) lane_running(q, lane);
     // the lane's state and visited table were written by the wave that ran
     // its last turn, released before the lane was queued
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    GORIO_QUEUE_FENCE_ACQ();
+    if (qa == kNone) {  // resumed: leave the waiter sets of the slots it parked on
+      const LaneOut &o = r.out[lane];
+      const uint32_t nw = min(o.nwait, kLaneWaitCap);
+      const uint32_t sl = (uint32_t)l < nw ? o.wait[l] : kNone;
+      if (sl < p.cache.slots) park_withdraw(q, lane, sl);
+    }
     for (;;) {
       lane_turn<KPL, M, N2S>(p, r, lane, qa, lds, qbuf);
       // the report (written by several lanes of this wave) is complete and read from L2
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      GORIO_QUEUE_FENCE_REL();
       __syncthreads();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      GORIO_QUEUE_FENCE_ACQ();
       const LaneOut &o = r.out[lane];
       const uint32_t code = o.code;
       if (code == kLaneDone) {
@@ -1001,31 +959,23 @@ __global__ __launch_bounds__(kWave) void paged_queue(PagedParams p, RoundParams 
       const uint32_t nw = min(o.nwait, kLaneWaitCap);
       if (code == kLaneYield || o.retry || nw == 0) {
         // it can go on without a page arriving (or could not report them all)
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        if (l == 0) {
-          __hip_atomic_store(&q.lane_st[lane], (uint32_t)kLsQueued, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          queue_push(p, q, lane);
-        }
+        GORIO_QUEUE_FENCE_REL();
+        if (l == 0) requeue_lane(q, lane, stop);
         break;
       }
-      // park: PARKED, then the bits, then a second look at the slots
-      if (l == 0) __hip_atomic_store(&q.lane_st[lane], (uint32_t)kLsParked, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      const uint64_t bit = 1ull << (lane & 63u);
-      const uint32_t word = lane >> 6;
-      for (uint32_t j = l; j < nw; j += kWave) {
-        const uint32_t sl = o.wait[j];
-        if (sl < p.cache.slots) atomicOr(&q.waiters[(uint64_t)sl * q.words + word], (unsigned long long)bit);
-      }
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
-      bool ready = false;
-      for (uint32_t j = l; j < nw; j += kWave) {
-        const uint32_t sl = o.wait[j];
-        ready |= sl < p.cache.slots && slot_ready(p.cache, sl);
-      }
-      if (ballot(ready) != 0 && l == 0 &&
-          atomicCAS(&q.lane_st[lane], (uint32_t)kLsParked, (uint32_t)kLsQueued) == kLsParked)
-        queue_push(p, q, lane);
+      // park: PARKED, then the bits, then a second look at the slots.  Each
+      // lane of the wave takes its wait entry (at most one: the report holds
+      // fewer waits than a wave has lanes) before the lane can be woken: from
+      // then on another executor may run it and rewrite its report.
+      static_assert(kLaneWaitCap <= kWave, "one wait entry per lane of the wave");
+      const uint32_t sl = (uint32_t)l < nw ? o.wait[l] : kNone;
+      const bool mine = sl < p.cache.slots;
+      if (l == 0) park_begin(q, lane);
+      GORIO_QUEUE_FENCE_REL();
+      if (mine) park_wait_on(q, lane, sl);
+      GORIO_QUEUE_FENCE_SEQ();
+      const bool ready = mine && slot_ready(p.cache, sl);
+      if (ballot(ready) != 0 && l == 0) park_recheck_wake(q, lane, stop);
       break;
     }
   }
