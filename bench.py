@@ -56,8 +56,8 @@ SHAPE_C3 = {"oversub": 1, "query_waves": 30}
 # 100 / 156 (the default) lanes gave 7.0k / 7.25k / 7.2k / 7.05k / 6.6k / 6.0k queries/s
 SHAPE_HOST = {"query_waves": 40}
 # GPU resume queue (fill waves queue the lanes parked on the pages they fill, executor
-# waves run them): 20 / 30 / 40 / 60 / 100 / 156 (the default) lanes gave 6.2k / 7.0k /
-# 7.1k / 7.0k / 6.6k / 6.0k queries/s
+# waves run them): 30 / 40 / 60 lanes gave 7.0k / 7.2k / 7.1k queries/s (20 / 100 / 156,
+# the default, 6.2k / 6.6k / 6.0k before resumed lanes withdrew their other waits)
 SHAPE_QUEUE = {"query_waves": 40}
 SHAPE_C4 = {"oversub": 4, "query_waves": 30}
 SHAPE_C5 = {"oversub": 1, "query_waves": 60}
